@@ -1,0 +1,191 @@
+"""CPDP oracle: the plain CPU statement of the reconcile hot path.
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and
+``bench.py``'s CPU-baseline leg may import this package.  It shares no code
+with the HIP library (``paper_2607_21224_amd``) and never imports it.
+
+The arithmetic lives in ``cpdp_oracle.c`` (fp64, explicit rounding points);
+this module compiles it with gcc, wraps it with ctypes, and adds the host
+cadence of Sec. 3.2 / Sec. 3.1 (synchronisation indicator s_t and the forced
+synchronisation at the end of an epoch) and the Algorithm 1 driver loop.
+
+Storage types are named "f32", "bf16" or "f64" ("f64" = no rounding).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass, field
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "cpdp_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+
+_DT = {"f32": 0, "bf16": 1, "f64": 2}
+
+_D = ctypes.POINTER(ctypes.c_double)
+
+
+def build(src: str = _SRC, out: str = _LIB_PATH) -> str:
+    """Compile the oracle with gcc (IEEE double, no FMA contraction)."""
+    cmd = ["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math",
+           "-fPIC", "-shared", "-o", out, src, "-lm"]
+    subprocess.run(cmd, check=True)
+    return out
+
+
+def load(path: str = _LIB_PATH) -> ctypes.CDLL:
+    """Load a compiled oracle (building it first if nothing is built)."""
+    if not os.path.exists(path):
+        build(out=path)
+    lib = ctypes.CDLL(path)
+    i, i64, d = ctypes.c_int, ctypes.c_int64, ctypes.c_double
+    lib.oracle_round.argtypes = [i, d]
+    lib.oracle_round.restype = d
+    lib.oracle_state_init.argtypes = [i, i64, i, i, _D, _D, _D, _D, _D]
+    lib.oracle_state_init.restype = None
+    lib.oracle_local_step.argtypes = [i, i64, i, i, _D, _D, _D, d, d]
+    lib.oracle_local_step.restype = None
+    lib.oracle_reconcile.argtypes = [i, i64, i, i, i, _D, _D, _D, _D, _D,
+                                     d, d, d, d]
+    lib.oracle_reconcile.restype = None
+    lib.oracle_reconcile_vform.argtypes = [i, i64, i, i, i, _D, _D, _D, _D,
+                                           _D, d, d, d]
+    lib.oracle_reconcile_vform.restype = None
+    return lib
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        _lib = load()
+    return _lib
+
+
+def _ptr(a: np.ndarray):
+    assert a.dtype == np.float64 and a.flags["C_CONTIGUOUS"]
+    return a.ctypes.data_as(_D)
+
+
+@dataclass
+class OracleState:
+    """State of Algorithm 1 for W workers over P coordinates (all float64).
+
+    params, mom: (W, P); slow: (P,) holds u (u-form) or v (v-form);
+    anchor: (P,) is the reference model theta_ref.
+    """
+    W: int
+    P: int
+    params: np.ndarray
+    mom: np.ndarray
+    slow: np.ndarray
+    anchor: np.ndarray
+    param_dt: str = "f32"
+    mom_dt: str = "f32"
+    aux_dt: str = "f32"
+    lib: ctypes.CDLL | None = field(default=None, repr=False)
+
+    def copy(self) -> "OracleState":
+        return OracleState(self.W, self.P, self.params.copy(), self.mom.copy(),
+                           self.slow.copy(), self.anchor.copy(), self.param_dt,
+                           self.mom_dt, self.aux_dt, self.lib)
+
+    @property
+    def _l(self):
+        return self.lib if self.lib is not None else lib()
+
+
+def round_to(dt: str, x: float, use=None) -> float:
+    return (use or lib()).oracle_round(_DT[dt], float(x))
+
+
+def state_init(theta0, W: int, param_dt="f32", mom_dt="f32", aux_dt="f32",
+               use=None) -> OracleState:
+    """Algorithm 1 initialisation from theta0 (shape (P,))."""
+    theta0 = np.ascontiguousarray(theta0, dtype=np.float64)
+    P = theta0.shape[0]
+    st = OracleState(W, P, np.empty((W, P)), np.empty((W, P)), np.empty(P),
+                     np.empty(P), param_dt, mom_dt, aux_dt, use)
+    st._l.oracle_state_init(W, P, _DT[param_dt], _DT[aux_dt], _ptr(theta0),
+                            _ptr(st.params), _ptr(st.mom), _ptr(st.slow),
+                            _ptr(st.anchor))
+    return st
+
+
+def _grads(st: OracleState, grads) -> np.ndarray:
+    g = np.ascontiguousarray(grads, dtype=np.float64)
+    assert g.shape == (st.W, st.P), (g.shape, st.W, st.P)
+    return g
+
+
+def local_step(st: OracleState, grads, lr: float, mu: float) -> None:
+    """Local update phase (s_t = 0), in place."""
+    g = _grads(st, grads)
+    st._l.oracle_local_step(st.W, st.P, _DT[st.param_dt], _DT[st.mom_dt],
+                            _ptr(st.params), _ptr(st.mom), _ptr(g),
+                            float(lr), float(mu))
+
+
+def reconcile(st: OracleState, grads, lr: float, mu: float, beta: float,
+              alpha: float) -> None:
+    """Synchronization phase (s_t = 1), u-form SlowMo, in place."""
+    g = _grads(st, grads)
+    st._l.oracle_reconcile(st.W, st.P, _DT[st.param_dt], _DT[st.mom_dt],
+                           _DT[st.aux_dt], _ptr(st.params), _ptr(st.mom),
+                           _ptr(g), _ptr(st.slow), _ptr(st.anchor), float(lr),
+                           float(mu), float(beta), float(alpha))
+
+
+def reconcile_vform(st: OracleState, grads, lr: float, mu: float,
+                    beta: float) -> None:
+    """Synchronization phase in the paper's v variables (st.slow holds v)."""
+    g = _grads(st, grads)
+    st._l.oracle_reconcile_vform(st.W, st.P, _DT[st.param_dt],
+                                 _DT[st.mom_dt], _DT[st.aux_dt],
+                                 _ptr(st.params), _ptr(st.mom), _ptr(g),
+                                 _ptr(st.slow), _ptr(st.anchor), float(lr),
+                                 float(mu), float(beta))
+
+
+def is_sync_step(t: int, K: int, T: int = 0) -> bool:
+    """Synchronisation indicator.
+
+    Sec. 3.2: s_t = 1 iff t mod K = 0, with t the 1-based step counter inside
+    an epoch.  Sec. 3.1 / Sec. 4.2: when the epoch length T is not a multiple
+    of K, its last step is also a synchronisation boundary.  T = 0 means the
+    run has no epoch boundary.
+    """
+    if K < 1 or t < 1 or T < 0 or (T > 0 and t > T):
+        raise ValueError("need K >= 1, t >= 1, T >= 0 and t <= T when T > 0")
+    return t % K == 0 or (T > 0 and t == T)
+
+
+def run(theta0, grad_fn, W: int, K: int, n_steps: int, lr: float, mu: float,
+        beta: float, alpha: float, T: int = 0, param_dt="f32", mom_dt="f32",
+        aux_dt="f32", callback=None, use=None) -> OracleState:
+    """Algorithm 1 driven for n_steps steps.
+
+    grad_fn(step, W, P) returns the (W, P) gradients of 1-based global step
+    ``step`` (the stand-in for the backward pass).  With T > 0 the within-epoch
+    step counter restarts every T steps.  callback(step, kind, state) is called
+    after every step with kind "local" or "reconcile".
+    """
+    st = state_init(theta0, W, param_dt, mom_dt, aux_dt, use)
+    for step in range(1, n_steps + 1):
+        t = ((step - 1) % T) + 1 if T > 0 else step
+        g = grad_fn(step, W, st.P)
+        if is_sync_step(t, K, T):
+            reconcile(st, g, lr, mu, beta, alpha)
+            kind = "reconcile"
+        else:
+            local_step(st, g, lr, mu)
+            kind = "local"
+        if callback is not None:
+            callback(step, kind, st)
+    return st

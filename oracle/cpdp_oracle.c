@@ -1,0 +1,193 @@
+/*
+ * CPDP oracle: plain, slow CPU reference for the reconcile hot path.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing on the product path may link, load or
+ * call this file; only the test suite, the smoke check and the benchmark's
+ * CPU-baseline leg do.  It shares no code, header or constant with the HIP
+ * library: it is a second, independent statement of the method.
+ *
+ * What it computes (Controlled Periodic Data Parallelism with SlowMo):
+ *   - initialisation            Algorithm 1 (CPDP with SlowMo), the two
+ *                               "Initialize" statements: every worker starts
+ *                               from the same parameters, velocity 0,
+ *                               reference model = initial parameters.
+ *   - local update phase        Sec. 3.2, Eq. (local_update), executed as the
+ *                               framework optimizer does it (Sec. 4.2): SGD
+ *                               with a per-worker momentum buffer
+ *                               (buf <- mu*buf + g; theta <- theta - lr*buf).
+ *                               mu = 0 gives Eq. (local_update) exactly.
+ *   - synchronization phase     Sec. 3.2 stages 1-2, Sec. 3.3 Eqs. (Delta, v,
+ *                               theta_new, broadcast, reference update),
+ *                               in the execution order fixed by Sec. 4.2:
+ *                               gradient mean -> optimizer step with the mean
+ *                               gradient (momentum buffers stay local) ->
+ *                               parameter mean -> SlowMo -> copy back.
+ *   - SlowMo, u-form            u <- beta*u + (ref - avg)/lr,
+ *                               new = ref - alpha*lr*u.  With v = -lr*u,
+ *                               alpha = 1 and a constant lr this is exactly
+ *                               the paper's v <- beta*v + (avg - ref),
+ *                               new = ref + v (Sec. 3.3); the v-form is also
+ *                               provided (oracle_reconcile_vform).
+ *
+ * Arithmetic: every value is held in a double.  Stored tensors are rounded to
+ * their storage type exactly where the framework implementation writes a
+ * tensor (parameters after the optimizer step, momentum buffers, the fp32
+ * mean gradient, SlowMo state, reference model).  Rounding is
+ * round-to-nearest-even; bf16 rounds the fp32 value (two-step), the way a
+ * device holding fp32 intermediates stores bf16.  A storage type of "f64"
+ * disables rounding for that family, which turns the oracle into an exact-
+ * arithmetic statement of the algorithm (used against rational brute force).
+ *
+ * Layout: replica i of a per-replica family occupies [i*P, (i+1)*P).  Every
+ * coordinate is independent of every other, so any subset of coordinates can
+ * be run on its own.
+ *
+ * Pins (tests check this file against): a hand-derived worked example of
+ * Algorithm 1, exact rational brute force, closed forms for constant
+ * gradients, reductions to PyTorch's SGD (K = 1 and W = 1), replica-permutation
+ * invariance, fixed points, Table 2's synchronisation counts, and a mutation
+ * test that plants mistakes in a copy of this file.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+/* storage types understood by the oracle (its own numbering) */
+#define ORACLE_F32 0
+#define ORACLE_BF16 1
+#define ORACLE_F64 2
+
+static double round_to_f32(double x) { return (double)(float)x; }
+
+/* bf16 = upper half of an fp32 bit pattern, rounded to nearest, ties to even */
+static double round_to_bf16(double x) {
+    float f = (float)x;
+    if (isnan(f)) return (double)f;
+    uint32_t b;
+    memcpy(&b, &f, sizeof b);
+    uint32_t lsb = (b >> 16) & 1u;
+    b = (b + 0x7FFFu + lsb) & 0xFFFF0000u;
+    memcpy(&f, &b, sizeof f);
+    return (double)f;
+}
+
+static double store_as(int dt, double x) {
+    if (dt == ORACLE_F32) return round_to_f32(x);
+    if (dt == ORACLE_BF16) return round_to_bf16(x);
+    return x;
+}
+
+/* exported so the tests can check the rounding against library conversions */
+double oracle_round(int dt, double x) { return store_as(dt, x); }
+
+/*
+ * Algorithm 1, initialisation: theta_i <- theta for every worker, SlowMo
+ * state <- 0, reference model <- theta.  theta0 is taken as the parameter
+ * storage type holds it; the reference model keeps that representable value.
+ */
+void oracle_state_init(int W, int64_t P, int param_dt, int aux_dt,
+                       const double* theta0, double* params, double* mom,
+                       double* slow, double* anchor) {
+    for (int64_t p = 0; p < P; ++p) {
+        double th = store_as(param_dt, theta0[p]);
+        for (int i = 0; i < W; ++i) {
+            params[(int64_t)i * P + p] = th;
+            mom[(int64_t)i * P + p] = 0.0;
+        }
+        slow[p] = 0.0;
+        anchor[p] = store_as(aux_dt, th);
+    }
+}
+
+/*
+ * Local update phase (s_t = 0): each worker steps on its own gradient with
+ * its own momentum buffer; no communication.
+ */
+void oracle_local_step(int W, int64_t P, int param_dt, int mom_dt,
+                       double* params, double* mom, const double* grads,
+                       double lr, double mu) {
+    for (int i = 0; i < W; ++i) {
+        for (int64_t p = 0; p < P; ++p) {
+            int64_t k = (int64_t)i * P + p;
+            double buf = store_as(mom_dt, mu * mom[k] + grads[k]);
+            mom[k] = buf;
+            params[k] = store_as(param_dt, params[k] - lr * buf);
+        }
+    }
+}
+
+/*
+ * Synchronization phase (s_t = 1), u-form SlowMo.
+ *   1. gbar = (1/W) sum_i g_i                     (stored in fp32 like .grad)
+ *   2. buf_i <- mu*buf_i + gbar; x_i = theta_i - lr*buf_i   (optimizer step)
+ *   3. avg = (1/W) sum_i x_i                      (parameter average)
+ *   4. u <- beta*u + (ref - avg)/lr
+ *   5. new = ref - alpha*lr*u
+ *   6. theta_i <- new for all i; ref <- new       (momentum buffers untouched)
+ */
+void oracle_reconcile(int W, int64_t P, int param_dt, int mom_dt, int aux_dt,
+                      double* params, double* mom, const double* grads,
+                      double* slow, double* anchor,
+                      double lr, double mu, double beta, double alpha) {
+    for (int64_t p = 0; p < P; ++p) {
+        double gsum = 0.0;
+        for (int i = 0; i < W; ++i) gsum += grads[(int64_t)i * P + p];
+        double gbar = store_as(aux_dt, gsum / (double)W);
+
+        double xsum = 0.0;
+        for (int i = 0; i < W; ++i) {
+            int64_t k = (int64_t)i * P + p;
+            double buf = store_as(mom_dt, mu * mom[k] + gbar);
+            mom[k] = buf;
+            double x = store_as(param_dt, params[k] - lr * buf);
+            xsum += x;
+        }
+        double avg = xsum / (double)W;
+
+        double ref = anchor[p];
+        double u = store_as(aux_dt, beta * slow[p] + (ref - avg) / lr);
+        double fresh = store_as(aux_dt, ref - alpha * lr * u);
+
+        slow[p] = u;
+        anchor[p] = fresh;
+        for (int i = 0; i < W; ++i)
+            params[(int64_t)i * P + p] = store_as(param_dt, fresh);
+    }
+}
+
+/*
+ * Synchronization phase in the paper's own variables (Sec. 3.3):
+ *   Delta = avg - ref;  v <- beta*v + Delta;  new = ref + v;
+ *   theta_i <- new;  ref <- new.
+ * Stages 1-3 are the same as in oracle_reconcile.
+ */
+void oracle_reconcile_vform(int W, int64_t P, int param_dt, int mom_dt,
+                            int aux_dt, double* params, double* mom,
+                            const double* grads, double* velocity,
+                            double* anchor, double lr, double mu,
+                            double beta) {
+    for (int64_t p = 0; p < P; ++p) {
+        double gsum = 0.0;
+        for (int i = 0; i < W; ++i) gsum += grads[(int64_t)i * P + p];
+        double gbar = store_as(aux_dt, gsum / (double)W);
+
+        double xsum = 0.0;
+        for (int i = 0; i < W; ++i) {
+            int64_t k = (int64_t)i * P + p;
+            double buf = store_as(mom_dt, mu * mom[k] + gbar);
+            mom[k] = buf;
+            xsum += store_as(param_dt, params[k] - lr * buf);
+        }
+        double avg = xsum / (double)W;
+
+        double ref = anchor[p];
+        double delta = avg - ref;
+        double v = store_as(aux_dt, beta * velocity[p] + delta);
+        double fresh = store_as(aux_dt, ref + v);
+
+        velocity[p] = v;
+        anchor[p] = fresh;
+        for (int i = 0; i < W; ++i)
+            params[(int64_t)i * P + p] = store_as(param_dt, fresh);
+    }
+}

@@ -1,0 +1,324 @@
+"""Pins for the CPDP oracle: checks against things other than the oracle itself.
+
+Each ``pin_*`` function takes ``use`` (a loaded oracle library, or None for the
+default build) and raises AssertionError when the oracle disagrees with what
+the paper or the mathematics fixes.  ``tests/test_oracle_pins.py`` runs them on
+the real oracle; ``tests/test_oracle_mutants.py`` runs them on copies of the
+oracle with planted mistakes and requires every mistake to be caught.
+"""
+from __future__ import annotations
+
+import json
+import os
+from fractions import Fraction
+
+import numpy as np
+
+import oracle
+from brute_cpdp import run_exact
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _close(a, b, rtol, atol, what):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    ok = np.abs(a - b) <= atol + rtol * np.abs(b)
+    assert ok.all(), f"{what}: got {a[~ok][:4]} want {b[~ok][:4]}"
+
+
+def pin_worked_example(use=None):
+    """Hand-derived trajectory of Algorithm 1 (tests/golden), exact arithmetic."""
+    fx = json.load(open(os.path.join(GOLDEN, "worked_example_w2_k2.json")))
+    s = fx["setup"]
+    grads = [np.array(g, dtype=np.float64) for g in fx["grads"]]
+    snaps = {}
+
+    def cb(step, kind, st):
+        snaps[step] = (kind, st.copy())
+
+    oracle.run(s["theta0"], lambda step, W, P: grads[step - 1], s["W"], s["K"],
+               len(grads), s["lr"], s["mu"], s["beta"], s["alpha"],
+               param_dt="f64", mom_dt="f64", aux_dt="f64", callback=cb, use=use)
+    for e in fx["expected"]:
+        kind, st = snaps[e["step"]]
+        assert kind == e["kind"], (e["step"], kind)
+        _close(st.mom[:, 0], e["mom"], 1e-12, 1e-12, f"mom step {e['step']}")
+        _close(st.params[:, 0], e["params"], 1e-12, 1e-12,
+               f"params step {e['step']}")
+        _close(st.slow[0], e["u"], 1e-12, 1e-12, f"u step {e['step']}")
+        _close(st.anchor[0], e["anchor"], 1e-12, 1e-12,
+               f"anchor step {e['step']}")
+
+
+def pin_worked_example_vform(use=None):
+    """Same example through the paper's v variables (Sec. 3.3)."""
+    fx = json.load(open(os.path.join(GOLDEN, "worked_example_w2_k2.json")))
+    s = fx["setup"]
+    st = oracle.state_init(s["theta0"], s["W"], "f64", "f64", "f64", use=use)
+    for e, g in zip(fx["expected"], fx["grads"]):
+        g = np.array(g, dtype=np.float64)
+        if e["kind"] == "local":
+            oracle.local_step(st, g, s["lr"], s["mu"])
+        else:
+            oracle.reconcile_vform(st, g, s["lr"], s["mu"], s["beta"])
+        _close(st.slow[0], e["v"], 1e-12, 1e-12, f"v step {e['step']}")
+        _close(st.anchor[0], e["anchor"], 1e-12, 1e-12,
+               f"vform anchor step {e['step']}")
+        _close(st.params[:, 0], e["params"], 1e-12, 1e-12,
+               f"vform params step {e['step']}")
+
+
+def _rand_dyadic(rng, shape, scale=8):
+    return rng.integers(-4 * scale, 4 * scale + 1, size=shape) / scale
+
+
+def pin_brute_force(use=None, cases=12, seed=5):
+    """Exact rational Algorithm 1 (tests/brute_cpdp.py) on tiny random inputs."""
+    rng = np.random.default_rng(seed)
+    for c in range(cases):
+        W = int(rng.integers(1, 6))
+        P = int(rng.integers(1, 9))
+        K = int(rng.integers(1, 5))
+        T = int(rng.choice([0, 0, 5, 7]))
+        n = int(rng.integers(K, 3 * K + 3))
+        lr = float(rng.choice([0.125, 0.25, 0.1, 0.05]))
+        mu = float(rng.choice([0.0, 0.5, 0.9, 0.75]))
+        beta = float(rng.choice([0.0, 0.5, 0.3, 0.875]))
+        alpha = float(rng.choice([1.0, 1.0, 0.5, 1.5]))
+        theta0 = _rand_dyadic(rng, P)
+        grads = [_rand_dyadic(rng, (W, P)) for _ in range(n)]
+        exact = run_exact([Fraction(x) for x in theta0],
+                          [[[Fraction(x) for x in r] for r in g] for g in grads],
+                          W, K, Fraction(lr), Fraction(mu), Fraction(beta),
+                          Fraction(alpha), T=T)
+        snaps = []
+        oracle.run(theta0, lambda step, W_, P_: grads[step - 1], W, K, n, lr,
+                   mu, beta, alpha, T=T, param_dt="f64", mom_dt="f64",
+                   aux_dt="f64", use=use,
+                   callback=lambda step, kind, st: snaps.append((kind, st.copy())))
+        for s, ((kind, st), ex) in enumerate(zip(snaps, exact)):
+            tag = f"case {c} step {s + 1} (W={W} P={P} K={K} T={T})"
+            assert kind == ex["kind"], tag
+            _close(st.params, [[float(x) for x in r] for r in ex["params"]],
+                   1e-12, 1e-12, tag + " params")
+            _close(st.mom, [[float(x) for x in r] for r in ex["mom"]], 1e-12,
+                   1e-12, tag + " mom")
+            _close(st.anchor, [float(x) for x in ex["ref"]], 1e-12, 1e-12,
+                   tag + " anchor")
+            # u-form state: v = -lr * u  (alpha does not enter v's recursion)
+            _close(-lr * st.slow,
+                   [float(x) for x in ex["v"]], 1e-12, 1e-12, tag + " u")
+
+
+def pin_closed_form_slowmo(use=None):
+    """Constant gradient c on every worker and step, mu = 0.
+
+    Each period moves the average K*lr*c away from the reference, so
+    u_n = K c (1 - beta^n) / (1 - beta) and
+    ref_n = theta0 - alpha lr K c [n - beta (1 - beta^n)/(1 - beta)] / (1 - beta).
+    Within a period, after j local steps, theta = ref - j lr c.
+    """
+    for (W, K, beta, alpha, lr, c) in [(3, 4, 0.5, 1.0, 0.1, 0.7),
+                                       (2, 2, 0.3, 0.5, 0.25, -1.5),
+                                       (5, 3, 0.875, 1.5, 0.05, 2.0),
+                                       (1, 1, 0.6, 1.0, 0.1, 1.0)]:
+        theta0 = np.array([0.3, -2.0, 5.5])
+        P = theta0.size
+        periods = 6
+        rec = []
+        oracle.run(theta0, lambda s, W_, P_: np.full((W_, P_), c), W, K,
+                   periods * K, lr, 0.0, beta, alpha, param_dt="f64",
+                   mom_dt="f64", aux_dt="f64", use=use,
+                   callback=lambda s, kind, st: rec.append((s, kind, st.copy())))
+        for s, kind, st in rec:
+            n, j = divmod(s, K)
+            if j == 0:
+                u = K * c * (1 - beta ** n) / (1 - beta)
+                ref = theta0 - alpha * lr * K * c * (
+                    n - beta * (1 - beta ** n) / (1 - beta)) / (1 - beta)
+                assert kind == "reconcile"
+                _close(st.slow, np.full(P, u), 1e-12, 1e-12, f"u n={n}")
+                _close(st.anchor, ref, 1e-12, 1e-12, f"ref n={n}")
+                _close(st.params, np.tile(ref, (W, 1)), 1e-12, 1e-12,
+                       f"params n={n}")
+            else:
+                assert kind == "local"
+                ref = st.anchor
+                _close(st.params, np.tile(ref - j * lr * c, (W, 1)), 1e-12,
+                       1e-12, f"local j={j}")
+            _close(st.mom, np.full((W, P), c), 1e-12, 1e-12, "mom = c")
+
+
+def pin_closed_form_momentum(use=None):
+    """beta = 0, alpha = 1, identical workers, constant gradient c.
+
+    Averaging identical replicas is the identity and SlowMo with beta = 0,
+    alpha = 1 returns the average, so the run is heavy-ball SGD with a constant
+    gradient: buf_t = c (1 - mu^t)/(1 - mu) and
+    theta_t = theta0 - lr c [t - mu (1 - mu^t)/(1 - mu)] / (1 - mu).
+    """
+    for (W, K, mu, lr, c) in [(4, 3, 0.9, 0.1, 1.0), (2, 1, 0.5, 0.25, -3.0),
+                              (3, 5, 0.75, 0.05, 0.5)]:
+        theta0 = np.array([1.0, -0.25])
+        rec = []
+        oracle.run(theta0, lambda s, W_, P_: np.full((W_, P_), c), W, K,
+                   4 * K + 1, lr, mu, 0.0, 1.0, param_dt="f64", mom_dt="f64",
+                   aux_dt="f64", use=use,
+                   callback=lambda s, kind, st: rec.append((s, st.copy())))
+        for t, st in rec:
+            buf = c * (1 - mu ** t) / (1 - mu)
+            th = theta0 - lr * c * (t - mu * (1 - mu ** t) / (1 - mu)) / (1 - mu)
+            _close(st.mom, np.full(st.mom.shape, buf), 1e-12, 1e-12,
+                   f"buf t={t}")
+            _close(st.params, np.tile(th, (W, 1)), 1e-12, 1e-12, f"theta t={t}")
+
+
+def _torch_reference(theta0, grads, W, K, lr, mu):
+    """Sec. 4.2 implementation with beta = 0, alpha = 1, written with
+    torch.optim.SGD: per-worker optimizers, averaged gradient on sync steps,
+    then parameter averaging copied back into every worker (buffers untouched).
+    """
+    import torch
+    ps = [torch.nn.Parameter(torch.tensor(theta0, dtype=torch.float64))
+          for _ in range(W)]
+    opts = [torch.optim.SGD([p], lr=lr, momentum=mu) for p in ps]
+    out = []
+    for s, g in enumerate(grads, start=1):
+        sync = s % K == 0
+        gbar = g.mean(axis=0)
+        for i in range(W):
+            ps[i].grad = torch.tensor(gbar if sync else g[i])
+            opts[i].step()
+        if sync:
+            avg = torch.stack([p.detach() for p in ps]).mean(0)
+            for p in ps:
+                p.data.copy_(avg)
+        bufs = np.stack([
+            opts[i].state[ps[i]]["momentum_buffer"].numpy().copy()
+            if mu > 0 else (gbar if sync else g[i]) for i in range(W)])
+        out.append((np.stack([p.detach().numpy().copy() for p in ps]), bufs))
+    return out
+
+
+def pin_torch_sgd(use=None):
+    """beta = 0: the run equals per-worker torch.optim.SGD with the averaged
+    gradient on sync steps followed by parameter averaging; covers K = 1
+    (synchronous DDP, Sec. 3.1) and W = 1 (plain momentum SGD)."""
+    rng = np.random.default_rng(11)
+    for (W, K, mu, lr) in [(4, 1, 0.9, 0.1), (1, 3, 0.9, 0.1), (3, 2, 0.5, 0.2),
+                           (5, 4, 0.9, 0.05), (2, 3, 0.0, 0.1)]:
+        P = 6
+        n = 3 * K + 2
+        theta0 = rng.normal(0, 1, P)
+        grads = [rng.normal(0, 1, (W, P)) for _ in range(n)]
+        ref = _torch_reference(theta0, grads, W, K, lr, mu)
+        rec = []
+        oracle.run(theta0, lambda s, W_, P_: grads[s - 1], W, K, n, lr, mu,
+                   0.0, 1.0, param_dt="f64", mom_dt="f64", aux_dt="f64",
+                   use=use, callback=lambda s, kind, st: rec.append(st.copy()))
+        for s, (st, (p_ref, b_ref)) in enumerate(zip(rec, ref), start=1):
+            _close(st.params, p_ref, 1e-12, 1e-12, f"W={W} K={K} params s={s}")
+            _close(st.mom, b_ref, 1e-12, 1e-12, f"W={W} K={K} mom s={s}")
+
+
+def pin_permutation(use=None):
+    """Relabelling the workers permutes params/mom and leaves SlowMo state and
+    the reference model unchanged."""
+    rng = np.random.default_rng(3)
+    W, P, K, n = 5, 7, 3, 10
+    theta0 = rng.normal(0, 1, P)
+    grads = [rng.normal(0, 1, (W, P)) for _ in range(n)]
+    perm = np.array([3, 0, 4, 1, 2])
+    a = oracle.run(theta0, lambda s, W_, P_: grads[s - 1], W, K, n - 1, 0.1,
+                   0.9, 0.5, 1.0, param_dt="f64", mom_dt="f64", aux_dt="f64",
+                   use=use)
+    b = oracle.run(theta0, lambda s, W_, P_: grads[s - 1][perm], W, K, n - 1,
+                   0.1, 0.9, 0.5, 1.0, param_dt="f64", mom_dt="f64",
+                   aux_dt="f64", use=use)
+    _close(b.params, a.params[perm], 1e-13, 1e-13, "perm params")
+    _close(b.mom, a.mom[perm], 1e-13, 1e-13, "perm mom")
+    _close(b.slow, a.slow, 1e-13, 1e-13, "perm u")
+    _close(b.anchor, a.anchor, 1e-13, 1e-13, "perm anchor")
+
+
+def pin_fixed_point(use=None):
+    """Zero gradients from identical workers: nothing moves, u stays 0
+    (averaging identical replicas is the identity, Sec. 3.2)."""
+    theta0 = np.array([0.125, -3.0, 7.5, 0.0], dtype=np.float64)
+    for dt in ("f32", "f64"):
+        st = oracle.run(theta0, lambda s, W_, P_: np.zeros((W_, P_)), 4, 3, 9,
+                        0.1, 0.9, 0.7, 1.3, param_dt=dt, mom_dt=dt,
+                        aux_dt=dt, use=use)
+        assert np.array_equal(st.params, np.tile(theta0, (4, 1))), dt
+        assert np.array_equal(st.anchor, theta0), dt
+        assert not st.slow.any() and not st.mom.any(), dt
+
+
+def pin_identical_workers(use=None):
+    """W identical workers behave exactly like one worker (power-of-two W keeps
+    the means exact, so this holds bitwise in fp32 storage too)."""
+    rng = np.random.default_rng(9)
+    P, K, n = 16, 4, 12
+    theta0 = rng.normal(0, 0.02, P).astype(np.float32).astype(np.float64)
+    g1 = [rng.normal(0, 1e-3, (1, P)).astype(np.float32).astype(np.float64)
+          for _ in range(n)]
+    one = oracle.run(theta0, lambda s, W_, P_: g1[s - 1], 1, K, n, 0.1, 0.9,
+                     0.5, 1.0, use=use)
+    four = oracle.run(theta0, lambda s, W_, P_: np.repeat(g1[s - 1], 4, 0), 4,
+                      K, n, 0.1, 0.9, 0.5, 1.0, use=use)
+    assert np.array_equal(four.params, np.repeat(one.params, 4, 0))
+    assert np.array_equal(four.mom, np.repeat(one.mom, 4, 0))
+    assert np.array_equal(four.slow, one.slow)
+    assert np.array_equal(four.anchor, one.anchor)
+
+
+def pin_linearity(use=None):
+    """Gradients do not depend on theta here, so the state after any number of
+    steps is linear in (theta0, gradients): F(a + b) = F(a) + F(b)."""
+    rng = np.random.default_rng(21)
+    W, P, K, n = 3, 5, 3, 8
+    ta, tb = rng.normal(0, 1, P), rng.normal(0, 1, P)
+    ga = [rng.normal(0, 1, (W, P)) for _ in range(n)]
+    gb = [rng.normal(0, 1, (W, P)) for _ in range(n)]
+
+    def go(t0, gs):
+        return oracle.run(t0, lambda s, W_, P_: gs[s - 1], W, K, n - 1, 0.1,
+                          0.9, 0.5, 0.8, param_dt="f64", mom_dt="f64",
+                          aux_dt="f64", use=use)
+
+    a, b = go(ta, ga), go(tb, gb)
+    ab = go(ta + tb, [x + y for x, y in zip(ga, gb)])
+    for name in ("params", "mom", "slow", "anchor"):
+        _close(getattr(ab, name), getattr(a, name) + getattr(b, name), 1e-11,
+               1e-11, "linearity " + name)
+
+
+def pin_rounding(use=None):
+    """Storage rounding: fp32 = IEEE round-to-nearest-even (numpy's cast);
+    bf16 = torch's float32 -> bfloat16 conversion (also nearest-even)."""
+    import torch
+    rng = np.random.default_rng(0)
+    xs = np.concatenate([rng.normal(0, 1, 2000) * 10.0 ** rng.integers(-8, 8, 2000),
+                         [0.0, -0.0, 1.0 + 2.0 ** -24, 1.0 + 2.0 ** -8,
+                          1.0 + 3 * 2.0 ** -8, 3.4e38, -3.4e38, 1e39, np.inf,
+                          -np.inf, 1e-40],
+                         # exact bf16 ties on both parities of the kept bit
+                         1.0 + (np.arange(1, 64) + 0.5) * 2.0 ** -7,
+                         -(2.0 + (np.arange(1, 64) + 0.5) * 2.0 ** -6)])
+    with np.errstate(over="ignore"):
+        f32 = xs.astype(np.float32)
+    bf = torch.from_numpy(f32).to(torch.bfloat16).to(torch.float64).numpy()
+    for x, want32, want16 in zip(xs, f32.astype(np.float64), bf):
+        got32 = oracle.round_to("f32", x, use=use)
+        got16 = oracle.round_to("bf16", x, use=use)
+        assert got32 == want32 or (np.isnan(got32) and np.isnan(want32)), x
+        assert got16 == want16 or (np.isnan(got16) and np.isnan(want16)), x
+    assert np.isnan(oracle.round_to("bf16", np.nan, use=use))
+    assert oracle.round_to("f64", 0.1, use=use) == 0.1
+
+
+ALL_PINS = [pin_worked_example, pin_worked_example_vform, pin_brute_force,
+            pin_closed_form_slowmo, pin_closed_form_momentum, pin_torch_sgd,
+            pin_permutation, pin_fixed_point, pin_identical_workers,
+            pin_linearity, pin_rounding]

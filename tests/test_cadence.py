@@ -1,0 +1,43 @@
+"""Host cadence of Sec. 3.2 / Sec. 3.1 against Table 2's counts (CPU only)."""
+import math
+
+import pytest
+
+import oracle
+
+
+@pytest.mark.parametrize("K", range(1, 11))
+def test_table2_counts(K):
+    # Table 2: CPDP performs ceil(T/K) gradient and ceil(T/K) parameter
+    # synchronisations per epoch; K = 1 is DDP's T per epoch.
+    for T in range(1, 61):
+        syncs = sum(oracle.is_sync_step(t, K, T) for t in range(1, T + 1))
+        assert syncs == math.ceil(T / K)
+        if K == 1:
+            assert syncs == T
+
+
+@pytest.mark.parametrize("K", range(1, 9))
+def test_at_most_k_minus_1_local_steps(K):
+    # Sec. 5: up to K - 1 local updates between two synchronisation steps, and
+    # the last step of every epoch synchronises (Sec. 3.1).
+    for T in range(1, 40):
+        run = 0
+        for t in range(1, T + 1):
+            if oracle.is_sync_step(t, K, T):
+                run = 0
+            else:
+                run += 1
+                assert run <= K - 1
+        assert oracle.is_sync_step(T, K, T)
+
+
+def test_no_epoch_boundary():
+    assert [oracle.is_sync_step(t, 3) for t in range(1, 8)] == [
+        False, False, True, False, False, True, False]
+
+
+@pytest.mark.parametrize("bad", [(0, 2, 0), (1, 0, 0), (5, 2, 4), (1, 2, -1)])
+def test_invalid(bad):
+    with pytest.raises(ValueError):
+        oracle.is_sync_step(*bad)

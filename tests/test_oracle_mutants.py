@@ -1,0 +1,72 @@
+"""Plant mistakes in a copy of the oracle and require the pins to catch each.
+
+Every mutant is a textual edit of ``oracle/cpdp_oracle.c`` compiled into a
+temporary library (CPU only).  A mutant that passes every pin would mean the
+pins cannot tell that mistake from the method, so the test fails.
+"""
+import os
+
+import pytest
+
+import oracle
+import oracle_pins
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "cpdp_oracle.c")
+
+# (name, old text, new text, which occurrence of old text to replace)
+MUTANTS = [
+    ("local_drops_mu", "mu * mom[k] + grads[k]", "mom[k] + grads[k]", 0),
+    ("local_steps_on_grad",
+     "params[k] = store_as(param_dt, params[k] - lr * buf);",
+     "params[k] = store_as(param_dt, params[k] - lr * grads[k]);", 0),
+    ("gbar_not_divided", "gsum / (double)W", "gsum", 0),
+    ("sync_uses_local_grad", "mu * mom[k] + gbar", "mu * mom[k] + grads[k]", 0),
+    ("sync_drops_mu", "mu * mom[k] + gbar", "mom[k] + gbar", 0),
+    ("sync_buffer_not_stored", "mom[k] = buf;\n            double x",
+     "double x", 0),
+    ("u_sign_flipped", "(ref - avg) / lr", "(avg - ref) / lr", 0),
+    ("u_drops_lr", "(ref - avg) / lr", "(ref - avg)", 0),
+    ("u_drops_beta", "beta * slow[p] +", "slow[p] +", 0),
+    ("drops_alpha", "ref - alpha * lr * u", "ref - lr * u", 0),
+    ("new_ignores_u", "ref - alpha * lr * u", "avg", 0),
+    ("anchor_not_updated", "anchor[p] = fresh;", "", 0),
+    ("broadcast_avg", "store_as(param_dt, fresh);", "store_as(param_dt, avg);", 0),
+    ("u_not_stored", "slow[p] = u;", "", 0),
+    ("replica_index_dropped", "gsum += grads[(int64_t)i * P + p];",
+     "gsum += grads[p];", 0),
+    ("first_replica_skipped", "for (int i = 0; i < W; ++i) gsum",
+     "for (int i = 1; i < W; ++i) gsum", 0),
+    ("avg_wrong_divisor", "xsum / (double)W", "xsum / (double)(W + 1)", 0),
+    ("avg_of_pre_step_params", "xsum += x;", "xsum += params[k];", 0),
+    ("init_mom_not_zero", "mom[(int64_t)i * P + p] = 0.0;",
+     "mom[(int64_t)i * P + p] = th;", 0),
+    ("init_anchor_zero", "anchor[p] = store_as(aux_dt, th);", "anchor[p] = 0.0;", 0),
+    ("bf16_ties_away", "uint32_t lsb = (b >> 16) & 1u;", "uint32_t lsb = 0u;", 0),
+    ("f32_rounding_dropped", "return (double)(float)x;", "return x;", 0),
+    ("vform_drops_beta", "beta * velocity[p] + delta", "velocity[p] + delta", 0),
+    ("vform_delta_sign", "double delta = avg - ref;", "double delta = ref - avg;", 0),
+]
+
+
+def _mutate(src, old, new, occ):
+    parts = src.split(old)
+    assert len(parts) > occ + 1, f"mutation site {old!r} not found"
+    return old.join(parts[: occ + 1]) + new + old.join(parts[occ + 1:])
+
+
+@pytest.mark.parametrize("name,old,new,occ", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(tmp_path, name, old, new, occ):
+    src = open(SRC).read()
+    mutated = _mutate(src, old, new, occ)
+    assert mutated != src
+    c_path = tmp_path / f"{name}.c"
+    c_path.write_text(mutated)
+    lib = oracle.load(oracle.build(str(c_path), str(tmp_path / f"lib{name}.so")))
+    caught = []
+    for pin in oracle_pins.ALL_PINS:
+        try:
+            pin(use=lib)
+        except (AssertionError, ValueError, FloatingPointError) as e:
+            caught.append((pin.__name__, str(e)[:80]))
+            break
+    assert caught, f"mutant {name} passed every pin"
