@@ -1,0 +1,124 @@
+/*
+ * cpdp.h -- C ABI of the Controlled Periodic Data Parallelism (CPDP) reconcile
+ * hot path on one AMD Instinct MI355X (gfx950).
+ *
+ * The method (paper: "Controlled Periodic Synchronization for Efficient
+ * Data-Parallel Training"): W worker replicas take independent momentum-SGD
+ * steps; every K steps they are reconciled by a gradient mean, a synchronized
+ * optimizer step with that mean, a parameter mean, and a SlowMo outer update
+ * whose result is copied back to every replica.  On one GPU all W replicas
+ * live in HBM and the cross-worker means (the AllReduce of the paper's DDP
+ * deployment) are computed inside one kernel.
+ *
+ * Layout (all entry points)
+ *   A per-replica family (params, mom, grads) is W rows of P coordinates with
+ *   a row stride of ld elements: replica i, coordinate p is at base[i*ld + p].
+ *   Elements p in [P, ld) of every row are never read or written.
+ *   slow_mom (u) and anchor (the reference model theta_ref) are P fp32 values.
+ *   All pointers are device pointers owned by the caller; the library never
+ *   allocates, frees or keeps them.  Each family must start on a 16-byte
+ *   boundary and ld * sizeof(element) must be a multiple of 16.  The ranges
+ *   of different arguments must not overlap.
+ *
+ * Storage types (param_dt, grad_dt, mom_dt): CPDP_F32 everywhere, or
+ *   params in CPDP_BF16 with fp32 grads and momentum.  All arithmetic is fp32;
+ *   bf16 parameters are rounded to nearest-even each time they are written.
+ *
+ * Hyperparameters are fp32: lr > 0 and finite (Sec. 3.1), 0 <= mu < 1,
+ *   0 <= beta < 1 (Sec. 3.1), alpha > 0 and finite, K >= 1 (Sec. 3.1).
+ *   K is validated but does not enter the arithmetic: the caller decides
+ *   which step synchronises (cpdp_is_sync_step).
+ *
+ * Streams and errors
+ *   `stream` is a hipStream_t passed as void* (NULL = the null stream).  Every
+ *   device entry point validates all arguments on the host first and returns
+ *   a cpdp_status without touching the GPU when one is invalid; otherwise it
+ *   enqueues its kernel(s) on `stream` and returns CPDP_OK, or CPDP_ERR_HIP if
+ *   the launch failed.  Results are ready when the stream is synchronised.
+ *   P = 0 is a valid no-op.  NaN and Inf propagate without being checked.
+ *   Calls are reentrant; two calls that touch the same buffers on different
+ *   streams without ordering race.
+ */
+#ifndef CPDP_H
+#define CPDP_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { CPDP_F32 = 0, CPDP_BF16 = 1 } cpdp_dtype;
+
+typedef enum {
+    CPDP_OK = 0,
+    CPDP_ERR_INVALID_ARG = 1, /* W, P, ld, K or a hyperparameter out of range */
+    CPDP_ERR_NULL = 2,        /* a required pointer is NULL (P > 0)          */
+    CPDP_ERR_MISALIGNED = 3,  /* pointer or row stride not 16-byte aligned   */
+    CPDP_ERR_OVERLAP = 4,     /* two argument ranges overlap                 */
+    CPDP_ERR_DTYPE = 5,       /* unsupported storage-type combination        */
+    CPDP_ERR_HIP = 6          /* the HIP runtime rejected the launch         */
+} cpdp_status;
+
+/*
+ * Initialisation of Algorithm 1 (CPDP with SlowMo): every replica starts from
+ * theta0, the SlowMo state starts at 0 and the reference model at theta0.
+ *   theta0   [P] in param_dt (read)
+ *   params   [W x ld] param_dt  <- theta0 in every row
+ *   mom      [W x ld] mom_dt    <- 0
+ *   slow_mom [P] fp32           <- 0
+ *   anchor   [P] fp32           <- theta0 (widened)
+ */
+int cpdp_state_init(const void* theta0, void* params, void* mom,
+                    float* slow_mom, float* anchor, int W, int64_t P,
+                    int64_t ld, int K, int param_dt, int mom_dt, void* stream);
+
+/*
+ * Local update phase (Sec. 3.2, Eq. local_update, run as the framework's SGD
+ * optimizer with a per-replica momentum buffer, Sec. 4.2), for every replica
+ * i and coordinate p < P, with no communication:
+ *   mom_i   <- mu * mom_i + grad_i
+ *   param_i <- param_i - lr * mom_i
+ * grads [W x ld] are read only; params and mom are updated in place.
+ */
+int cpdp_local_step(void* params, void* mom, const void* grads, int W,
+                    int64_t P, int64_t ld, int K, float lr, float mu,
+                    int param_dt, int grad_dt, int mom_dt, void* stream);
+
+/*
+ * Synchronization phase (Sec. 3.2 stages one and two, Sec. 3.3 SlowMo, in
+ * the execution order of Sec. 4.2), in one pass over HBM.  Per coordinate p:
+ *   gbar    = (1/W) * sum_i grad_i          (fixed order i = 0..W-1)
+ *   mom_i  <- mu * mom_i + gbar             (stored; buffers stay per replica)
+ *   x_i     = param_i - lr * mom_i          (rounded to param_dt)
+ *   avg     = (1/W) * sum_i x_i             (accumulated as x_i - anchor)
+ *   u      <- beta * u + (anchor - avg) / lr
+ *   new     = anchor - alpha * lr * u
+ *   param_i <- new for every i;  anchor <- new
+ * With v = -lr*u and alpha = 1 this is the paper's v <- beta v + (avg - ref),
+ * new = ref + v.  grads are read only (the mean is not written back).
+ */
+int cpdp_reconcile(void* params, void* mom, const void* grads,
+                   float* slow_mom, float* anchor, int W, int64_t P,
+                   int64_t ld, int K, float lr, float mu, float beta,
+                   float alpha, int param_dt, int grad_dt, int mom_dt,
+                   void* stream);
+
+/*
+ * Synchronisation indicator (Sec. 3.2) with the forced synchronisation at the
+ * end of an epoch (Sec. 3.1, Sec. 4.2).  Host only, no GPU work.
+ *   t: 1-based step counter inside the epoch; K: period (>= 1);
+ *   T: steps per epoch, or 0 when there is no epoch boundary.
+ * Returns 1 if step t synchronises (t mod K == 0, or t == T), 0 if it is a
+ * local step, or -CPDP_ERR_INVALID_ARG if t < 1, K < 1, T < 0 or t > T > 0.
+ */
+int cpdp_is_sync_step(int64_t t, int K, int64_t T);
+
+/* Static, human-readable name of a status code (never NULL). */
+const char* cpdp_status_str(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CPDP_H */

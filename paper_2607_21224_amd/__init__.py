@@ -1,0 +1,12 @@
+"""MI355X-native (gfx950) implementation of the reconcile hot path of
+Controlled Periodic Data Parallelism (CPDP) with SlowMo.
+
+Submodules
+  cpdp   ctypes binding of the C ABI in include/cpdp.h (libcpdp.so)
+  state  HBM-resident replica state and the host cadence driving it
+  build  hipcc build of the shared libraries
+
+Importing ``cpdp`` (directly or through ``state``) raises ImportError when the
+HIP library is not built: there is no CPU fallback.
+"""
+__all__ = ["cpdp", "state", "build"]

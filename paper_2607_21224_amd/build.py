@@ -1,0 +1,53 @@
+"""Build the gfx950 shared library of the CPDP path (and the synthetic-input
+library the tests and benchmark use) with hipcc, in-tree."""
+from __future__ import annotations
+
+import os
+import subprocess
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+ARCH = "gfx950"
+
+LIB_CPDP = os.path.join(PKG, "libcpdp.so")
+LIB_SYNTH = os.path.join(ROOT, "synth", "libsynth.so")
+
+# -ffp-contract=off: only the explicit fmaf calls fuse, so the arithmetic is
+# exactly what the source says.  Packed fp32 instructions are disabled.
+HIP_FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
+             "-ffp-contract=off", "-Xclang", "-target-feature", "-Xclang",
+             "-packed-fp32-ops", "-Wall", "-Wno-unused-command-line-argument"]
+
+
+def _run(cmd):
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("build failed:\n" + " ".join(cmd) + "\n" + r.stdout + r.stderr)
+
+
+def build_cpdp(out: str = LIB_CPDP, extra=()) -> str:
+    csrc = os.path.join(PKG, "csrc")
+    tmp = out + ".tmp"
+    _run([HIPCC, *HIP_FLAGS, *extra, "-I", os.path.join(ROOT, "include"), "-I", csrc,
+          "-o", tmp, os.path.join(csrc, "cpdp_kernels.hip"),
+          os.path.join(csrc, "cpdp_api.cpp")])
+    os.replace(tmp, out)
+    return out
+
+
+def build_synth(out: str = LIB_SYNTH) -> str:
+    tmp = out + ".tmp"
+    _run([HIPCC, *HIP_FLAGS, "-o", tmp, os.path.join(ROOT, "synth", "synth.hip")])
+    os.replace(tmp, out)
+    return out
+
+
+def build_all() -> None:
+    build_cpdp()
+    build_synth()
+
+
+if __name__ == "__main__":
+    build_all()
+    print("built", LIB_CPDP, LIB_SYNTH)

@@ -1,0 +1,137 @@
+"""Python binding of the CPDP C ABI (include/cpdp.h).
+
+Argument marshalling only: every step of the path runs in the gfx950 kernels
+of ``libcpdp.so``.  The functions carry the C names and argument order.
+Pointer arguments accept a ``torch.Tensor`` (its ``data_ptr()``) or a plain
+integer address; ``stream`` accepts ``None`` (the null stream), a
+``torch.cuda.Stream`` or a raw ``hipStream_t`` integer.  A non-zero status is
+raised as :class:`CpdpError` unless ``check=False``.
+
+There is no fallback: if the library is not built, importing this module
+raises ImportError.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libcpdp.so")
+
+CPDP_F32 = 0
+CPDP_BF16 = 1
+
+CPDP_OK = 0
+CPDP_ERR_INVALID_ARG = 1
+CPDP_ERR_NULL = 2
+CPDP_ERR_MISALIGNED = 3
+CPDP_ERR_OVERLAP = 4
+CPDP_ERR_DTYPE = 5
+CPDP_ERR_HIP = 6
+
+DTYPES = {"f32": CPDP_F32, "bf16": CPDP_BF16}
+
+# every symbol declared in include/cpdp.h
+EXPORTS = ("cpdp_state_init", "cpdp_local_step", "cpdp_reconcile",
+           "cpdp_is_sync_step", "cpdp_status_str")
+
+
+def _load() -> ctypes.CDLL:
+    # PyTorch ships its own HIP runtime.  Import it first so that libcpdp.so's
+    # libamdhip64.so.7 dependency resolves to that already-loaded runtime: the
+    # device memory and stream handles torch hands us belong to it, and a
+    # second runtime instance in the process would not see the device.
+    import torch  # noqa: F401
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is not built; run `python -m paper_2607_21224_amd.build` "
+            "(the CPDP path has no CPU fallback)")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i, i64, f = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_float
+    lib.cpdp_state_init.argtypes = [vp, vp, vp, vp, vp, i, i64, i64, i, i, i, vp]
+    lib.cpdp_local_step.argtypes = [vp, vp, vp, i, i64, i64, i, f, f, i, i, i, vp]
+    lib.cpdp_reconcile.argtypes = [vp, vp, vp, vp, vp, i, i64, i64, i, f, f, f, f,
+                                   i, i, i, vp]
+    lib.cpdp_is_sync_step.argtypes = [i64, i, i64]
+    lib.cpdp_status_str.argtypes = [i]
+    lib.cpdp_status_str.restype = ctypes.c_char_p
+    for name in ("cpdp_state_init", "cpdp_local_step", "cpdp_reconcile",
+                 "cpdp_is_sync_step"):
+        getattr(lib, name).restype = ctypes.c_int
+    return lib
+
+
+lib = _load()
+
+
+class CpdpError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {cpdp_status_str(status)}")
+
+
+def _addr(x) -> int | None:
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return int(x.data_ptr())
+
+
+def _stream(s) -> int | None:
+    if s is None:
+        return None
+    if isinstance(s, int):
+        return s
+    return int(s.cuda_stream)
+
+
+def _dt(x) -> int:
+    return DTYPES[x] if isinstance(x, str) else int(x)
+
+
+def _done(status: int, where: str, check: bool) -> int:
+    if check and status != CPDP_OK:
+        raise CpdpError(status, where)
+    return status
+
+
+def cpdp_status_str(status: int) -> str:
+    return lib.cpdp_status_str(int(status)).decode()
+
+
+def cpdp_is_sync_step(t: int, K: int, T: int = 0) -> bool:
+    r = lib.cpdp_is_sync_step(int(t), int(K), int(T))
+    if r < 0:
+        raise CpdpError(-r, "cpdp_is_sync_step")
+    return bool(r)
+
+
+def cpdp_state_init(theta0, params, mom, slow_mom, anchor, W, P, ld, K,
+                    param_dt=CPDP_F32, mom_dt=CPDP_F32, stream=None, check=True):
+    s = lib.cpdp_state_init(_addr(theta0), _addr(params), _addr(mom),
+                            _addr(slow_mom), _addr(anchor), int(W), int(P),
+                            int(ld), int(K), _dt(param_dt), _dt(mom_dt),
+                            _stream(stream))
+    return _done(s, "cpdp_state_init", check)
+
+
+def cpdp_local_step(params, mom, grads, W, P, ld, K, lr, mu,
+                    param_dt=CPDP_F32, grad_dt=CPDP_F32, mom_dt=CPDP_F32,
+                    stream=None, check=True):
+    s = lib.cpdp_local_step(_addr(params), _addr(mom), _addr(grads), int(W),
+                            int(P), int(ld), int(K), float(lr), float(mu),
+                            _dt(param_dt), _dt(grad_dt), _dt(mom_dt),
+                            _stream(stream))
+    return _done(s, "cpdp_local_step", check)
+
+
+def cpdp_reconcile(params, mom, grads, slow_mom, anchor, W, P, ld, K, lr, mu,
+                   beta, alpha, param_dt=CPDP_F32, grad_dt=CPDP_F32,
+                   mom_dt=CPDP_F32, stream=None, check=True):
+    s = lib.cpdp_reconcile(_addr(params), _addr(mom), _addr(grads),
+                           _addr(slow_mom), _addr(anchor), int(W), int(P),
+                           int(ld), int(K), float(lr), float(mu), float(beta),
+                           float(alpha), _dt(param_dt), _dt(grad_dt),
+                           _dt(mom_dt), _stream(stream))
+    return _done(s, "cpdp_reconcile", check)

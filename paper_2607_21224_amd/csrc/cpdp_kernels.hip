@@ -1,0 +1,382 @@
+// gfx950 kernels of the CPDP reconcile hot path (state initialisation, local
+// momentum-SGD step, fused reconcile).
+//
+// All three are HBM-streaming kernels: nothing here is a dense contraction, so
+// there is no MFMA and no LDS.  Every thread owns VEC = 4 consecutive
+// coordinates and moves them with 128-bit (fp32) or 64-bit (bf16) vector
+// accesses; a wavefront therefore touches 1 KiB (fp32) of each array row per
+// access, fully coalesced.  Every output element is written by exactly one
+// thread, there are no atomics and no inter-block dependencies, and the
+// cross-replica sums run in a fixed order (replica 0, 1, ..., W-1) inside one
+// thread, so results are bitwise independent of the launch shape.
+//
+// Arithmetic is fp32 with explicit fmaf at the two optimizer updates and the
+// SlowMo step (the library is built with -ffp-contract=off so nothing else is
+// fused).  bf16 parameters are widened on load and rounded to nearest-even on
+// every store, including the x_i fed to the parameter mean, where the
+// framework implementation writes the optimizer's result to the parameter
+// tensor before averaging it (Sec. 4.2).
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "cpdp_launch.h"
+
+namespace cpdp {
+namespace {
+
+constexpr int kBlock = 256;
+constexpr int kVec = 4;
+
+// State tensors are streamed exactly once per call; nontemporal accesses keep
+// them from displacing anything useful in L2 / MALL.
+#ifndef CPDP_NONTEMPORAL
+#define CPDP_NONTEMPORAL 1
+#endif
+constexpr bool kNT = CPDP_NONTEMPORAL != 0;
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+template <bool NT, class V>
+__device__ __forceinline__ V vload(const V* p) {
+    if constexpr (NT) return __builtin_nontemporal_load(p);
+    else return *p;
+}
+
+template <bool NT, class V>
+__device__ __forceinline__ void vstore(V* p, V v) {
+    if constexpr (NT) __builtin_nontemporal_store(v, p);
+    else *p = v;
+}
+
+// ---- fp32 lanes: FULL = all 4 coordinates valid, else the first n --------
+
+template <bool FULL, bool NT>
+__device__ __forceinline__ void load_f32(const float* p, int n, float (&x)[kVec]) {
+    if constexpr (FULL) {
+        f32x4 v = vload<NT>(reinterpret_cast<const f32x4*>(p));
+        x[0] = v.x; x[1] = v.y; x[2] = v.z; x[3] = v.w;
+    } else {
+#pragma unroll
+        for (int k = 0; k < kVec; ++k) x[k] = k < n ? p[k] : 0.0f;
+    }
+}
+
+template <bool FULL, bool NT>
+__device__ __forceinline__ void store_f32(float* p, int n, const float (&x)[kVec]) {
+    if constexpr (FULL) {
+        f32x4 v = {x[0], x[1], x[2], x[3]};
+        vstore<NT>(reinterpret_cast<f32x4*>(p), v);
+    } else {
+#pragma unroll
+        for (int k = 0; k < kVec; ++k)
+            if (k < n) p[k] = x[k];
+    }
+}
+
+// ---- parameter storage ----------------------------------------------------
+
+struct ParamF32 {
+    using T = float;
+    __device__ static __forceinline__ float round(float x) { return x; }
+    template <bool FULL, bool NT>
+    __device__ static __forceinline__ void load(const T* p, int n, float (&x)[kVec]) {
+        load_f32<FULL, NT>(p, n, x);
+    }
+    template <bool FULL, bool NT>
+    __device__ static __forceinline__ void store(T* p, int n, const float (&x)[kVec]) {
+        store_f32<FULL, NT>(p, n, x);
+    }
+};
+
+__device__ __forceinline__ uint32_t bf16_bits(float f) {
+    uint32_t b = __float_as_uint(f);
+    if ((b & 0x7FFFFFFFu) > 0x7F800000u) return (b >> 16) | 0x40u;  // keep NaN quiet
+    b += 0x7FFFu + ((b >> 16) & 1u);                                  // nearest, ties even
+    return b >> 16;
+}
+
+__device__ __forceinline__ float bf16_value(uint32_t h) { return __uint_as_float(h << 16); }
+
+struct ParamBF16 {
+    using T = uint16_t;
+    __device__ static __forceinline__ float round(float x) { return bf16_value(bf16_bits(x)); }
+    template <bool FULL, bool NT>
+    __device__ static __forceinline__ void load(const T* p, int n, float (&x)[kVec]) {
+        if constexpr (FULL) {
+            u32x2 v = vload<NT>(reinterpret_cast<const u32x2*>(p));
+            x[0] = __uint_as_float(v.x << 16);
+            x[1] = __uint_as_float(v.x & 0xFFFF0000u);
+            x[2] = __uint_as_float(v.y << 16);
+            x[3] = __uint_as_float(v.y & 0xFFFF0000u);
+        } else {
+#pragma unroll
+            for (int k = 0; k < kVec; ++k) x[k] = k < n ? bf16_value(p[k]) : 0.0f;
+        }
+    }
+    template <bool FULL, bool NT>
+    __device__ static __forceinline__ void store(T* p, int n, const float (&x)[kVec]) {
+        if constexpr (FULL) {
+            u32x2 v = {bf16_bits(x[0]) | (bf16_bits(x[1]) << 16),
+                       bf16_bits(x[2]) | (bf16_bits(x[3]) << 16)};
+            vstore<NT>(reinterpret_cast<u32x2*>(p), v);
+        } else {
+#pragma unroll
+            for (int k = 0; k < kVec; ++k)
+                if (k < n) p[k] = (uint16_t)bf16_bits(x[k]);
+        }
+    }
+};
+
+// ---- state initialisation ---------------------------------------------------
+
+template <class PS, bool FULL>
+__device__ __forceinline__ void init_chunk(const typename PS::T* theta0, typename PS::T* params,
+                                           float* mom, float* slow, float* anchor, int W,
+                                           int64_t ld, int64_t p0, int n) {
+    float th[kVec];
+    const float zero[kVec] = {0.0f, 0.0f, 0.0f, 0.0f};
+    PS::template load<FULL, false>(theta0 + p0, n, th);
+    for (int i = 0; i < W; ++i) {
+        const int64_t off = (int64_t)i * ld + p0;
+        PS::template store<FULL, kNT>(params + off, n, th);
+        store_f32<FULL, kNT>(mom + off, n, zero);
+    }
+    store_f32<FULL, kNT>(slow + p0, n, zero);
+    store_f32<FULL, kNT>(anchor + p0, n, th);
+}
+
+template <class PS>
+__global__ __launch_bounds__(kBlock) void state_init_kernel(
+    const typename PS::T* __restrict__ theta0, typename PS::T* __restrict__ params,
+    float* __restrict__ mom, float* __restrict__ slow, float* __restrict__ anchor, int W,
+    int64_t ld, int64_t P) {
+    const int64_t p0 = ((int64_t)blockIdx.x * kBlock + threadIdx.x) * kVec;
+    if (p0 >= P) return;
+    if (p0 + kVec <= P)
+        init_chunk<PS, true>(theta0, params, mom, slow, anchor, W, ld, p0, kVec);
+    else
+        init_chunk<PS, false>(theta0, params, mom, slow, anchor, W, ld, p0, (int)(P - p0));
+}
+
+// ---- local step: one replica row per block, 4 coordinates per thread -------
+
+template <class PS, bool FULL>
+__device__ __forceinline__ void local_chunk(typename PS::T* params, float* mom,
+                                            const float* grads, int64_t off, int n, float lr,
+                                            float mu) {
+    float g[kVec], m[kVec], th[kVec];
+    load_f32<FULL, kNT>(grads + off, n, g);
+    load_f32<FULL, kNT>(mom + off, n, m);
+    PS::template load<FULL, kNT>(params + off, n, th);
+#pragma unroll
+    for (int k = 0; k < kVec; ++k) {
+        m[k] = fmaf(mu, m[k], g[k]);
+        th[k] = fmaf(-lr, m[k], th[k]);
+    }
+    store_f32<FULL, kNT>(mom + off, n, m);
+    PS::template store<FULL, kNT>(params + off, n, th);
+}
+
+template <class PS>
+__global__ __launch_bounds__(kBlock) void local_step_kernel(
+    typename PS::T* __restrict__ params, float* __restrict__ mom,
+    const float* __restrict__ grads, int64_t ld, int64_t P, int64_t blocks_per_row, float lr,
+    float mu) {
+    const int64_t row = blockIdx.x / blocks_per_row;
+    const int64_t col = blockIdx.x - row * blocks_per_row;
+    const int64_t p0 = (col * kBlock + threadIdx.x) * kVec;
+    if (p0 >= P) return;
+    const int64_t off = row * ld + p0;
+    if (p0 + kVec <= P)
+        local_chunk<PS, true>(params, mom, grads, off, kVec, lr, mu);
+    else
+        local_chunk<PS, false>(params, mom, grads, off, (int)(P - p0), lr, mu);
+}
+
+// ---- fused reconcile ----------------------------------------------------------
+//
+// One thread owns 4 coordinates across all W replicas.  WT > 0 fixes W at
+// compile time (fully unrolled, all loads of a phase in flight together);
+// WT == 0 takes W at run time.
+
+template <int WT, class PS, bool FULL>
+__device__ __forceinline__ void reconcile_chunk(typename PS::T* params, float* mom,
+                                                const float* grads, float* slow, float* anchor,
+                                                int W, int64_t ld, int64_t p0, int n, float lr,
+                                                float mu, float beta, float alpha_lr,
+                                                float inv_w) {
+    const int nw = WT > 0 ? WT : W;
+
+    // gradient mean (the AllReduce of the synchronisation step), fixed order
+    float acc[kVec], g[kVec];
+    load_f32<FULL, kNT>(grads + p0, n, acc);
+#pragma unroll
+    for (int i = 1; i < nw; ++i) {
+        load_f32<FULL, kNT>(grads + (int64_t)i * ld + p0, n, g);
+#pragma unroll
+        for (int k = 0; k < kVec; ++k) acc[k] += g[k];
+    }
+    float gbar[kVec];
+#pragma unroll
+    for (int k = 0; k < kVec; ++k) gbar[k] = acc[k] * inv_w;
+
+    float a[kVec], u[kVec];
+    load_f32<FULL, kNT>(anchor + p0, n, a);
+    load_f32<FULL, kNT>(slow + p0, n, u);
+
+    // synchronized optimizer step per replica, then the parameter mean taken
+    // as a + mean(x_i - a) so the small difference keeps its precision
+    float s[kVec] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int i = 0; i < nw; ++i) {
+        const int64_t off = (int64_t)i * ld + p0;
+        float m[kVec], th[kVec];
+        load_f32<FULL, kNT>(mom + off, n, m);
+        PS::template load<FULL, kNT>(params + off, n, th);
+#pragma unroll
+        for (int k = 0; k < kVec; ++k) {
+            m[k] = fmaf(mu, m[k], gbar[k]);
+            const float x = PS::round(fmaf(-lr, m[k], th[k]));
+            s[k] += x - a[k];
+        }
+        store_f32<FULL, kNT>(mom + off, n, m);
+    }
+
+    // SlowMo outer step: u <- beta u + (a - avg)/lr ; new = a - alpha lr u
+#pragma unroll
+    for (int k = 0; k < kVec; ++k) {
+        const float drift = s[k] * inv_w;  // avg - a
+        u[k] = fmaf(beta, u[k], -drift / lr);
+        a[k] = fmaf(-alpha_lr, u[k], a[k]);
+    }
+    store_f32<FULL, kNT>(slow + p0, n, u);
+    store_f32<FULL, kNT>(anchor + p0, n, a);
+
+    // copy the reconciled model back into every replica
+#pragma unroll
+    for (int i = 0; i < nw; ++i)
+        PS::template store<FULL, kNT>(params + (int64_t)i * ld + p0, n, a);
+}
+
+template <int WT, class PS>
+__global__ __launch_bounds__(kBlock) void reconcile_kernel(
+    typename PS::T* __restrict__ params, float* __restrict__ mom,
+    const float* __restrict__ grads, float* __restrict__ slow, float* __restrict__ anchor,
+    int W, int64_t ld, int64_t P, float lr, float mu, float beta, float alpha_lr,
+    float inv_w) {
+    const int64_t p0 = ((int64_t)blockIdx.x * kBlock + threadIdx.x) * kVec;
+    if (p0 >= P) return;
+    if (p0 + kVec <= P)
+        reconcile_chunk<WT, PS, true>(params, mom, grads, slow, anchor, W, ld, p0, kVec, lr,
+                                      mu, beta, alpha_lr, inv_w);
+    else
+        reconcile_chunk<WT, PS, false>(params, mom, grads, slow, anchor, W, ld, p0,
+                                       (int)(P - p0), lr, mu, beta, alpha_lr, inv_w);
+}
+
+// ---- launch helpers -------------------------------------------------------------
+
+inline int64_t blocks_for(int64_t P) { return (P + (int64_t)kBlock * kVec - 1) / ((int64_t)kBlock * kVec); }
+
+template <class T>
+struct same_type {
+    using type = T;
+};
+
+// Argument types come from the kernel's signature only (the trailing
+// parameters are a non-deduced context), so every argument is converted to
+// exactly what the kernel takes before its address goes into argv.
+template <class... Args>
+int launch(void (*kernel)(Args...), int64_t blocks, void* stream,
+           typename same_type<Args>::type... args) {
+    void* argv[] = {static_cast<void*>(&args)...};
+    hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(kernel),
+                                   dim3((unsigned)blocks), dim3(kBlock), argv, 0,
+                                   static_cast<hipStream_t>(stream));
+    return (int)e;
+}
+
+template <class PS>
+int state_init_t(const void* theta0, void* params, float* mom, float* slow, float* anchor,
+                 int W, int64_t P, int64_t ld, void* stream) {
+    using T = typename PS::T;
+    return launch(state_init_kernel<PS>, blocks_for(P), stream,
+                  static_cast<const T*>(theta0), static_cast<T*>(params), mom, slow, anchor, W,
+                  ld, P);
+}
+
+template <class PS>
+int local_step_t(void* params, float* mom, const float* grads, int W, int64_t P, int64_t ld,
+                 float lr, float mu, void* stream) {
+    using T = typename PS::T;
+    const int64_t bpr = blocks_for(P);
+    return launch(local_step_kernel<PS>, bpr * W, stream, static_cast<T*>(params), mom, grads,
+                  ld, P, bpr, lr, mu);
+}
+
+template <int WT, class PS>
+int reconcile_w(void* params, float* mom, const float* grads, float* slow, float* anchor,
+                int W, int64_t P, int64_t ld, float lr, float mu, float beta, float alpha,
+                void* stream) {
+    using T = typename PS::T;
+    const float alpha_lr = alpha * lr;
+    const float inv_w = 1.0f / (float)W;
+    return launch(reconcile_kernel<WT, PS>, blocks_for(P), stream, static_cast<T*>(params),
+                  mom, grads, slow, anchor, W, ld, P, lr, mu, beta, alpha_lr, inv_w);
+}
+
+template <class PS>
+int reconcile_t(void* params, float* mom, const float* grads, float* slow, float* anchor,
+                int W, int64_t P, int64_t ld, float lr, float mu, float beta, float alpha,
+                void* stream) {
+#define CPDP_W_CASE(N)                                                                      \
+    case N:                                                                                 \
+        return reconcile_w<N, PS>(params, mom, grads, slow, anchor, W, P, ld, lr, mu, beta, \
+                                  alpha, stream);
+    switch (W) {
+        CPDP_W_CASE(1)
+        CPDP_W_CASE(2)
+        CPDP_W_CASE(4)
+        CPDP_W_CASE(8)
+        CPDP_W_CASE(16)
+        CPDP_W_CASE(32)
+        default:
+            return reconcile_w<0, PS>(params, mom, grads, slow, anchor, W, P, ld, lr, mu, beta,
+                                      alpha, stream);
+    }
+#undef CPDP_W_CASE
+}
+
+}  // namespace
+
+int launch_state_init(Param pt, const void* theta0, void* params, float* mom, float* slow,
+                      float* anchor, int W, int64_t P, int64_t ld, void* stream) {
+    return pt == Param::BF16
+               ? state_init_t<ParamBF16>(theta0, params, mom, slow, anchor, W, P, ld, stream)
+               : state_init_t<ParamF32>(theta0, params, mom, slow, anchor, W, P, ld, stream);
+}
+
+int launch_local_step(Param pt, void* params, float* mom, const float* grads, int W, int64_t P,
+                      int64_t ld, float lr, float mu, void* stream) {
+    return pt == Param::BF16
+               ? local_step_t<ParamBF16>(params, mom, grads, W, P, ld, lr, mu, stream)
+               : local_step_t<ParamF32>(params, mom, grads, W, P, ld, lr, mu, stream);
+}
+
+int launch_reconcile(Param pt, void* params, float* mom, const float* grads, float* slow,
+                     float* anchor, int W, int64_t P, int64_t ld, float lr, float mu, float beta,
+                     float alpha, void* stream) {
+    return pt == Param::BF16 ? reconcile_t<ParamBF16>(params, mom, grads, slow, anchor, W, P,
+                                                      ld, lr, mu, beta, alpha, stream)
+                             : reconcile_t<ParamF32>(params, mom, grads, slow, anchor, W, P, ld,
+                                                     lr, mu, beta, alpha, stream);
+}
+
+bool grid_fits(int rows, int64_t P) {
+    return rows >= 1 && blocks_for(P) <= (int64_t)0x7FFFFFFF / rows;
+}
+
+const char* hip_error_string(int err) { return hipGetErrorString((hipError_t)err); }
+
+}  // namespace cpdp

@@ -1,0 +1,88 @@
+"""Device-resident CPDP state and the host cadence that drives it.
+
+PyTorch only allocates the HBM buffers and supplies the stream; every update
+goes through the C ABI (``cpdp.py``).  Layout: params / mom are (W, ld)
+tensors whose first P columns are the replicas' coordinates (row stride ld);
+slow_mom (u) and anchor (the reference model) are (P,) fp32 tensors.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import torch
+
+from . import cpdp
+
+
+def round_up(x: int, m: int) -> int:
+    return (x + m - 1) // m * m
+
+
+@dataclass(frozen=True)
+class Hyper:
+    """Hyperparameters as the fp32 values the kernels use."""
+    lr: float
+    mu: float
+    beta: float
+    alpha: float
+
+    @staticmethod
+    def fp32(lr, mu, beta, alpha) -> "Hyper":
+        f = lambda x: float(torch.tensor(x, dtype=torch.float32))  # noqa: E731
+        return Hyper(f(lr), f(mu), f(beta), f(alpha))
+
+
+class CpdpState:
+    """W replicas of a P-coordinate model with per-replica momentum, SlowMo
+    velocity u and the reference (anchor) model, all in HBM."""
+
+    def __init__(self, W: int, P: int, ld: int | None = None, K: int = 1,
+                 param_dt: str = "f32", device="cuda"):
+        self.W, self.P, self.K = int(W), int(P), int(K)
+        align = 128 if param_dt == "bf16" else 64  # 256-byte rows
+        self.ld = int(ld) if ld is not None else round_up(max(self.P, 1), align)
+        self.param_dt = param_dt
+        tdt = torch.bfloat16 if param_dt == "bf16" else torch.float32
+        self.params = torch.empty((self.W, self.ld), dtype=tdt, device=device)
+        self.mom = torch.empty((self.W, self.ld), dtype=torch.float32, device=device)
+        self.slow_mom = torch.empty(max(self.P, 1), dtype=torch.float32, device=device)
+        self.anchor = torch.empty(max(self.P, 1), dtype=torch.float32, device=device)
+
+    @property
+    def torch_param_dtype(self):
+        return self.params.dtype
+
+    def init(self, theta0: torch.Tensor, stream=None) -> None:
+        """Algorithm 1 initialisation; theta0 is (P,) in the parameter dtype."""
+        assert theta0.dtype == self.params.dtype and theta0.numel() >= self.P
+        cpdp.cpdp_state_init(theta0, self.params, self.mom, self.slow_mom,
+                             self.anchor, self.W, self.P, self.ld, self.K,
+                             self.param_dt, "f32", stream)
+
+    def local_step(self, grads: torch.Tensor, h: Hyper, stream=None) -> None:
+        self._check_grads(grads)
+        cpdp.cpdp_local_step(self.params, self.mom, grads, self.W, self.P,
+                             self.ld, self.K, h.lr, h.mu, self.param_dt, "f32",
+                             "f32", stream)
+
+    def reconcile(self, grads: torch.Tensor, h: Hyper, stream=None) -> None:
+        self._check_grads(grads)
+        cpdp.cpdp_reconcile(self.params, self.mom, grads, self.slow_mom,
+                            self.anchor, self.W, self.P, self.ld, self.K, h.lr,
+                            h.mu, h.beta, h.alpha, self.param_dt, "f32", "f32",
+                            stream)
+
+    def step(self, t: int, grads: torch.Tensor, h: Hyper, T: int = 0,
+             stream=None) -> str:
+        """Step t (1-based within the epoch): a reconcile when the cadence of
+        Sec. 3.2 (with the epoch-end rule of Sec. 3.1) says so, else a local
+        step.  Returns "reconcile" or "local"."""
+        if cpdp.cpdp_is_sync_step(t, self.K, T):
+            self.reconcile(grads, h, stream)
+            return "reconcile"
+        self.local_step(grads, h, stream)
+        return "local"
+
+    def _check_grads(self, g: torch.Tensor) -> None:
+        assert g.dtype == torch.float32 and g.is_contiguous()
+        assert g.shape == (self.W, self.ld), (tuple(g.shape), self.W, self.ld)

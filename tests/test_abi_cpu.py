@@ -1,0 +1,170 @@
+"""The C-ABI library on the CPU: it loads, exports every symbol the header
+declares, and rejects invalid arguments on the host before any GPU work.
+Only argument combinations that fail validation are passed here, so no call
+reaches HIP; the pointers are fake aligned addresses that are never read."""
+import ctypes
+import math
+import re
+
+import pytest
+
+import oracle
+from paper_2607_21224_amd import cpdp
+from paper_2607_21224_amd.build import ROOT
+
+HEADER = f"{ROOT}/include/cpdp.h"
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(cpdp_\w+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    names = declared_functions()
+    assert names == sorted(cpdp.EXPORTS)
+    lib = ctypes.CDLL(cpdp.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings():
+    for s in range(7):
+        assert cpdp.cpdp_status_str(s).startswith("CPDP")
+    assert "unknown" in cpdp.cpdp_status_str(99)
+
+
+@pytest.mark.parametrize("K", range(1, 9))
+def test_sync_indicator_matches_oracle_and_table2(K):
+    for T in [0] + list(range(1, 30)):
+        n = T if T else 40
+        got = [cpdp.cpdp_is_sync_step(t, K, T) for t in range(1, n + 1)]
+        want = [oracle.is_sync_step(t, K, T) for t in range(1, n + 1)]
+        assert got == want
+        if T:
+            assert sum(got) == math.ceil(T / K)  # Table 2
+
+
+@pytest.mark.parametrize("args", [(0, 2, 0), (1, 0, 0), (5, 2, 4), (1, 1, -1)])
+def test_sync_indicator_invalid(args):
+    with pytest.raises(cpdp.CpdpError):
+        cpdp.cpdp_is_sync_step(*args)
+
+
+# fake device addresses: 256-byte aligned, far apart, never dereferenced
+A = 1 << 40
+B = A + (1 << 36)
+C = A + 2 * (1 << 36)
+U = A + 3 * (1 << 36)
+V = A + 4 * (1 << 36)
+T0 = A + 5 * (1 << 36)
+
+GOOD = dict(W=4, P=1000, ld=1024, K=2, lr=0.1, mu=0.9, beta=0.5, alpha=1.0)
+
+
+def rec(**kw):
+    a = dict(GOOD, params=A, mom=B, grads=C, slow=U, anchor=V, pdt=0, gdt=0, mdt=0)
+    a.update(kw)
+    return cpdp.cpdp_reconcile(a["params"], a["mom"], a["grads"], a["slow"],
+                               a["anchor"], a["W"], a["P"], a["ld"], a["K"],
+                               a["lr"], a["mu"], a["beta"], a["alpha"],
+                               a["pdt"], a["gdt"], a["mdt"], None, check=False)
+
+
+def loc(**kw):
+    a = dict(GOOD, params=A, mom=B, grads=C, pdt=0, gdt=0, mdt=0)
+    a.update(kw)
+    return cpdp.cpdp_local_step(a["params"], a["mom"], a["grads"], a["W"],
+                                a["P"], a["ld"], a["K"], a["lr"], a["mu"],
+                                a["pdt"], a["gdt"], a["mdt"], None, check=False)
+
+
+def ini(**kw):
+    a = dict(GOOD, theta0=T0, params=A, mom=B, slow=U, anchor=V, pdt=0, mdt=0)
+    a.update(kw)
+    return cpdp.cpdp_state_init(a["theta0"], a["params"], a["mom"], a["slow"],
+                                a["anchor"], a["W"], a["P"], a["ld"], a["K"],
+                                a["pdt"], a["mdt"], None, check=False)
+
+
+E = cpdp
+SHAPE_CASES = [dict(W=0), dict(W=-3), dict(P=-1), dict(ld=999), dict(K=0),
+               dict(P=(1 << 42), ld=(1 << 42)), dict(P=8, ld=(1 << 58))]
+
+
+@pytest.mark.parametrize("kw", SHAPE_CASES)
+@pytest.mark.parametrize("fn", [rec, loc, ini])
+def test_bad_shape(fn, kw):
+    assert fn(**kw) == E.CPDP_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("kw", [
+    dict(lr=0.0), dict(lr=-0.1), dict(lr=float("nan")), dict(lr=float("inf")),
+    dict(mu=-0.1), dict(mu=1.0), dict(mu=float("nan"))])
+@pytest.mark.parametrize("fn", [rec, loc])
+def test_bad_lr_mu(fn, kw):
+    assert fn(**kw) == E.CPDP_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("kw", [
+    dict(beta=1.0), dict(beta=-0.01), dict(beta=float("nan")), dict(alpha=0.0),
+    dict(alpha=-1.0), dict(alpha=float("inf")), dict(alpha=float("nan"))])
+def test_bad_slowmo(kw):
+    assert rec(**kw) == E.CPDP_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("kw", [dict(pdt=2), dict(gdt=1), dict(mdt=1), dict(pdt=-1)])
+def test_bad_dtype(kw):
+    assert rec(**kw) == E.CPDP_ERR_DTYPE
+    kl = {k: v for k, v in kw.items()}
+    assert loc(**kl) == E.CPDP_ERR_DTYPE
+
+
+def test_bad_dtype_init():
+    assert ini(pdt=3) == E.CPDP_ERR_DTYPE
+    assert ini(mdt=1) == E.CPDP_ERR_DTYPE
+
+
+@pytest.mark.parametrize("name", ["params", "mom", "grads", "slow", "anchor"])
+def test_null(name):
+    assert rec(**{name: None}) == E.CPDP_ERR_NULL
+
+
+def test_null_init_and_local():
+    assert ini(theta0=None) == E.CPDP_ERR_NULL
+    assert loc(grads=None) == E.CPDP_ERR_NULL
+
+
+@pytest.mark.parametrize("name", ["params", "mom", "grads", "slow", "anchor"])
+def test_misaligned_pointer(name):
+    base = dict(params=A, mom=B, grads=C, slow=U, anchor=V)[name]
+    assert rec(**{name: base + 4}) == E.CPDP_ERR_MISALIGNED
+
+
+def test_misaligned_stride():
+    assert rec(P=1001, ld=1002) == E.CPDP_ERR_MISALIGNED  # 4008 B rows
+    assert loc(P=1001, ld=1002) == E.CPDP_ERR_MISALIGNED
+    # bf16 rows need ld % 8 == 0
+    assert rec(P=1000, ld=1004, pdt=1) == E.CPDP_ERR_MISALIGNED
+
+
+def test_overlap():
+    row_bytes = 1024 * 4
+    # grads starting inside the last used row of params
+    assert rec(grads=A + 3 * row_bytes + 16) == E.CPDP_ERR_OVERLAP
+    assert rec(anchor=U + 16) == E.CPDP_ERR_OVERLAP
+    assert rec(mom=A) == E.CPDP_ERR_OVERLAP
+    assert loc(mom=C) == E.CPDP_ERR_OVERLAP
+    assert ini(theta0=A + 64) == E.CPDP_ERR_OVERLAP
+
+
+def test_p_zero_is_noop_without_pointers():
+    assert rec(P=0, params=None, mom=None, grads=None, slow=None, anchor=None) == E.CPDP_OK
+    assert loc(P=0, params=None, mom=None, grads=None) == E.CPDP_OK
+    assert ini(P=0, theta0=None, params=None, mom=None, slow=None, anchor=None) == E.CPDP_OK
+
+
+def test_binding_raises():
+    with pytest.raises(cpdp.CpdpError, match="INVALID_ARG"):
+        cpdp.cpdp_reconcile(A, B, C, U, V, 0, 10, 16, 1, 0.1, 0.9, 0.5, 1.0)

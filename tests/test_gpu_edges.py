@@ -1,0 +1,133 @@
+"""Edge cases of the HIP path: ragged and empty sizes, row padding left
+untouched, NaN/Inf propagation, determinism, and coordinate independence."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_harness import Case, GpuRun, compare, log, oracle_inputs, run_parity
+from paper_2607_21224_amd import cpdp
+from paper_2607_21224_amd.state import CpdpState, Hyper
+
+pytestmark = pytest.mark.gpu
+
+RAGGED = [(W, P) for W in (1, 2, 3, 8, 32) for P in (1, 3, 4, 5, 7, 8, 9, 1023, 1025, 4097)]
+
+
+@pytest.mark.parametrize("W,P", RAGGED)
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_ragged_sizes_and_pad_canaries(W, P, dt):
+    """Every ragged size matches the oracle, and the padding columns
+    [P, ld) of every row keep their canary bytes."""
+    ld = ((P + 127) // 128) * 128 + 128
+    c = Case(W=W, P=P, K=2, lr=0.1, mu=0.9, beta=0.5, alpha=1.0, steps=4,
+             param_dt=dt, ld=ld, seed=P * 100 + W)
+    log(f"[ragged] W={W} P={P} dt={dt}")
+    refs = {}
+    th0, grads = oracle_inputs(c, np.arange(P))
+    oracle.run(th0, grads, W, c.K, c.steps, *c.hyper32(), param_dt=dt,
+               callback=lambda s, k, st: refs.__setitem__(s, st.copy()))
+    g = GpuRun(c)
+    canary = torch.tensor(-1280.0, dtype=torch.float32)  # exact in bf16
+    g.st.params[:, P:] = canary.to(g.st.params.dtype)
+    g.st.mom[:, P:] = canary
+    g.grads[:, P:] = canary
+    for s in range(1, c.steps + 1):
+        g.step(s)
+        compare(g.snapshot(), refs[s], dt, f"W={W} P={P} step {s}")
+    torch.cuda.synchronize()
+    assert (g.st.params[:, P:].float() == -1280.0).all()
+    assert (g.st.mom[:, P:] == -1280.0).all()
+
+
+def test_p_zero_is_noop():
+    st = CpdpState(4, 0, ld=64)
+    h = Hyper.fp32(0.1, 0.9, 0.5, 1.0)
+    g = torch.zeros((4, 64), device="cuda")
+    st.mom.fill_(7.0)
+    st.init(torch.zeros(1, device="cuda"))
+    st.local_step(g, h)
+    st.reconcile(g, h)
+    torch.cuda.synchronize()
+    assert (st.mom == 7.0).all()
+
+
+def test_nan_inf_propagation():
+    """A NaN in one replica's gradient reaches every replica through the
+    gradient mean at the next reconcile; an Inf likewise; positions match the
+    oracle."""
+    W, P, K = 4, 4096, 2
+    c = Case(W=W, P=P, K=K, lr=0.1, mu=0.9, beta=0.5, alpha=1.0, steps=4)
+    h = c.hyper32()
+    th0, grads = oracle_inputs(c, np.arange(P))
+    poison = {2: [(1, 17, np.nan), (3, 4095, np.inf)], 3: [(0, 100, -np.inf)]}
+
+    def gfun(step, W_, P_):
+        x = grads(step, W_, P_)
+        for (i, p, v) in poison.get(step, []):
+            x[i, p] = v
+        return x
+
+    refs = {}
+    oracle.run(th0, gfun, W, K, c.steps, *h,
+               callback=lambda s, k, st: refs.__setitem__(s, st.copy()))
+    g = GpuRun(c)
+    for s in range(1, c.steps + 1):
+        from synth import device as sdev
+        sdev.fill_grads(g.grads, P, c.seed, s, c.grad_sigma)
+        for (i, p, v) in poison.get(s, []):
+            g.grads[i, p] = float(v)
+        t = s
+        g.st.step(t, g.grads, g.h)
+        snap = g.snapshot()
+        compare(snap, refs[s], "f32", f"nan step {s}")
+    assert np.isnan(snap["params"][:, 17]).all()
+
+
+def test_bitwise_deterministic():
+    c = Case(W=8, P=100_003, K=4, lr=0.1, mu=0.9, beta=0.5, alpha=1.0, steps=8)
+    a, b = GpuRun(c), GpuRun(c)
+    for s in range(1, c.steps + 1):
+        a.step(s)
+        b.step(s)
+    sa, sb = a.snapshot(), b.snapshot()
+    for k in sa:
+        assert np.array_equal(sa[k], sb[k], equal_nan=True), k
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_subset_equals_full(dt):
+    """Coordinates are independent: a run over the first P_sub coordinates
+    (whose ragged tail takes the scalar path) is bitwise equal to the same
+    coordinates of a run over P_full (vector path)."""
+    full = Case(W=8, P=65_536, K=2, lr=0.1, mu=0.9, beta=0.5, alpha=1.0,
+                steps=6, param_dt=dt)
+    sub = Case(**{**full.__dict__, "P": 65_531})
+    a, b = GpuRun(full), GpuRun(sub)
+    for s in range(1, full.steps + 1):
+        a.step(s)
+        b.step(s)
+    sa, sb = a.snapshot(), b.snapshot()
+    for k in sa:
+        x = sa[k][..., :sub.P]
+        assert np.array_equal(x, sb[k], equal_nan=True), k
+
+
+def test_streams():
+    """Work enqueued on a non-default stream lands in order on that stream."""
+    s = torch.cuda.Stream()
+    c = Case(W=4, P=20_000, K=2, lr=0.1, mu=0.9, beta=0.5, alpha=1.0, steps=4)
+    with torch.cuda.stream(s):
+        run_parity(c, stream=s)
+
+
+def test_invalid_call_leaves_state_untouched():
+    st = CpdpState(2, 100)
+    st.init(torch.ones(100, device="cuda"))
+    torch.cuda.synchronize()
+    before = st.params.clone()
+    g = torch.zeros((2, st.ld), device="cuda")
+    with pytest.raises(cpdp.CpdpError):
+        st.reconcile(g, Hyper(0.1, 0.9, 1.5, 1.0))  # beta >= 1
+    torch.cuda.synchronize()
+    assert torch.equal(before, st.params)

@@ -1,0 +1,59 @@
+"""GPU parity: the HIP path (through the C ABI) against the oracle, element by
+element after every local step and every reconcile."""
+import pytest
+
+from gpu_harness import Case, run_parity, sample_indices
+from synth import WORKLOADS
+
+pytestmark = pytest.mark.gpu
+
+
+def case_of(name, seed=42, steps=None):
+    w = WORKLOADS[name]
+    return Case(W=w.W, P=w.P, K=w.K, lr=w.lr, mu=w.mu, beta=w.beta,
+                alpha=w.alpha, steps=steps or w.steps, param_dt=w.param_dt,
+                seed=seed, ld=w.ld, theta_sigma=w.theta_sigma,
+                grad_sigma=w.grad_sigma, outlier_rate=w.outlier_rate)
+
+
+@pytest.mark.parametrize("seed", [42, 123, 777])
+def test_tiny_every_coordinate(seed):
+    """W=4, P=262,144, K=2, 10 periods: the whole state after every step."""
+    run_parity(case_of("tiny", seed))
+
+
+@pytest.mark.parametrize("name", ["r50_100", "vit_s", "r50_200", "stress"])
+def test_full_size_sampled(name):
+    """Full-size workloads in the benchmark's launch configuration, compared
+    on both ends (ragged tail included), every tensor boundary and a random
+    sample of coordinates (coordinates are independent)."""
+    w = WORKLOADS[name]
+    idx = sample_indices(w.P, w.boundaries()[1:], n_random=1 << 15, seed=1)
+    run_parity(case_of(name), idx)
+
+
+SMALL = [
+    # K = 1: every step reconciles (synchronous DDP cadence)
+    Case(W=8, P=10_007, K=1, lr=0.1, mu=0.9, beta=0.3, alpha=1.0, steps=6),
+    # plain SGD local steps, no outer momentum, alpha != 1, run-time W
+    Case(W=5, P=4_099, K=3, lr=0.2, mu=0.0, beta=0.0, alpha=1.5, steps=9),
+    # epoch boundary not a multiple of K: forced sync at t = T
+    Case(W=4, P=3_001, K=4, lr=0.1, mu=0.9, beta=0.5, alpha=1.0, steps=12, T=6),
+    Case(W=16, P=2_053, K=8, lr=0.1, mu=0.9, beta=0.6, alpha=1.0, steps=16,
+         outlier_rate=0.01),
+    Case(W=32, P=1_031, K=4, lr=0.1, mu=0.9, beta=0.5, alpha=1.0, steps=8),
+    Case(W=32, P=5_003, K=4, lr=0.1, mu=0.9, beta=0.5, alpha=1.0, steps=8,
+         param_dt="bf16"),
+    Case(W=8, P=777, K=2, lr=0.05, mu=0.9, beta=0.7, alpha=0.75, steps=8,
+         param_dt="bf16"),
+    Case(W=3, P=1_000, K=2, lr=0.5, mu=0.5, beta=0.9, alpha=1.0, steps=10,
+         theta_sigma=1.0, grad_sigma=0.1),
+    Case(W=1, P=513, K=3, lr=0.1, mu=0.9, beta=0.5, alpha=1.0, steps=9),
+    Case(W=2, P=64, K=2, lr=0.1, mu=0.9, beta=0.5, alpha=1.0, steps=6, ld=128),
+]
+
+
+@pytest.mark.parametrize("c", SMALL, ids=lambda c: f"W{c.W}-P{c.P}-K{c.K}-{c.param_dt}"
+                         + (f"-T{c.T}" if c.T else ""))
+def test_small_variants(c):
+    run_parity(c)
