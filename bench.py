@@ -98,6 +98,9 @@ def main() -> int:
     ap.add_argument("--workload", default="r50_100")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=10.0)
+    ap.add_argument("--row-align-bytes", type=int, default=0,
+                    help="round each replica row up to a multiple of this many bytes "
+                         "(0 = the workload's default of 1 MiB)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -112,6 +115,10 @@ def main() -> int:
     from synth import device as sdev
 
     w = WORKLOADS[args.workload]
+    if args.row_align_bytes:
+        import dataclasses
+        assert args.row_align_bytes % 256 == 0
+        w = dataclasses.replace(w, row_align_bytes=args.row_align_bytes)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.Stream(device=dev)  # default priority

@@ -24,15 +24,22 @@
 namespace cpdp {
 namespace {
 
-constexpr int kBlock = 256;
+#ifndef CPDP_BLOCK
+#define CPDP_BLOCK 256
+#endif
+constexpr int kBlock = CPDP_BLOCK;
 constexpr int kVec = 4;
 
 // State tensors are streamed exactly once per call; nontemporal accesses keep
 // them from displacing anything useful in L2 / MALL.
-#ifndef CPDP_NONTEMPORAL
-#define CPDP_NONTEMPORAL 1
+#ifndef CPDP_NT_LOAD
+#define CPDP_NT_LOAD 1
 #endif
-constexpr bool kNT = CPDP_NONTEMPORAL != 0;
+#ifndef CPDP_NT_STORE
+#define CPDP_NT_STORE 1
+#endif
+constexpr bool kNTL = CPDP_NT_LOAD != 0;
+constexpr bool kNTS = CPDP_NT_STORE != 0;
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
@@ -139,11 +146,11 @@ __device__ __forceinline__ void init_chunk(const typename PS::T* theta0, typenam
     PS::template load<FULL, false>(theta0 + p0, n, th);
     for (int i = 0; i < W; ++i) {
         const int64_t off = (int64_t)i * ld + p0;
-        PS::template store<FULL, kNT>(params + off, n, th);
-        store_f32<FULL, kNT>(mom + off, n, zero);
+        PS::template store<FULL, kNTS>(params + off, n, th);
+        store_f32<FULL, kNTS>(mom + off, n, zero);
     }
-    store_f32<FULL, kNT>(slow + p0, n, zero);
-    store_f32<FULL, kNT>(anchor + p0, n, th);
+    store_f32<FULL, kNTS>(slow + p0, n, zero);
+    store_f32<FULL, kNTS>(anchor + p0, n, th);
 }
 
 template <class PS>
@@ -166,16 +173,16 @@ __device__ __forceinline__ void local_chunk(typename PS::T* params, float* mom,
                                             const float* grads, int64_t off, int n, float lr,
                                             float mu) {
     float g[kVec], m[kVec], th[kVec];
-    load_f32<FULL, kNT>(grads + off, n, g);
-    load_f32<FULL, kNT>(mom + off, n, m);
-    PS::template load<FULL, kNT>(params + off, n, th);
+    load_f32<FULL, kNTL>(grads + off, n, g);
+    load_f32<FULL, kNTL>(mom + off, n, m);
+    PS::template load<FULL, kNTL>(params + off, n, th);
 #pragma unroll
     for (int k = 0; k < kVec; ++k) {
         m[k] = fmaf(mu, m[k], g[k]);
         th[k] = fmaf(-lr, m[k], th[k]);
     }
-    store_f32<FULL, kNT>(mom + off, n, m);
-    PS::template store<FULL, kNT>(params + off, n, th);
+    store_f32<FULL, kNTS>(mom + off, n, m);
+    PS::template store<FULL, kNTS>(params + off, n, th);
 }
 
 template <class PS>
@@ -197,8 +204,17 @@ __global__ __launch_bounds__(kBlock) void local_step_kernel(
 // ---- fused reconcile ----------------------------------------------------------
 //
 // One thread owns 4 coordinates across all W replicas.  WT > 0 fixes W at
-// compile time (fully unrolled, all loads of a phase in flight together);
-// WT == 0 takes W at run time.
+// compile time (fully unrolled); WT == 0 takes W at run time.  Replicas are
+// visited in batches of kChunk: all loads of a batch are issued before any of
+// its stores.  The batching matters because the compiler cannot prove that
+// mom + i*ld and mom + j*ld never alias (ld is a run-time value), so a store
+// for replica i would otherwise hold back the loads of replica i+1 and the
+// thread would wait for one round trip to HBM per replica.
+
+#ifndef CPDP_RECON_CHUNK
+#define CPDP_RECON_CHUNK 8
+#endif
+constexpr int kChunk = CPDP_RECON_CHUNK;
 
 template <int WT, class PS, bool FULL>
 __device__ __forceinline__ void reconcile_chunk(typename PS::T* params, float* mom,
@@ -206,41 +222,55 @@ __device__ __forceinline__ void reconcile_chunk(typename PS::T* params, float* m
                                                 int W, int64_t ld, int64_t p0, int n, float lr,
                                                 float mu, float beta, float alpha_lr,
                                                 float inv_w) {
+    constexpr int C = WT > 0 ? (WT < kChunk ? WT : kChunk) : 1;
+    static_assert(WT <= 0 || WT % C == 0, "replica batches must tile W");
     const int nw = WT > 0 ? WT : W;
 
-    // gradient mean (the AllReduce of the synchronisation step), fixed order
-    float acc[kVec], g[kVec];
-    load_f32<FULL, kNT>(grads + p0, n, acc);
+    // gradient mean (the AllReduce of the synchronisation step): summed in
+    // the fixed order i = 0, 1, ..., W-1
+    float acc[kVec] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-    for (int i = 1; i < nw; ++i) {
-        load_f32<FULL, kNT>(grads + (int64_t)i * ld + p0, n, g);
+    for (int i0 = 0; i0 < nw; i0 += C) {
+        float g[C][kVec];
 #pragma unroll
-        for (int k = 0; k < kVec; ++k) acc[k] += g[k];
+        for (int c = 0; c < C; ++c)
+            load_f32<FULL, kNTL>(grads + (int64_t)(i0 + c) * ld + p0, n, g[c]);
+#pragma unroll
+        for (int c = 0; c < C; ++c)
+#pragma unroll
+            for (int k = 0; k < kVec; ++k) acc[k] += g[c][k];
     }
     float gbar[kVec];
 #pragma unroll
     for (int k = 0; k < kVec; ++k) gbar[k] = acc[k] * inv_w;
 
     float a[kVec], u[kVec];
-    load_f32<FULL, kNT>(anchor + p0, n, a);
-    load_f32<FULL, kNT>(slow + p0, n, u);
+    load_f32<FULL, kNTL>(anchor + p0, n, a);
+    load_f32<FULL, kNTL>(slow + p0, n, u);
 
     // synchronized optimizer step per replica, then the parameter mean taken
     // as a + mean(x_i - a) so the small difference keeps its precision
     float s[kVec] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-    for (int i = 0; i < nw; ++i) {
-        const int64_t off = (int64_t)i * ld + p0;
-        float m[kVec], th[kVec];
-        load_f32<FULL, kNT>(mom + off, n, m);
-        PS::template load<FULL, kNT>(params + off, n, th);
+    for (int i0 = 0; i0 < nw; i0 += C) {
+        float m[C][kVec], th[C][kVec];
 #pragma unroll
-        for (int k = 0; k < kVec; ++k) {
-            m[k] = fmaf(mu, m[k], gbar[k]);
-            const float x = PS::round(fmaf(-lr, m[k], th[k]));
-            s[k] += x - a[k];
+        for (int c = 0; c < C; ++c) {
+            const int64_t off = (int64_t)(i0 + c) * ld + p0;
+            load_f32<FULL, kNTL>(mom + off, n, m[c]);
+            PS::template load<FULL, kNTL>(params + off, n, th[c]);
         }
-        store_f32<FULL, kNT>(mom + off, n, m);
+#pragma unroll
+        for (int c = 0; c < C; ++c)
+#pragma unroll
+            for (int k = 0; k < kVec; ++k) {
+                m[c][k] = fmaf(mu, m[c][k], gbar[k]);
+                const float x = PS::round(fmaf(-lr, m[c][k], th[c][k]));
+                s[k] += x - a[k];
+            }
+#pragma unroll
+        for (int c = 0; c < C; ++c)
+            store_f32<FULL, kNTS>(mom + (int64_t)(i0 + c) * ld + p0, n, m[c]);
     }
 
     // SlowMo outer step: u <- beta u + (a - avg)/lr ; new = a - alpha lr u
@@ -250,13 +280,13 @@ __device__ __forceinline__ void reconcile_chunk(typename PS::T* params, float* m
         u[k] = fmaf(beta, u[k], -drift / lr);
         a[k] = fmaf(-alpha_lr, u[k], a[k]);
     }
-    store_f32<FULL, kNT>(slow + p0, n, u);
-    store_f32<FULL, kNT>(anchor + p0, n, a);
+    store_f32<FULL, kNTS>(slow + p0, n, u);
+    store_f32<FULL, kNTS>(anchor + p0, n, a);
 
     // copy the reconciled model back into every replica
 #pragma unroll
     for (int i = 0; i < nw; ++i)
-        PS::template store<FULL, kNT>(params + (int64_t)i * ld + p0, n, a);
+        PS::template store<FULL, kNTS>(params + (int64_t)i * ld + p0, n, a);
 }
 
 template <int WT, class PS>

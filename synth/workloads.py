@@ -73,11 +73,11 @@ class Workload:
     outlier_rate: float = 0.0
     outlier_scale: float = 100.0
     tensors: tuple = field(default=(), repr=False)
-    ld_align: int = 64             # replica stride rounded up to this many elements
+    row_align_bytes: int = 1 << 20  # replica rows rounded up to a multiple of this
 
     @property
     def ld(self) -> int:
-        return round_up(self.P, self.ld_align)
+        return round_up(self.P, self.row_align_bytes // self.param_bytes())
 
     @property
     def steps(self) -> int:
@@ -124,7 +124,7 @@ def _make() -> dict[str, Workload]:
                             tensors=r200),
         "stress": Workload("stress", W=32, P=100_000_000, K=4, lr=0.1, mu=0.9,
                            beta=0.5, alpha=1.0, periods=3, param_dt="bf16",
-                           ld_align=128, tensors=(("flat", 100_000_000),)),
+                           tensors=(("flat", 100_000_000),)),
     }
 
 
