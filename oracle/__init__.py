@@ -55,6 +55,10 @@ def load(path: str = _LIB_PATH) -> ctypes.CDLL:
     lib.oracle_reconcile_vform.argtypes = [i, i64, i, i, i, _D, _D, _D, _D,
                                            _D, d, d, d]
     lib.oracle_reconcile_vform.restype = None
+    lib.oracle_localsgd_sync.argtypes = [i, i64, i, i, i, _D, _D, _D, _D, d, d]
+    lib.oracle_localsgd_sync.restype = None
+    lib.oracle_ddp_step.argtypes = [i, i64, i, i, i, _D, _D, _D, d, d]
+    lib.oracle_ddp_step.restype = None
     return lib
 
 
@@ -153,6 +157,27 @@ def reconcile_vform(st: OracleState, grads, lr: float, mu: float,
                                  float(mu), float(beta))
 
 
+def localsgd_sync(st: OracleState, grads, lr: float, mu: float) -> None:
+    """LocalSGD synchronisation step (Sec. 5.3): local optimizer step, then
+    parameter averaging; the average is also written to st.anchor."""
+    g = _grads(st, grads)
+    st._l.oracle_localsgd_sync(st.W, st.P, _DT[st.param_dt], _DT[st.mom_dt],
+                               _DT[st.aux_dt], _ptr(st.params), _ptr(st.mom),
+                               _ptr(g), _ptr(st.anchor), float(lr), float(mu))
+
+
+def ddp_step(st: OracleState, grads, lr: float, mu: float) -> None:
+    """Synchronous DDP step (Sec. 3.1, Sec. 5.3): gradient mean, then the same
+    optimizer step on every worker; no parameter averaging."""
+    g = _grads(st, grads)
+    st._l.oracle_ddp_step(st.W, st.P, _DT[st.param_dt], _DT[st.mom_dt],
+                          _DT[st.aux_dt], _ptr(st.params), _ptr(st.mom), _ptr(g),
+                          float(lr), float(mu))
+
+
+METHODS = ("cpdp", "localsgd", "ddp")
+
+
 def is_sync_step(t: int, K: int, T: int = 0) -> bool:
     """Synchronisation indicator.
 
@@ -168,20 +193,31 @@ def is_sync_step(t: int, K: int, T: int = 0) -> bool:
 
 def run(theta0, grad_fn, W: int, K: int, n_steps: int, lr: float, mu: float,
         beta: float, alpha: float, T: int = 0, param_dt="f32", mom_dt="f32",
-        aux_dt="f32", callback=None, use=None) -> OracleState:
+        aux_dt="f32", callback=None, use=None, method: str = "cpdp") -> OracleState:
     """Algorithm 1 driven for n_steps steps.
 
     grad_fn(step, W, P) returns the (W, P) gradients of 1-based global step
     ``step`` (the stand-in for the backward pass).  With T > 0 the within-epoch
     step counter restarts every T steps.  callback(step, kind, state) is called
-    after every step with kind "local" or "reconcile".
+    after every step with kind "local" or "reconcile".  ``method`` selects the
+    synchronisation step: "cpdp" (Algorithm 1), "localsgd" (parameter
+    averaging only) or "ddp" (gradient averaging at every step; K is ignored,
+    DDP being the K = 1 schedule).
     """
+    if method not in METHODS:
+        raise ValueError(method)
     st = state_init(theta0, W, param_dt, mom_dt, aux_dt, use)
     for step in range(1, n_steps + 1):
         t = ((step - 1) % T) + 1 if T > 0 else step
         g = grad_fn(step, W, st.P)
-        if is_sync_step(t, K, T):
-            reconcile(st, g, lr, mu, beta, alpha)
+        if method == "ddp":
+            ddp_step(st, g, lr, mu)
+            kind = "reconcile"
+        elif is_sync_step(t, K, T):
+            if method == "cpdp":
+                reconcile(st, g, lr, mu, beta, alpha)
+            else:
+                localsgd_sync(st, g, lr, mu)
             kind = "reconcile"
         else:
             local_step(st, g, lr, mu)

@@ -22,6 +22,11 @@
  *                               gradient mean -> optimizer step with the mean
  *                               gradient (momentum buffers stay local) ->
  *                               parameter mean -> SlowMo -> copy back.
+ *   - baselines of Sec. 5.3     oracle_localsgd_sync (local step, then
+ *                               parameter averaging; no gradient AllReduce,
+ *                               no SlowMo) and oracle_ddp_step (gradient
+ *                               mean and the same step on every worker, no
+ *                               averaging), run with the same cadence.
  *   - SlowMo, u-form            u <- beta*u + (ref - avg)/lr,
  *                               new = ref - alpha*lr*u.  With v = -lr*u,
  *                               alpha = 1 and a constant lr this is exactly
@@ -189,5 +194,55 @@ void oracle_reconcile_vform(int W, int64_t P, int param_dt, int mom_dt,
         anchor[p] = fresh;
         for (int i = 0; i < W; ++i)
             params[(int64_t)i * P + p] = store_as(param_dt, fresh);
+    }
+}
+
+/*
+ * LocalSGD synchronisation step (Sec. 5.3, second baseline; Table 2 row
+ * "LocalSGD"): no gradient AllReduce and no SlowMo.  Every worker takes its
+ * own optimizer step with its local gradient, then the parameters are
+ * averaged and the average is copied back into every worker.  The averaged
+ * model is also stored in `anchor` (if not NULL) as the reference model.
+ * Momentum buffers stay local.
+ */
+void oracle_localsgd_sync(int W, int64_t P, int param_dt, int mom_dt,
+                          int aux_dt, double* params, double* mom,
+                          const double* grads, double* anchor, double lr,
+                          double mu) {
+    for (int64_t p = 0; p < P; ++p) {
+        double xsum = 0.0;
+        for (int i = 0; i < W; ++i) {
+            int64_t k = (int64_t)i * P + p;
+            double buf = store_as(mom_dt, mu * mom[k] + grads[k]);
+            mom[k] = buf;
+            xsum += store_as(param_dt, params[k] - lr * buf);
+        }
+        double avg = store_as(aux_dt, xsum / (double)W);
+        if (anchor) anchor[p] = avg;
+        for (int i = 0; i < W; ++i)
+            params[(int64_t)i * P + p] = store_as(param_dt, avg);
+    }
+}
+
+/*
+ * Synchronous DDP step (Sec. 3.1 Eqs. for gbar and the update; Sec. 5.3,
+ * first baseline): the gradient is averaged over the workers at every step
+ * and every worker applies the same optimizer step with it; there is no
+ * parameter averaging.  Momentum buffers are per worker (they stay equal when
+ * the workers start equal).
+ */
+void oracle_ddp_step(int W, int64_t P, int param_dt, int mom_dt, int aux_dt,
+                     double* params, double* mom, const double* grads,
+                     double lr, double mu) {
+    for (int64_t p = 0; p < P; ++p) {
+        double gsum = 0.0;
+        for (int i = 0; i < W; ++i) gsum += grads[(int64_t)i * P + p];
+        double gbar = store_as(aux_dt, gsum / (double)W);
+        for (int i = 0; i < W; ++i) {
+            int64_t k = (int64_t)i * P + p;
+            double buf = store_as(mom_dt, mu * mom[k] + gbar);
+            mom[k] = buf;
+            params[k] = store_as(param_dt, params[k] - lr * buf);
+        }
     }
 }

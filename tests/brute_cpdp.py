@@ -13,8 +13,12 @@ from __future__ import annotations
 from fractions import Fraction
 
 
-def run_exact(theta0, grads, W, K, lr, mu, beta, alpha=1, T=0):
-    """Run Algorithm 1 exactly.
+def run_exact(theta0, grads, W, K, lr, mu, beta, alpha=1, T=0, method="cpdp"):
+    """Run Algorithm 1 exactly (method "cpdp"), or the two baselines of
+    Sec. 5.3 with the same optimizer: "localsgd" (local steps; at a sync step
+    each worker steps on its own gradient, then parameters are averaged, no
+    SlowMo) and "ddp" (every step averages the gradient; no parameter
+    averaging).
 
     theta0: list of P numbers; grads: list over steps of W lists of P numbers
     (grads[s][i][p] is g_{i, s+1}).  Returns a list with one snapshot per step:
@@ -31,9 +35,24 @@ def run_exact(theta0, grads, W, K, lr, mu, beta, alpha=1, T=0):
     for s, g_step in enumerate(grads):
         step = s + 1
         t = ((step - 1) % T) + 1 if T > 0 else step
-        sync = (t % K == 0) or (T > 0 and t == T)
+        sync = (t % K == 0) or (T > 0 and t == T) or method == "ddp"
         g = [[F(x) for x in row] for row in g_step]
-        if not sync:
+        if sync and method == "ddp":
+            for p in range(P):
+                gbar = sum(g[i][p] for i in range(W)) / W
+                for i in range(W):
+                    buf[i][p] = mu * buf[i][p] + gbar
+                    theta[i][p] = theta[i][p] - lr * buf[i][p]
+        elif sync and method == "localsgd":
+            for p in range(P):
+                for i in range(W):
+                    buf[i][p] = mu * buf[i][p] + g[i][p]
+                    theta[i][p] = theta[i][p] - lr * buf[i][p]
+                avg = sum(theta[i][p] for i in range(W)) / W
+                for i in range(W):
+                    theta[i][p] = avg
+                ref[p] = avg
+        elif not sync:
             for i in range(W):
                 for p in range(P):
                     buf[i][p] = mu * buf[i][p] + g[i][p]

@@ -73,7 +73,7 @@ def _rand_dyadic(rng, shape, scale=8):
     return rng.integers(-4 * scale, 4 * scale + 1, size=shape) / scale
 
 
-def pin_brute_force(use=None, cases=12, seed=5):
+def pin_brute_force(use=None, cases=12, seed=5, methods=("cpdp",)):
     """Exact rational Algorithm 1 (tests/brute_cpdp.py) on tiny random inputs."""
     rng = np.random.default_rng(seed)
     for c in range(cases):
@@ -86,19 +86,20 @@ def pin_brute_force(use=None, cases=12, seed=5):
         mu = float(rng.choice([0.0, 0.5, 0.9, 0.75]))
         beta = float(rng.choice([0.0, 0.5, 0.3, 0.875]))
         alpha = float(rng.choice([1.0, 1.0, 0.5, 1.5]))
+        method = methods[c % len(methods)]
         theta0 = _rand_dyadic(rng, P)
         grads = [_rand_dyadic(rng, (W, P)) for _ in range(n)]
         exact = run_exact([Fraction(x) for x in theta0],
                           [[[Fraction(x) for x in r] for r in g] for g in grads],
                           W, K, Fraction(lr), Fraction(mu), Fraction(beta),
-                          Fraction(alpha), T=T)
+                          Fraction(alpha), T=T, method=method)
         snaps = []
         oracle.run(theta0, lambda step, W_, P_: grads[step - 1], W, K, n, lr,
                    mu, beta, alpha, T=T, param_dt="f64", mom_dt="f64",
-                   aux_dt="f64", use=use,
+                   aux_dt="f64", use=use, method=method,
                    callback=lambda step, kind, st: snaps.append((kind, st.copy())))
         for s, ((kind, st), ex) in enumerate(zip(snaps, exact)):
-            tag = f"case {c} step {s + 1} (W={W} P={P} K={K} T={T})"
+            tag = f"case {c} {method} step {s + 1} (W={W} P={P} K={K} T={T})"
             assert kind == ex["kind"], tag
             _close(st.params, [[float(x) for x in r] for r in ex["params"]],
                    1e-12, 1e-12, tag + " params")
@@ -174,10 +175,13 @@ def pin_closed_form_momentum(use=None):
             _close(st.params, np.tile(th, (W, 1)), 1e-12, 1e-12, f"theta t={t}")
 
 
-def _torch_reference(theta0, grads, W, K, lr, mu):
-    """Sec. 4.2 implementation with beta = 0, alpha = 1, written with
-    torch.optim.SGD: per-worker optimizers, averaged gradient on sync steps,
-    then parameter averaging copied back into every worker (buffers untouched).
+def _torch_reference(theta0, grads, W, K, lr, mu, method="cpdp"):
+    """The three strategies of Sec. 5.3 written with torch.optim.SGD, one
+    optimizer per worker (local momentum buffers, Sec. 4.2):
+      cpdp (beta = 0, alpha = 1): averaged gradient on sync steps, then
+        parameter averaging copied back into every worker;
+      localsgd: local gradient on every step, parameter averaging on sync steps;
+      ddp: averaged gradient on every step, no parameter averaging.
     """
     import torch
     ps = [torch.nn.Parameter(torch.tensor(theta0, dtype=torch.float64))
@@ -185,18 +189,19 @@ def _torch_reference(theta0, grads, W, K, lr, mu):
     opts = [torch.optim.SGD([p], lr=lr, momentum=mu) for p in ps]
     out = []
     for s, g in enumerate(grads, start=1):
-        sync = s % K == 0
+        sync = s % K == 0 or method == "ddp"
+        use_gbar = sync and method in ("cpdp", "ddp")
         gbar = g.mean(axis=0)
         for i in range(W):
-            ps[i].grad = torch.tensor(gbar if sync else g[i])
+            ps[i].grad = torch.tensor(gbar if use_gbar else g[i])
             opts[i].step()
-        if sync:
+        if sync and method in ("cpdp", "localsgd"):
             avg = torch.stack([p.detach() for p in ps]).mean(0)
             for p in ps:
                 p.data.copy_(avg)
         bufs = np.stack([
             opts[i].state[ps[i]]["momentum_buffer"].numpy().copy()
-            if mu > 0 else (gbar if sync else g[i]) for i in range(W)])
+            if mu > 0 else (gbar if use_gbar else g[i]) for i in range(W)])
         out.append((np.stack([p.detach().numpy().copy() for p in ps]), bufs))
     return out
 
@@ -322,3 +327,55 @@ ALL_PINS = [pin_worked_example, pin_worked_example_vform, pin_brute_force,
             pin_closed_form_slowmo, pin_closed_form_momentum, pin_torch_sgd,
             pin_permutation, pin_fixed_point, pin_identical_workers,
             pin_linearity, pin_rounding]
+
+
+def pin_torch_baselines(use=None):
+    """LocalSGD and DDP (Sec. 5.3) against per-worker torch.optim.SGD."""
+    rng = np.random.default_rng(17)
+    for method in ("localsgd", "ddp"):
+        for (W, K, mu, lr) in [(4, 2, 0.9, 0.1), (3, 3, 0.5, 0.2), (1, 2, 0.9, 0.1),
+                               (5, 4, 0.0, 0.05)]:
+            P = 5
+            n = 3 * K + 1
+            theta0 = rng.normal(0, 1, P)
+            grads = [rng.normal(0, 1, (W, P)) for _ in range(n)]
+            ref = _torch_reference(theta0, grads, W, K, lr, mu, method)
+            rec = []
+            oracle.run(theta0, lambda s, W_, P_: grads[s - 1], W, K, n, lr, mu,
+                       0.5, 1.0, param_dt="f64", mom_dt="f64", aux_dt="f64",
+                       use=use, method=method,
+                       callback=lambda s, kind, st: rec.append(st.copy()))
+            for s, (st, (p_ref, b_ref)) in enumerate(zip(rec, ref), start=1):
+                tag = f"{method} W={W} K={K} s={s}"
+                _close(st.params, p_ref, 1e-12, 1e-12, tag + " params")
+                _close(st.mom, b_ref, 1e-12, 1e-12, tag + " mom")
+                assert not st.slow.any(), tag + ": SlowMo state must stay 0"
+
+
+def pin_brute_force_baselines(use=None):
+    pin_brute_force(use, cases=10, seed=8, methods=("localsgd", "ddp"))
+
+
+def pin_localsgd_closed_form(use=None):
+    """LocalSGD, mu = 0, worker i always sees the constant gradient c_i: every
+    period moves the average by K lr mean(c), so after n periods all workers
+    hold theta0 - n K lr mean(c); j local steps into a period, worker i holds
+    that minus j lr c_i."""
+    c = np.array([0.5, -1.25, 2.0])
+    W, K, lr = 3, 4, 0.1
+    theta0 = np.array([1.0, -2.0])
+    rec = []
+    oracle.run(theta0, lambda s, W_, P_: np.tile(c[:, None], (1, P_)), W, K,
+               3 * K, lr, 0.0, 0.7, 1.0, param_dt="f64", mom_dt="f64",
+               aux_dt="f64", use=use, method="localsgd",
+               callback=lambda s, kind, st: rec.append((s, st.copy())))
+    for s, st in rec:
+        n, j = divmod(s, K)
+        base = theta0 - n * K * lr * c.mean()
+        want = base[None, :] - j * lr * c[:, None]
+        _close(st.params, want, 1e-12, 1e-12, f"localsgd closed form s={s}")
+        if j == 0:
+            _close(st.anchor, base, 1e-12, 1e-12, f"localsgd anchor s={s}")
+
+
+ALL_PINS += [pin_torch_baselines, pin_brute_force_baselines, pin_localsgd_closed_form]

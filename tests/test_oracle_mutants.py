@@ -45,6 +45,14 @@ MUTANTS = [
     ("f32_rounding_dropped", "return (double)(float)x;", "return x;", 0),
     ("vform_drops_beta", "beta * velocity[p] + delta", "velocity[p] + delta", 0),
     ("vform_delta_sign", "double delta = avg - ref;", "double delta = ref - avg;", 0),
+    ("localsgd_not_broadcast", "params[(int64_t)i * P + p] = store_as(param_dt, avg);", ";", 0),
+    ("localsgd_anchor_skipped", "if (anchor) anchor[p] = avg;", "", 0),
+    ("localsgd_grad_of_replica0", "mu * mom[k] + grads[k]", "mu * mom[k] + grads[p]", 1),
+    ("localsgd_avg_wrong_divisor", "store_as(aux_dt, xsum / (double)W)",
+     "store_as(aux_dt, xsum / (double)(W + 1))", 0),
+    ("ddp_uses_local_grad", "mu * mom[k] + gbar", "mu * mom[k] + grads[k]", 2),
+    ("ddp_gbar_not_divided", "gsum / (double)W", "gsum", 2),
+    ("ddp_drops_mu", "mu * mom[k] + gbar", "mom[k] + gbar", 2),
 ]
 
 
