@@ -96,6 +96,8 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=100, help="timed CPDP periods")
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="r50_100")
+    ap.add_argument("--method", default="cpdp", choices=["cpdp", "localsgd", "ddp"],
+                    help="synchronisation strategy (Sec. 5.3); cpdp is the paper's method")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=10.0)
     ap.add_argument("--row-align-bytes", type=int, default=0,
@@ -149,7 +151,7 @@ def main() -> int:
                 e0 = torch.cuda.Event(enable_timing=True)
                 e1 = torch.cuda.Event(enable_timing=True)
                 e0.record(stream)
-            kind = st.step(s, grads[s - 1], h, 0, stream)
+            kind = st.step(s, grads[s - 1], h, 0, stream, method=args.method)
             if evs is not None:
                 e1.record(stream)
                 evs.append((kind, e0, e1))
@@ -175,6 +177,7 @@ def main() -> int:
     dur = {"reconcile": [], "local": []}
     for kind, e0, e1 in evs:
         dur[kind].append(e0.elapsed_time(e1))
+    sync_kernel = {"cpdp": "reconcile", "localsgd": "localsgd_sync", "ddp": "ddp_step"}[args.method]
     rec_ms = sum(dur["reconcile"]) / len(dur["reconcile"])
     loc_ms = sum(dur["local"]) / len(dur["local"]) if dur["local"] else None
 
@@ -191,7 +194,7 @@ def main() -> int:
     torch.cuda.synchronize()
     copy_gbps = 2 * 4 * n_copy * reps / (c0.elapsed_time(c1) * 1e-3) / 1e9
 
-    rec_bytes = w.reconcile_bytes()
+    rec_bytes = w.sync_bytes(args.method)
     loc_bytes = w.local_step_bytes()
     rec_gbps = rec_bytes / (rec_ms * 1e-3) / 1e9
     wp = w.W * w.P
@@ -217,8 +220,13 @@ def main() -> int:
         "config": {"workload": f"{w.name}: W={w.W} replicas, P={w.P} ({w.param_dt} params), "
                                f"K={w.K}, lr={w.lr}, mu={w.mu}, beta={w.beta}, alpha={w.alpha}",
                    "W": w.W, "P": w.P, "ld": w.ld, "K": w.K,
-                   "step": f"one CPDP period: {w.K - 1} local steps + 1 reconcile"},
-        "reconcile": {"replica_params_per_s": wp / (rec_ms * 1e-3),
+                   "method": args.method,
+                   "step": (f"{w.K} DDP steps (K=1 schedule), same gradients as a CPDP period"
+                            if args.method == "ddp" else
+                            f"one period: {w.K - 1} local steps + 1 {sync_kernel}")},
+        "method": args.method,
+        "sync_kernel": sync_kernel,
+        sync_kernel: {"replica_params_per_s": wp / (rec_ms * 1e-3),
                       "GB_per_s": round(rec_gbps, 1),
                       "frac_of_hbm_peak": round(rec_gbps / HBM_PEAK_GBPS, 4),
                       "ms": round(rec_ms, 5)},
@@ -227,7 +235,7 @@ def main() -> int:
             "GB_per_s": round(loc_bytes / (loc_ms * 1e-3) / 1e9, 1),
             "frac_of_hbm_peak": round(loc_bytes / (loc_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
             "ms": round(loc_ms, 5)},
-        "roofline": roofline("reconcile", rec_bytes, rec_ms),
+        "roofline": roofline(sync_kernel, rec_bytes, rec_ms),
         "roofline_local_step": None if loc_ms is None else roofline("local_step", loc_bytes, loc_ms),
         "copy_ceiling_GBps": round(copy_gbps, 1),
         "wall_s_timed_region": round(wall, 4),

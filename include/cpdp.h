@@ -105,6 +105,34 @@ int cpdp_reconcile(void* params, void* mom, const void* grads,
                    void* stream);
 
 /*
+ * LocalSGD synchronisation step, the second baseline of Sec. 5.3 (Table 2,
+ * one parameter AllReduce per period): no gradient mean and no SlowMo.  Per
+ * coordinate p < P:
+ *   mom_i   <- mu * mom_i + grad_i          (each replica's own gradient)
+ *   x_i      = param_i - lr * mom_i         (rounded to param_dt)
+ *   avg      = (1/W) * sum_i x_i
+ *   param_i <- avg for every i;  anchor <- avg if anchor != NULL
+ * Arguments and layout as cpdp_reconcile; anchor is optional ([P] fp32).
+ */
+int cpdp_localsgd_sync(void* params, void* mom, const void* grads,
+                       float* anchor, int W, int64_t P, int64_t ld, int K,
+                       float lr, float mu, int param_dt, int grad_dt,
+                       int mom_dt, void* stream);
+
+/*
+ * Synchronous DDP step, the first baseline of Sec. 5.3 (Sec. 3.1: gradient
+ * AllReduce and identical updates at every step, no parameter averaging).
+ * Called at every step (the K = 1 schedule).  Per coordinate p < P:
+ *   gbar     = (1/W) * sum_i grad_i         (fixed order i = 0..W-1)
+ *   mom_i   <- mu * mom_i + gbar
+ *   param_i <- param_i - lr * mom_i
+ * Arguments and layout as cpdp_local_step.
+ */
+int cpdp_ddp_step(void* params, void* mom, const void* grads, int W,
+                  int64_t P, int64_t ld, float lr, float mu, int param_dt,
+                  int grad_dt, int mom_dt, void* stream);
+
+/*
  * Synchronisation indicator (Sec. 3.2) with the forced synchronisation at the
  * end of an epoch (Sec. 3.1, Sec. 4.2).  Host only, no GPU work.
  *   t: 1-based step counter inside the epoch; K: period (>= 1);

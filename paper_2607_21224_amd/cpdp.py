@@ -33,7 +33,8 @@ DTYPES = {"f32": CPDP_F32, "bf16": CPDP_BF16}
 
 # every symbol declared in include/cpdp.h
 EXPORTS = ("cpdp_state_init", "cpdp_local_step", "cpdp_reconcile",
-           "cpdp_is_sync_step", "cpdp_status_str")
+           "cpdp_localsgd_sync", "cpdp_ddp_step", "cpdp_is_sync_step",
+           "cpdp_status_str")
 
 
 def _load() -> ctypes.CDLL:
@@ -52,11 +53,13 @@ def _load() -> ctypes.CDLL:
     lib.cpdp_local_step.argtypes = [vp, vp, vp, i, i64, i64, i, f, f, i, i, i, vp]
     lib.cpdp_reconcile.argtypes = [vp, vp, vp, vp, vp, i, i64, i64, i, f, f, f, f,
                                    i, i, i, vp]
+    lib.cpdp_localsgd_sync.argtypes = [vp, vp, vp, vp, i, i64, i64, i, f, f, i, i, i, vp]
+    lib.cpdp_ddp_step.argtypes = [vp, vp, vp, i, i64, i64, f, f, i, i, i, vp]
     lib.cpdp_is_sync_step.argtypes = [i64, i, i64]
     lib.cpdp_status_str.argtypes = [i]
     lib.cpdp_status_str.restype = ctypes.c_char_p
     for name in ("cpdp_state_init", "cpdp_local_step", "cpdp_reconcile",
-                 "cpdp_is_sync_step"):
+                 "cpdp_localsgd_sync", "cpdp_ddp_step", "cpdp_is_sync_step"):
         getattr(lib, name).restype = ctypes.c_int
     return lib
 
@@ -135,3 +138,21 @@ def cpdp_reconcile(params, mom, grads, slow_mom, anchor, W, P, ld, K, lr, mu,
                            float(alpha), _dt(param_dt), _dt(grad_dt),
                            _dt(mom_dt), _stream(stream))
     return _done(s, "cpdp_reconcile", check)
+
+
+def cpdp_localsgd_sync(params, mom, grads, anchor, W, P, ld, K, lr, mu,
+                       param_dt=CPDP_F32, grad_dt=CPDP_F32, mom_dt=CPDP_F32,
+                       stream=None, check=True):
+    s = lib.cpdp_localsgd_sync(_addr(params), _addr(mom), _addr(grads),
+                               _addr(anchor), int(W), int(P), int(ld), int(K),
+                               float(lr), float(mu), _dt(param_dt), _dt(grad_dt),
+                               _dt(mom_dt), _stream(stream))
+    return _done(s, "cpdp_localsgd_sync", check)
+
+
+def cpdp_ddp_step(params, mom, grads, W, P, ld, lr, mu, param_dt=CPDP_F32,
+                  grad_dt=CPDP_F32, mom_dt=CPDP_F32, stream=None, check=True):
+    s = lib.cpdp_ddp_step(_addr(params), _addr(mom), _addr(grads), int(W),
+                          int(P), int(ld), float(lr), float(mu), _dt(param_dt),
+                          _dt(grad_dt), _dt(mom_dt), _stream(stream))
+    return _done(s, "cpdp_ddp_step", check)

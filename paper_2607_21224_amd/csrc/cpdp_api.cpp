@@ -134,10 +134,48 @@ int cpdp_reconcile(void* params, void* mom, const void* grads, float* slow_mom, 
                             rows(grads, W, P, ld, 4), vec(slow_mom, P, 4), vec(anchor, P, 4)};
     const size_t row_es[] = {sp, 4, 4, 0, 0};
     if (int s = check_pointers(ptrs, ranges, row_es, 5, ld)) return s;
-    return hip_status(cpdp::launch_reconcile(param_kind(param_dt), params,
-                                             static_cast<float*>(mom),
-                                             static_cast<const float*>(grads), slow_mom, anchor,
-                                             W, P, ld, lr, mu, beta, alpha, stream));
+    return hip_status(cpdp::launch_sync(cpdp::Sync::CPDP, param_kind(param_dt), params,
+                                        static_cast<float*>(mom), static_cast<const float*>(grads),
+                                        slow_mom, anchor, W, P, ld, lr, mu, beta, alpha, stream));
+}
+
+int cpdp_localsgd_sync(void* params, void* mom, const void* grads, float* anchor, int W,
+                       int64_t P, int64_t ld, int K, float lr, float mu, int param_dt,
+                       int grad_dt, int mom_dt, void* stream) {
+    if (int s = check_shape(W, P, ld, K)) return s;
+    if (int s = check_lr_mu(lr, mu)) return s;
+    if (!is_dtype(param_dt) || grad_dt != CPDP_F32 || mom_dt != CPDP_F32) return CPDP_ERR_DTYPE;
+    if (P == 0) return CPDP_OK;
+    if (!cpdp::grid_fits(1, P)) return CPDP_ERR_INVALID_ARG;
+    const size_t sp = esize(param_dt);
+    // anchor is optional: validate it only when given
+    const int n = anchor != nullptr ? 4 : 3;
+    const void* ptrs[] = {params, mom, grads, anchor};
+    const Range ranges[] = {rows(params, W, P, ld, sp), rows(mom, W, P, ld, 4),
+                            rows(grads, W, P, ld, 4), vec(anchor, P, 4)};
+    const size_t row_es[] = {sp, 4, 4, 0};
+    if (int s = check_pointers(ptrs, ranges, row_es, n, ld)) return s;
+    return hip_status(cpdp::launch_sync(cpdp::Sync::LocalSGD, param_kind(param_dt), params,
+                                        static_cast<float*>(mom), static_cast<const float*>(grads),
+                                        nullptr, anchor, W, P, ld, lr, mu, 0.0f, 1.0f, stream));
+}
+
+int cpdp_ddp_step(void* params, void* mom, const void* grads, int W, int64_t P, int64_t ld,
+                  float lr, float mu, int param_dt, int grad_dt, int mom_dt, void* stream) {
+    if (int s = check_shape(W, P, ld, 1)) return s;
+    if (int s = check_lr_mu(lr, mu)) return s;
+    if (!is_dtype(param_dt) || grad_dt != CPDP_F32 || mom_dt != CPDP_F32) return CPDP_ERR_DTYPE;
+    if (P == 0) return CPDP_OK;
+    if (!cpdp::grid_fits(1, P)) return CPDP_ERR_INVALID_ARG;
+    const size_t sp = esize(param_dt);
+    const void* ptrs[] = {params, mom, grads};
+    const Range ranges[] = {rows(params, W, P, ld, sp), rows(mom, W, P, ld, 4),
+                            rows(grads, W, P, ld, 4)};
+    const size_t row_es[] = {sp, 4, 4};
+    if (int s = check_pointers(ptrs, ranges, row_es, 3, ld)) return s;
+    return hip_status(cpdp::launch_sync(cpdp::Sync::DDP, param_kind(param_dt), params,
+                                        static_cast<float*>(mom), static_cast<const float*>(grads),
+                                        nullptr, nullptr, W, P, ld, lr, mu, 0.0f, 1.0f, stream));
 }
 
 int cpdp_is_sync_step(int64_t t, int K, int64_t T) {

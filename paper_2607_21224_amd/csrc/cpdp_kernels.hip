@@ -201,62 +201,76 @@ __global__ __launch_bounds__(kBlock) void local_step_kernel(
         local_chunk<PS, false>(params, mom, grads, off, (int)(P - p0), lr, mu);
 }
 
-// ---- fused reconcile ----------------------------------------------------------
+// ---- fused synchronisation steps ----------------------------------------------
 //
 // One thread owns 4 coordinates across all W replicas.  WT > 0 fixes W at
 // compile time (fully unrolled); WT == 0 takes W at run time.  Replicas are
 // visited in batches of kChunk: all loads of a batch are issued before any of
 // its stores.  The batching matters because the compiler cannot prove that
 // mom + i*ld and mom + j*ld never alias (ld is a run-time value), so a store
-// for replica i would otherwise hold back the loads of replica i+1 and the
-// thread would wait for one round trip to HBM per replica.
+// for replica i would otherwise hold back the loads of replica i+1.
+//
+// Sync::CPDP      gradient mean, synchronized optimizer step, parameter mean,
+//                 SlowMo, copy-back (the reconcile).
+// Sync::LocalSGD  each replica steps on its own gradient, then the parameter
+//                 mean is copied back (no gradient mean, no SlowMo).
+// Sync::DDP       gradient mean and the same optimizer step on every replica,
+//                 no parameter mean.
 
 #ifndef CPDP_RECON_CHUNK
 #define CPDP_RECON_CHUNK 8
 #endif
 constexpr int kChunk = CPDP_RECON_CHUNK;
 
-template <int WT, class PS, bool FULL>
-__device__ __forceinline__ void reconcile_chunk(typename PS::T* params, float* mom,
-                                                const float* grads, float* slow, float* anchor,
-                                                int W, int64_t ld, int64_t p0, int n, float lr,
-                                                float mu, float beta, float alpha_lr,
-                                                float inv_w) {
+template <Sync M, int WT, class PS, bool FULL>
+__device__ __forceinline__ void sync_chunk(typename PS::T* params, float* mom,
+                                           const float* grads, float* slow, float* anchor,
+                                           int W, int64_t ld, int64_t p0, int n, float lr,
+                                           float mu, float beta, float alpha_lr,
+                                           float inv_w) {
     constexpr int C = WT > 0 ? (WT < kChunk ? WT : kChunk) : 1;
     static_assert(WT <= 0 || WT % C == 0, "replica batches must tile W");
     const int nw = WT > 0 ? WT : W;
 
-    // gradient mean (the AllReduce of the synchronisation step): summed in
-    // the fixed order i = 0, 1, ..., W-1
-    float acc[kVec] = {0.0f, 0.0f, 0.0f, 0.0f};
+    // gradient mean (the gradient AllReduce of a synchronisation step),
+    // summed in the fixed order i = 0, 1, ..., W-1
+    float gbar[kVec] = {0.0f, 0.0f, 0.0f, 0.0f};
+    if constexpr (M != Sync::LocalSGD) {
+        float acc[kVec] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-    for (int i0 = 0; i0 < nw; i0 += C) {
-        float g[C][kVec];
+        for (int i0 = 0; i0 < nw; i0 += C) {
+            float g[C][kVec];
 #pragma unroll
-        for (int c = 0; c < C; ++c)
-            load_f32<FULL, kNTL>(grads + (int64_t)(i0 + c) * ld + p0, n, g[c]);
+            for (int c = 0; c < C; ++c)
+                load_f32<FULL, kNTL>(grads + (int64_t)(i0 + c) * ld + p0, n, g[c]);
 #pragma unroll
-        for (int c = 0; c < C; ++c)
+            for (int c = 0; c < C; ++c)
 #pragma unroll
-            for (int k = 0; k < kVec; ++k) acc[k] += g[c][k];
+                for (int k = 0; k < kVec; ++k) acc[k] += g[c][k];
+        }
+#pragma unroll
+        for (int k = 0; k < kVec; ++k) gbar[k] = acc[k] * inv_w;
     }
-    float gbar[kVec];
-#pragma unroll
-    for (int k = 0; k < kVec; ++k) gbar[k] = acc[k] * inv_w;
 
     float a[kVec], u[kVec];
-    load_f32<FULL, kNTL>(anchor + p0, n, a);
-    load_f32<FULL, kNTL>(slow + p0, n, u);
+    if constexpr (M == Sync::CPDP) {
+        load_f32<FULL, kNTL>(anchor + p0, n, a);
+        load_f32<FULL, kNTL>(slow + p0, n, u);
+    }
 
-    // synchronized optimizer step per replica, then the parameter mean taken
-    // as a + mean(x_i - a) so the small difference keeps its precision
+    // optimizer step of every replica.  The parameter mean is accumulated as
+    // a sum of differences to a reference that is close to every x_i (the
+    // anchor for CPDP, replica 0's x for LocalSGD), so the small deviations
+    // keep their precision.
     float s[kVec] = {0.0f, 0.0f, 0.0f, 0.0f};
+    float x0[kVec] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int i0 = 0; i0 < nw; i0 += C) {
-        float m[C][kVec], th[C][kVec];
+        float m[C][kVec], th[C][kVec], g[C][kVec];
 #pragma unroll
         for (int c = 0; c < C; ++c) {
             const int64_t off = (int64_t)(i0 + c) * ld + p0;
+            if constexpr (M == Sync::LocalSGD) load_f32<FULL, kNTL>(grads + off, n, g[c]);
             load_f32<FULL, kNTL>(mom + off, n, m[c]);
             PS::template load<FULL, kNTL>(params + off, n, th[c]);
         }
@@ -264,24 +278,42 @@ __device__ __forceinline__ void reconcile_chunk(typename PS::T* params, float* m
         for (int c = 0; c < C; ++c)
 #pragma unroll
             for (int k = 0; k < kVec; ++k) {
-                m[c][k] = fmaf(mu, m[c][k], gbar[k]);
+                const float gk = M == Sync::LocalSGD ? g[c][k] : gbar[k];
+                m[c][k] = fmaf(mu, m[c][k], gk);
                 const float x = PS::round(fmaf(-lr, m[c][k], th[c][k]));
-                s[k] += x - a[k];
+                if constexpr (M == Sync::CPDP) {
+                    s[k] += x - a[k];
+                } else if constexpr (M == Sync::LocalSGD) {
+                    if (i0 + c == 0) x0[k] = x;
+                    s[k] += x - x0[k];
+                } else {
+                    th[c][k] = x;
+                }
             }
 #pragma unroll
-        for (int c = 0; c < C; ++c)
-            store_f32<FULL, kNTS>(mom + (int64_t)(i0 + c) * ld + p0, n, m[c]);
+        for (int c = 0; c < C; ++c) {
+            const int64_t off = (int64_t)(i0 + c) * ld + p0;
+            store_f32<FULL, kNTS>(mom + off, n, m[c]);
+            if constexpr (M == Sync::DDP) PS::template store<FULL, kNTS>(params + off, n, th[c]);
+        }
     }
+    if constexpr (M == Sync::DDP) return;
 
-    // SlowMo outer step: u <- beta u + (a - avg)/lr ; new = a - alpha lr u
+    if constexpr (M == Sync::CPDP) {
+        // SlowMo outer step: u <- beta u + (a - avg)/lr ; new = a - alpha lr u
 #pragma unroll
-    for (int k = 0; k < kVec; ++k) {
-        const float drift = s[k] * inv_w;  // avg - a
-        u[k] = fmaf(beta, u[k], -drift / lr);
-        a[k] = fmaf(-alpha_lr, u[k], a[k]);
+        for (int k = 0; k < kVec; ++k) {
+            const float drift = s[k] * inv_w;  // avg - a
+            u[k] = fmaf(beta, u[k], -drift / lr);
+            a[k] = fmaf(-alpha_lr, u[k], a[k]);
+        }
+        store_f32<FULL, kNTS>(slow + p0, n, u);
+        store_f32<FULL, kNTS>(anchor + p0, n, a);
+    } else {
+#pragma unroll
+        for (int k = 0; k < kVec; ++k) a[k] = fmaf(s[k], inv_w, x0[k]);
+        if (anchor != nullptr) store_f32<FULL, kNTS>(anchor + p0, n, a);
     }
-    store_f32<FULL, kNTS>(slow + p0, n, u);
-    store_f32<FULL, kNTS>(anchor + p0, n, a);
 
     // copy the reconciled model back into every replica
 #pragma unroll
@@ -289,8 +321,8 @@ __device__ __forceinline__ void reconcile_chunk(typename PS::T* params, float* m
         PS::template store<FULL, kNTS>(params + (int64_t)i * ld + p0, n, a);
 }
 
-template <int WT, class PS>
-__global__ __launch_bounds__(kBlock) void reconcile_kernel(
+template <Sync M, int WT, class PS>
+__global__ __launch_bounds__(kBlock) void sync_kernel(
     typename PS::T* __restrict__ params, float* __restrict__ mom,
     const float* __restrict__ grads, float* __restrict__ slow, float* __restrict__ anchor,
     int W, int64_t ld, int64_t P, float lr, float mu, float beta, float alpha_lr,
@@ -298,11 +330,11 @@ __global__ __launch_bounds__(kBlock) void reconcile_kernel(
     const int64_t p0 = ((int64_t)blockIdx.x * kBlock + threadIdx.x) * kVec;
     if (p0 >= P) return;
     if (p0 + kVec <= P)
-        reconcile_chunk<WT, PS, true>(params, mom, grads, slow, anchor, W, ld, p0, kVec, lr,
-                                      mu, beta, alpha_lr, inv_w);
+        sync_chunk<M, WT, PS, true>(params, mom, grads, slow, anchor, W, ld, p0, kVec, lr, mu,
+                                    beta, alpha_lr, inv_w);
     else
-        reconcile_chunk<WT, PS, false>(params, mom, grads, slow, anchor, W, ld, p0,
-                                       (int)(P - p0), lr, mu, beta, alpha_lr, inv_w);
+        sync_chunk<M, WT, PS, false>(params, mom, grads, slow, anchor, W, ld, p0,
+                                     (int)(P - p0), lr, mu, beta, alpha_lr, inv_w);
 }
 
 // ---- launch helpers -------------------------------------------------------------
@@ -345,25 +377,23 @@ int local_step_t(void* params, float* mom, const float* grads, int W, int64_t P,
                   ld, P, bpr, lr, mu);
 }
 
-template <int WT, class PS>
-int reconcile_w(void* params, float* mom, const float* grads, float* slow, float* anchor,
-                int W, int64_t P, int64_t ld, float lr, float mu, float beta, float alpha,
-                void* stream) {
+template <Sync M, int WT, class PS>
+int sync_w(void* params, float* mom, const float* grads, float* slow, float* anchor, int W,
+           int64_t P, int64_t ld, float lr, float mu, float beta, float alpha, void* stream) {
     using T = typename PS::T;
     const float alpha_lr = alpha * lr;
     const float inv_w = 1.0f / (float)W;
-    return launch(reconcile_kernel<WT, PS>, blocks_for(P), stream, static_cast<T*>(params),
-                  mom, grads, slow, anchor, W, ld, P, lr, mu, beta, alpha_lr, inv_w);
+    return launch(sync_kernel<M, WT, PS>, blocks_for(P), stream, static_cast<T*>(params), mom,
+                  grads, slow, anchor, W, ld, P, lr, mu, beta, alpha_lr, inv_w);
 }
 
-template <class PS>
-int reconcile_t(void* params, float* mom, const float* grads, float* slow, float* anchor,
-                int W, int64_t P, int64_t ld, float lr, float mu, float beta, float alpha,
-                void* stream) {
-#define CPDP_W_CASE(N)                                                                      \
-    case N:                                                                                 \
-        return reconcile_w<N, PS>(params, mom, grads, slow, anchor, W, P, ld, lr, mu, beta, \
-                                  alpha, stream);
+template <Sync M, class PS>
+int sync_t(void* params, float* mom, const float* grads, float* slow, float* anchor, int W,
+           int64_t P, int64_t ld, float lr, float mu, float beta, float alpha, void* stream) {
+#define CPDP_W_CASE(N)                                                                     \
+    case N:                                                                                \
+        return sync_w<M, N, PS>(params, mom, grads, slow, anchor, W, P, ld, lr, mu, beta, \
+                                alpha, stream);
     switch (W) {
         CPDP_W_CASE(1)
         CPDP_W_CASE(2)
@@ -372,10 +402,20 @@ int reconcile_t(void* params, float* mom, const float* grads, float* slow, float
         CPDP_W_CASE(16)
         CPDP_W_CASE(32)
         default:
-            return reconcile_w<0, PS>(params, mom, grads, slow, anchor, W, P, ld, lr, mu, beta,
-                                      alpha, stream);
+            return sync_w<M, 0, PS>(params, mom, grads, slow, anchor, W, P, ld, lr, mu, beta,
+                                    alpha, stream);
     }
 #undef CPDP_W_CASE
+}
+
+template <Sync M>
+int sync_p(Param pt, void* params, float* mom, const float* grads, float* slow, float* anchor,
+           int W, int64_t P, int64_t ld, float lr, float mu, float beta, float alpha,
+           void* stream) {
+    return pt == Param::BF16 ? sync_t<M, ParamBF16>(params, mom, grads, slow, anchor, W, P, ld,
+                                                    lr, mu, beta, alpha, stream)
+                             : sync_t<M, ParamF32>(params, mom, grads, slow, anchor, W, P, ld,
+                                                   lr, mu, beta, alpha, stream);
 }
 
 }  // namespace
@@ -394,13 +434,20 @@ int launch_local_step(Param pt, void* params, float* mom, const float* grads, in
                : local_step_t<ParamF32>(params, mom, grads, W, P, ld, lr, mu, stream);
 }
 
-int launch_reconcile(Param pt, void* params, float* mom, const float* grads, float* slow,
-                     float* anchor, int W, int64_t P, int64_t ld, float lr, float mu, float beta,
-                     float alpha, void* stream) {
-    return pt == Param::BF16 ? reconcile_t<ParamBF16>(params, mom, grads, slow, anchor, W, P,
-                                                      ld, lr, mu, beta, alpha, stream)
-                             : reconcile_t<ParamF32>(params, mom, grads, slow, anchor, W, P, ld,
-                                                     lr, mu, beta, alpha, stream);
+int launch_sync(Sync mode, Param pt, void* params, float* mom, const float* grads, float* slow,
+                float* anchor, int W, int64_t P, int64_t ld, float lr, float mu, float beta,
+                float alpha, void* stream) {
+    switch (mode) {
+        case Sync::LocalSGD:
+            return sync_p<Sync::LocalSGD>(pt, params, mom, grads, slow, anchor, W, P, ld, lr, mu,
+                                          beta, alpha, stream);
+        case Sync::DDP:
+            return sync_p<Sync::DDP>(pt, params, mom, grads, slow, anchor, W, P, ld, lr, mu, beta,
+                                     alpha, stream);
+        default:
+            return sync_p<Sync::CPDP>(pt, params, mom, grads, slow, anchor, W, P, ld, lr, mu, beta,
+                                      alpha, stream);
+    }
 }
 
 bool grid_fits(int rows, int64_t P) {

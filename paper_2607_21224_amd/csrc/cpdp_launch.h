@@ -18,9 +18,15 @@ int launch_local_step(Param pt, void* params, float* mom, const float* grads,
                       int W, int64_t P, int64_t ld, float lr, float mu,
                       void* stream);
 
-int launch_reconcile(Param pt, void* params, float* mom, const float* grads,
-                     float* slow, float* anchor, int W, int64_t P, int64_t ld,
-                     float lr, float mu, float beta, float alpha, void* stream);
+// Synchronisation step of one of the three strategies (CPDP reconcile,
+// LocalSGD averaging, DDP gradient step).  slow/anchor are read and written
+// by CPDP; LocalSGD writes anchor only when it is not NULL; DDP uses neither.
+enum class Sync { CPDP, LocalSGD, DDP };
+
+int launch_sync(Sync mode, Param pt, void* params, float* mom,
+                const float* grads, float* slow, float* anchor, int W,
+                int64_t P, int64_t ld, float lr, float mu, float beta,
+                float alpha, void* stream);
 
 // True when a launch over P coordinates (rows = W for the row-parallel local
 // step, 1 otherwise) fits in one grid.

@@ -79,13 +79,43 @@ class CpdpState:
                             h.mu, h.beta, h.alpha, self.param_dt, "f32", "f32",
                             stream)
 
+    def localsgd_sync(self, grads: torch.Tensor, h: Hyper, stream=None,
+                      write_anchor: bool = True) -> None:
+        """LocalSGD synchronisation (Sec. 5.3): local step, then parameter
+        averaging; the average also goes to ``anchor`` unless told not to."""
+        self._check_grads(grads)
+        cpdp.cpdp_localsgd_sync(self.params, self.mom, grads,
+                                self.anchor if write_anchor else None, self.W,
+                                self.P, self.ld, self.K, h.lr, h.mu,
+                                self.param_dt, "f32", "f32", stream)
+
+    def ddp_step(self, grads: torch.Tensor, h: Hyper, stream=None) -> None:
+        """Synchronous DDP step (Sec. 3.1, Sec. 5.3)."""
+        self._check_grads(grads)
+        cpdp.cpdp_ddp_step(self.params, self.mom, grads, self.W, self.P,
+                           self.ld, h.lr, h.mu, self.param_dt, "f32", "f32",
+                           stream)
+
+    METHODS = ("cpdp", "localsgd", "ddp")
+
     def step(self, t: int, grads: torch.Tensor, h: Hyper, T: int = 0,
-             stream=None) -> str:
-        """Step t (1-based within the epoch): a reconcile when the cadence of
-        Sec. 3.2 (with the epoch-end rule of Sec. 3.1) says so, else a local
-        step.  Returns "reconcile" or "local"."""
+             stream=None, method: str = "cpdp") -> str:
+        """Step t (1-based within the epoch) of a synchronisation strategy.
+
+        cpdp / localsgd: a synchronisation step when the cadence of Sec. 3.2
+        (with the epoch-end rule of Sec. 3.1) says so, else a local step.
+        ddp: every step synchronises the gradient (the K = 1 schedule).
+        Returns "reconcile" for a synchronisation step, "local" otherwise."""
+        if method == "ddp":
+            self.ddp_step(grads, h, stream)
+            return "reconcile"
+        if method not in self.METHODS:
+            raise ValueError(method)
         if cpdp.cpdp_is_sync_step(t, self.K, T):
-            self.reconcile(grads, h, stream)
+            if method == "cpdp":
+                self.reconcile(grads, h, stream)
+            else:
+                self.localsgd_sync(grads, h, stream)
             return "reconcile"
         self.local_step(grads, h, stream)
         return "local"

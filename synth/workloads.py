@@ -102,6 +102,20 @@ class Workload:
         write = self.W * (sp + 4) + 8
         return self.P * (read + write)
 
+    def sync_bytes(self, method: str = "cpdp") -> int:
+        """Algorithmic HBM bytes of one synchronisation step of a strategy:
+        cpdp = the reconcile; localsgd = grads, mom, params read, mom, params
+        and the averaged model written; ddp = as a local step (grads, mom,
+        params read; mom, params written)."""
+        sp = self.param_bytes()
+        if method == "cpdp":
+            return self.reconcile_bytes()
+        if method == "localsgd":
+            return self.P * (self.W * (sp + 4 + 4) + self.W * (sp + 4) + 4)
+        if method == "ddp":
+            return self.local_step_bytes()
+        raise ValueError(method)
+
     def local_step_bytes(self) -> int:
         sp = self.param_bytes()
         return self.P * self.W * (2 * sp + 4 + 2 * 4)

@@ -42,6 +42,7 @@ class Case:
     theta_sigma: float = 0.02
     grad_sigma: float = 1e-3
     outlier_rate: float = 0.0
+    method: str = "cpdp"
 
     def hyper32(self):
         f = lambda x: float(np.float32(x))  # noqa: E731
@@ -81,7 +82,7 @@ def run_oracle(c: Case, idx: np.ndarray, on_step):
     h = c.hyper32()
     th0, grads = oracle_inputs(c, idx)
     oracle.run(th0, grads, c.W, c.K, c.steps, *h, T=c.T, param_dt=c.param_dt,
-               mom_dt="f32", aux_dt="f32", callback=on_step)
+               mom_dt="f32", aux_dt="f32", callback=on_step, method=c.method)
 
 
 class GpuRun:
@@ -106,7 +107,8 @@ class GpuRun:
         sdev.fill_grads(self.grads, c.P, c.seed, step, c.grad_sigma,
                         c.outlier_rate, stream=self.stream)
         t = ((step - 1) % c.T) + 1 if c.T > 0 else step
-        return self.st.step(t, self.grads, self.h, c.T, stream=self.stream)
+        return self.st.step(t, self.grads, self.h, c.T, stream=self.stream,
+                            method=c.method)
 
     def snapshot(self, idx: np.ndarray | None = None):
         torch.cuda.synchronize()
@@ -167,7 +169,7 @@ def run_parity(c: Case, idx: np.ndarray | None = None, stream=None):
     """Run a Case on both sides and compare after every step."""
     P = c.P
     sel = np.arange(P) if idx is None else idx
-    log(f"[parity] W={c.W} P={P} K={c.K} steps={c.steps} dt={c.param_dt} "
+    log(f"[parity] {c.method} W={c.W} P={P} K={c.K} steps={c.steps} dt={c.param_dt} "
         f"seed={c.seed} ld={c.ld} coords={sel.size}")
     refs = {}
     run_oracle(c, sel, lambda s, kind, st: refs.__setitem__(s, (kind, st.copy())))
@@ -178,7 +180,7 @@ def run_parity(c: Case, idx: np.ndarray | None = None, stream=None):
         rk, ref = refs[s]
         assert kind == rk, (s, kind, rk)
         compare(snap, ref, c.param_dt, f"step {s} ({kind})")
-        if kind == "reconcile":
+        if kind == "reconcile" and c.method != "ddp":
             check_replicas_reconciled(snap, c.param_dt, f"step {s}")
     log(f"[parity] ok: {c.steps} steps")
     return g

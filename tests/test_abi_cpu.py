@@ -168,3 +168,38 @@ def test_p_zero_is_noop_without_pointers():
 def test_binding_raises():
     with pytest.raises(cpdp.CpdpError, match="INVALID_ARG"):
         cpdp.cpdp_reconcile(A, B, C, U, V, 0, 10, 16, 1, 0.1, 0.9, 0.5, 1.0)
+
+
+def lsgd(**kw):
+    a = dict(GOOD, params=A, mom=B, grads=C, anchor=V, pdt=0, gdt=0, mdt=0)
+    a.update(kw)
+    return cpdp.cpdp_localsgd_sync(a["params"], a["mom"], a["grads"], a["anchor"],
+                                   a["W"], a["P"], a["ld"], a["K"], a["lr"], a["mu"],
+                                   a["pdt"], a["gdt"], a["mdt"], None, check=False)
+
+
+def ddp(**kw):
+    a = dict(GOOD, params=A, mom=B, grads=C, pdt=0, gdt=0, mdt=0)
+    a.update(kw)
+    return cpdp.cpdp_ddp_step(a["params"], a["mom"], a["grads"], a["W"], a["P"],
+                              a["ld"], a["lr"], a["mu"], a["pdt"], a["gdt"], a["mdt"],
+                              None, check=False)
+
+
+@pytest.mark.parametrize("fn", [lsgd, ddp])
+def test_baseline_validation(fn):
+    assert fn(W=0) == E.CPDP_ERR_INVALID_ARG
+    assert fn(ld=10) == E.CPDP_ERR_INVALID_ARG
+    assert fn(lr=0.0) == E.CPDP_ERR_INVALID_ARG
+    assert fn(mu=1.0) == E.CPDP_ERR_INVALID_ARG
+    assert fn(pdt=7) == E.CPDP_ERR_DTYPE
+    assert fn(params=None) == E.CPDP_ERR_NULL
+    assert fn(mom=B + 8) == E.CPDP_ERR_MISALIGNED
+    assert fn(grads=A) == E.CPDP_ERR_OVERLAP
+    assert fn(P=0, params=None, mom=None, grads=None) == E.CPDP_OK
+
+
+def test_localsgd_anchor_checks():
+    assert lsgd(K=0) == E.CPDP_ERR_INVALID_ARG
+    assert lsgd(anchor=V + 4) == E.CPDP_ERR_MISALIGNED
+    assert lsgd(anchor=A + 64) == E.CPDP_ERR_OVERLAP
