@@ -59,7 +59,32 @@ def load(path: str = _LIB_PATH) -> ctypes.CDLL:
     lib.oracle_localsgd_sync.restype = None
     lib.oracle_ddp_step.argtypes = [i, i64, i, i, i, _D, _D, _D, d, d]
     lib.oracle_ddp_step.restype = None
+    _OPTP = ctypes.POINTER(OracleOpt)
+    lib.oracle_local_step_opt.argtypes = [i, i64, i, i, i, _D, _D, _D, _D, _OPTP]
+    lib.oracle_local_step_opt.restype = None
+    lib.oracle_sync_opt.argtypes = [i, i, i64, i, i, i, _D, _D, _D, _D, _D, _D,
+                                    _OPTP, d, d]
+    lib.oracle_sync_opt.restype = None
     return lib
+
+
+class OracleOpt(ctypes.Structure):
+    """Optimizer descriptor of the oracle: kind 0 = SGD (momentum mu, coupled
+    weight decay wd), kind 1 = AdamW (beta1 = mu, beta2, eps, decoupled wd,
+    1-based bias-correction step)."""
+    _fields_ = [("kind", ctypes.c_int), ("lr", ctypes.c_double),
+                ("mu", ctypes.c_double), ("beta2", ctypes.c_double),
+                ("eps", ctypes.c_double), ("wd", ctypes.c_double),
+                ("step", ctypes.c_int64)]
+
+
+def sgd(lr, mu=0.0, wd=0.0) -> OracleOpt:
+    return OracleOpt(0, float(lr), float(mu), 0.0, 0.0, float(wd), 0)
+
+
+def adamw(lr, beta1=0.9, beta2=0.999, eps=1e-8, wd=0.0, step=1) -> OracleOpt:
+    return OracleOpt(1, float(lr), float(beta1), float(beta2), float(eps),
+                     float(wd), int(step))
 
 
 _lib = None
@@ -176,6 +201,55 @@ def ddp_step(st: OracleState, grads, lr: float, mu: float) -> None:
 
 
 METHODS = ("cpdp", "localsgd", "ddp")
+_STRATEGY = {"cpdp": 0, "localsgd": 1, "ddp": 2}
+
+
+def local_step_opt(st: OracleState, grads, opt: OracleOpt, mom2=None) -> None:
+    """Local step with a general optimizer; ``mom2`` ((W, P) float64) holds
+    AdamW's second moments and is updated in place."""
+    g = _grads(st, grads)
+    st._l.oracle_local_step_opt(st.W, st.P, _DT[st.param_dt], _DT[st.mom_dt],
+                                _DT[st.aux_dt], _ptr(st.params), _ptr(st.mom),
+                                _ptr(mom2) if mom2 is not None else None,
+                                _ptr(g), ctypes.byref(opt))
+
+
+def sync_opt(st: OracleState, method: str, grads, opt: OracleOpt, beta=0.0,
+             alpha=1.0, mom2=None, write_anchor=True) -> None:
+    """Synchronisation step of ``method`` with a general optimizer."""
+    g = _grads(st, grads)
+    st._l.oracle_sync_opt(_STRATEGY[method], st.W, st.P, _DT[st.param_dt],
+                          _DT[st.mom_dt], _DT[st.aux_dt], _ptr(st.params),
+                          _ptr(st.mom), _ptr(mom2) if mom2 is not None else None,
+                          _ptr(g), _ptr(st.slow),
+                          _ptr(st.anchor) if write_anchor else None,
+                          ctypes.byref(opt), float(beta), float(alpha))
+
+
+def run_opt(theta0, grad_fn, W: int, K: int, n_steps: int, make_opt, beta=0.0,
+            alpha=1.0, T: int = 0, method="cpdp", param_dt="f32", mom_dt="f32",
+            aux_dt="f32", callback=None, use=None):
+    """Algorithm 1 (or a Sec. 5.3 baseline) with a general optimizer.
+    make_opt(step) returns the OracleOpt of 1-based global step ``step`` (the
+    AdamW step count advances on every step, local or synchronising).
+    callback(step, kind, state, mom2) after every step.  Returns (state, mom2)."""
+    if method not in METHODS:
+        raise ValueError(method)
+    st = state_init(theta0, W, param_dt, mom_dt, aux_dt, use)
+    mom2 = np.zeros((W, st.P))
+    for step in range(1, n_steps + 1):
+        t = ((step - 1) % T) + 1 if T > 0 else step
+        g = grad_fn(step, W, st.P)
+        opt = make_opt(step)
+        if method == "ddp" or is_sync_step(t, K, T):
+            sync_opt(st, method, g, opt, beta, alpha, mom2)
+            kind = "reconcile"
+        else:
+            local_step_opt(st, g, opt, mom2)
+            kind = "local"
+        if callback is not None:
+            callback(step, kind, st, mom2)
+    return st, mom2
 
 
 def is_sync_step(t: int, K: int, T: int = 0) -> bool:

@@ -246,3 +246,103 @@ void oracle_ddp_step(int W, int64_t P, int param_dt, int mom_dt, int aux_dt,
         }
     }
 }
+
+/* ------------------------------------------------------------------------
+ * General optimizers (Sec. 5.2 / Table 3: SGD with momentum and weight decay
+ * for ResNet-50, AdamW for ViT-S), with the optimizer state kept per worker
+ * (Sec. 3.2 last paragraph, Sec. 4.2).  Semantics and storage points follow
+ * the PyTorch optimizers the paper's implementation calls:
+ *   SGD    d = g + wd*theta (stored); buf <- mu*buf + d; theta <- theta - lr*buf
+ *   AdamW  theta <- theta*(1 - lr*wd)                  (stored)
+ *          m <- b1*m + (1-b1)*g;  v <- b2*v + (1-b2)*g^2
+ *          theta <- theta - (lr/(1-b1^t)) * m / (sqrt(v)/sqrt(1-b2^t) + eps)
+ * with t the 1-based step count of this update.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+    int kind;      /* 0 = SGD, 1 = AdamW */
+    double lr;
+    double mu;     /* SGD momentum, or AdamW beta1 */
+    double beta2;  /* AdamW */
+    double eps;    /* AdamW */
+    double wd;     /* weight decay: coupled for SGD, decoupled for AdamW */
+    int64_t step;  /* AdamW bias-correction step count (1-based) */
+} oracle_opt;
+
+static void optimizer_update(const oracle_opt* o, int param_dt, int mom_dt,
+                             int grad_dt, double* theta, double* m, double* v,
+                             double g) {
+    if (o->kind == 0) {
+        double d = o->wd != 0.0 ? store_as(grad_dt, g + o->wd * *theta) : g;
+        *m = store_as(mom_dt, o->mu * *m + d);
+        *theta = store_as(param_dt, *theta - o->lr * *m);
+    } else {
+        double th = o->wd != 0.0 ? store_as(param_dt, *theta * (1.0 - o->lr * o->wd))
+                                 : *theta;
+        *m = store_as(mom_dt, o->mu * *m + (1.0 - o->mu) * g);
+        *v = store_as(mom_dt, o->beta2 * *v + (1.0 - o->beta2) * g * g);
+        double bc1 = 1.0 - pow(o->mu, (double)o->step);
+        double bc2 = 1.0 - pow(o->beta2, (double)o->step);
+        double denom = sqrt(*v) / sqrt(bc2) + o->eps;
+        *theta = store_as(param_dt, th - (o->lr / bc1) * *m / denom);
+    }
+}
+
+/* local step with a general optimizer; mom2 holds AdamW's second moments;
+ * aux_dt is the storage type of gradient-sized temporaries (fp32 like .grad) */
+void oracle_local_step_opt(int W, int64_t P, int param_dt, int mom_dt,
+                           int aux_dt, double* params, double* mom,
+                           double* mom2, const double* grads,
+                           const oracle_opt* o) {
+    for (int i = 0; i < W; ++i)
+        for (int64_t p = 0; p < P; ++p) {
+            int64_t k = (int64_t)i * P + p;
+            optimizer_update(o, param_dt, mom_dt, aux_dt, &params[k], &mom[k],
+                             mom2 ? &mom2[k] : NULL, grads[k]);
+        }
+}
+
+/*
+ * Synchronisation step of a strategy with a general optimizer.
+ *   strategy 0 (CPDP): gradient mean, optimizer step with it, parameter mean,
+ *                      SlowMo (u-form, beta, alpha), copy-back.
+ *   strategy 1 (LocalSGD): optimizer step with the local gradient, parameter
+ *                      mean, copy-back (anchor <- mean if anchor != NULL).
+ *   strategy 2 (DDP): gradient mean, optimizer step with it; no averaging.
+ * The SlowMo step length is the optimizer's lr, as in the SGD reconcile.
+ */
+void oracle_sync_opt(int strategy, int W, int64_t P, int param_dt, int mom_dt,
+                     int aux_dt, double* params, double* mom, double* mom2,
+                     const double* grads, double* slow, double* anchor,
+                     const oracle_opt* o, double beta, double alpha) {
+    for (int64_t p = 0; p < P; ++p) {
+        double gbar = 0.0;
+        if (strategy != 1) {
+            double gsum = 0.0;
+            for (int i = 0; i < W; ++i) gsum += grads[(int64_t)i * P + p];
+            gbar = store_as(aux_dt, gsum / (double)W);
+        }
+        double xsum = 0.0;
+        for (int i = 0; i < W; ++i) {
+            int64_t k = (int64_t)i * P + p;
+            optimizer_update(o, param_dt, mom_dt, aux_dt, &params[k], &mom[k],
+                             mom2 ? &mom2[k] : NULL,
+                             strategy == 1 ? grads[k] : gbar);
+            xsum += params[k];
+        }
+        if (strategy == 2) continue;
+        double avg = xsum / (double)W;
+        double fresh;
+        if (strategy == 0) {
+            double ref = anchor[p];
+            double u = store_as(aux_dt, beta * slow[p] + (ref - avg) / o->lr);
+            fresh = store_as(aux_dt, ref - alpha * o->lr * u);
+            slow[p] = u;
+            anchor[p] = fresh;
+        } else {
+            fresh = store_as(aux_dt, avg);
+            if (anchor) anchor[p] = fresh;
+        }
+        for (int i = 0; i < W; ++i)
+            params[(int64_t)i * P + p] = store_as(param_dt, fresh);
+    }
+}

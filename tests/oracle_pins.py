@@ -379,3 +379,114 @@ def pin_localsgd_closed_form(use=None):
 
 
 ALL_PINS += [pin_torch_baselines, pin_brute_force_baselines, pin_localsgd_closed_form]
+
+
+def _torch_opt_reference(theta0, grads, W, K, method, make_torch_opt):
+    """Per-worker torch optimizers (fp64) driven like the Sec. 4.2
+    implementation: averaged gradient on CPDP/DDP sync steps, local gradient
+    otherwise; parameter averaging on CPDP (beta = 0, alpha = 1) and LocalSGD
+    sync steps; optimizer states never averaged."""
+    import torch
+    ps = [torch.nn.Parameter(torch.tensor(theta0, dtype=torch.float64)) for _ in range(W)]
+    opts = [make_torch_opt([p]) for p in ps]
+    out = []
+    for s, g in enumerate(grads, start=1):
+        sync = s % K == 0 or method == "ddp"
+        use_gbar = sync and method in ("cpdp", "ddp")
+        gbar = g.mean(axis=0)
+        for i in range(W):
+            ps[i].grad = torch.tensor(gbar if use_gbar else g[i])
+            opts[i].step()
+        if sync and method in ("cpdp", "localsgd"):
+            avg = torch.stack([p.detach() for p in ps]).mean(0)
+            for p in ps:
+                p.data.copy_(avg)
+        out.append(np.stack([p.detach().numpy().copy() for p in ps]))
+    return out
+
+
+def pin_torch_optimizers(use=None):
+    """SGD with weight decay and AdamW (Table 3 optimizers) in every strategy
+    against torch.optim.SGD / torch.optim.AdamW, one optimizer per worker."""
+    import torch
+    rng = np.random.default_rng(23)
+    cfgs = [
+        ("sgd", dict(lr=0.1, momentum=0.9, weight_decay=5e-4),
+         lambda s: oracle.sgd(0.1, 0.9, 5e-4)),
+        ("sgd", dict(lr=0.05, momentum=0.0, weight_decay=0.01),
+         lambda s: oracle.sgd(0.05, 0.0, 0.01)),
+        ("adamw", dict(lr=5e-4, betas=(0.9, 0.999), eps=1e-8, weight_decay=0.05),
+         lambda s: oracle.adamw(5e-4, 0.9, 0.999, 1e-8, 0.05, s)),
+        ("adamw", dict(lr=1e-2, betas=(0.8, 0.99), eps=1e-6, weight_decay=0.0),
+         lambda s: oracle.adamw(1e-2, 0.8, 0.99, 1e-6, 0.0, s)),
+    ]
+    for method in ("cpdp", "localsgd", "ddp"):
+        for kind, tkw, mk in cfgs:
+            W, K, P = 3, 3, 4
+            n = 3 * K + 1
+            theta0 = rng.normal(0, 1, P)
+            grads = [rng.normal(0, 1, (W, P)) for _ in range(n)]
+            topt = ((lambda ps: torch.optim.SGD(ps, **tkw)) if kind == "sgd"
+                    else (lambda ps: torch.optim.AdamW(ps, **tkw)))
+            ref = _torch_opt_reference(theta0, grads, W, K, method, topt)
+            rec = []
+            oracle.run_opt(theta0, lambda s, W_, P_: grads[s - 1], W, K, n, mk, 0.0,
+                           1.0, method=method, param_dt="f64", mom_dt="f64",
+                           aux_dt="f64", use=use,
+                           callback=lambda s, k, st, m2: rec.append(st.copy()))
+            for s, (st, p_ref) in enumerate(zip(rec, ref), start=1):
+                _close(st.params, p_ref, 1e-11, 1e-12, f"{kind} {method} s={s}")
+
+
+def pin_adamw_closed_form(use=None):
+    """AdamW with a constant gradient c and no weight decay: the bias-corrected
+    moments are exactly c and c^2, so every step moves theta by
+    lr * c / (|c| + eps)."""
+    c, lr, eps = -0.3, 0.01, 1e-8
+    theta0 = np.array([0.5, -1.0])
+    for method in ("cpdp", "localsgd", "ddp"):
+        rec = []
+        oracle.run_opt(theta0, lambda s, W_, P_: np.full((W_, P_), c), 2, 3, 7,
+                       lambda s: oracle.adamw(lr, 0.9, 0.999, eps, 0.0, s), 0.0, 1.0,
+                       method=method, param_dt="f64", mom_dt="f64", aux_dt="f64",
+                       use=use, callback=lambda s, k, st, m2: rec.append((s, st.copy())))
+        for s, st in rec:
+            want = theta0 - s * lr * c / (abs(c) + eps)
+            _close(st.params, np.tile(want, (2, 1)), 1e-12, 1e-12, f"adamw cf {method} s={s}")
+
+
+def pin_sgd_weight_decay_closed_form(use=None):
+    """SGD, mu = 0, weight decay wd, constant gradient c: theta_{t+1} =
+    theta_t (1 - lr wd) - lr c, so theta_t = (theta0 + c/wd)(1 - lr wd)^t - c/wd."""
+    c, lr, wd = 0.7, 0.1, 0.05
+    theta0 = np.array([2.0, -3.0, 0.25])
+    rec = []
+    oracle.run_opt(theta0, lambda s, W_, P_: np.full((W_, P_), c), 4, 2, 9,
+                   lambda s: oracle.sgd(lr, 0.0, wd), 0.0, 1.0, method="cpdp",
+                   param_dt="f64", mom_dt="f64", aux_dt="f64", use=use,
+                   callback=lambda s, k, st, m2: rec.append((s, st.copy())))
+    for s, st in rec:
+        want = (theta0 + c / wd) * (1 - lr * wd) ** s - c / wd
+        _close(st.params, np.tile(want, (4, 1)), 1e-12, 1e-12, f"sgd wd cf s={s}")
+
+
+def pin_general_sgd_matches_plain(use=None):
+    """The general-optimizer path with plain SGD (no weight decay) is the same
+    computation as the plain local step and reconcile (bitwise, fp32 storage)."""
+    rng = np.random.default_rng(31)
+    W, P, K, n = 4, 64, 3, 9
+    theta0 = rng.normal(0, 0.02, P).astype(np.float32).astype(np.float64)
+    grads = [rng.normal(0, 1e-3, (W, P)).astype(np.float32).astype(np.float64)
+             for _ in range(n)]
+    for method in ("cpdp", "localsgd", "ddp"):
+        a = oracle.run(theta0, lambda s, W_, P_: grads[s - 1], W, K, n, 0.1, 0.9, 0.5,
+                       1.0, method=method, use=use)
+        b, _ = oracle.run_opt(theta0, lambda s, W_, P_: grads[s - 1], W, K, n,
+                              lambda s: oracle.sgd(0.1, 0.9, 0.0), 0.5, 1.0,
+                              method=method, use=use)
+        for name in ("params", "mom", "slow", "anchor"):
+            assert np.array_equal(getattr(a, name), getattr(b, name)), (method, name)
+
+
+ALL_PINS += [pin_torch_optimizers, pin_adamw_closed_form,
+             pin_sgd_weight_decay_closed_form, pin_general_sgd_matches_plain]
