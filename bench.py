@@ -40,10 +40,10 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def recorded_traffic(kernel: str, workload: str):
+def recorded_traffic(kernel: str, workload: str, variant: str = ""):
     """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE /
     WRITE_SIZE summary, or None when the kernel source changed since."""
-    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_pmc.txt")
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}{variant}_pmc.txt")
     if not os.path.exists(path):
         return None
     m = re.search(r"^TRAFFIC_JSON: (\{.*\})$", open(path).read(), re.M)
@@ -98,6 +98,10 @@ def main() -> int:
     ap.add_argument("--workload", default="r50_100")
     ap.add_argument("--method", default="cpdp", choices=["cpdp", "localsgd", "ddp"],
                     help="synchronisation strategy (Sec. 5.3); cpdp is the paper's method")
+    ap.add_argument("--optimizer", default="sgd", choices=["sgd", "sgd_wd", "adamw"],
+                    help="per-replica optimizer (Table 3): sgd = momentum SGD of the "
+                         "workload; sgd_wd adds weight decay 5e-4; adamw = AdamW "
+                         "(lr 5e-4, betas 0.9/0.999, eps 1e-8, weight decay 0.05)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=10.0)
     ap.add_argument("--row-align-bytes", type=int, default=0,
@@ -112,7 +116,7 @@ def main() -> int:
         return 2
 
     import torch
-    from paper_2607_21224_amd.state import CpdpState, Hyper
+    from paper_2607_21224_amd.state import CpdpState, Hyper, Optimizer
     from synth import WORKLOADS
     from synth import device as sdev
 
@@ -137,7 +141,15 @@ def main() -> int:
             g = torch.empty((w.W, w.ld), dtype=torch.float32, device=dev)
             sdev.fill_grads(g, w.P, 42, s, w.grad_sigma, w.outlier_rate, stream=stream)
             grads.append(g)
-        st.init(th, stream=stream)
+        opt = None
+        if args.optimizer == "sgd_wd":
+            opt = Optimizer("sgd", h.lr, h.mu, weight_decay=5e-4)
+        elif args.optimizer == "adamw":
+            opt = Optimizer("adamw", 5e-4, 0.9, 0.999, 1e-8, 0.05)
+        if opt is None:
+            st.init(th, stream=stream)
+        else:
+            st.init_opt(th, opt, stream=stream)
         # copy-kernel ceiling on a 4 GiB buffer pair (also the counter calibration)
         n_copy = 1 << 30
         csrc = torch.ones(n_copy, dtype=torch.float32, device=dev)
@@ -151,7 +163,11 @@ def main() -> int:
                 e0 = torch.cuda.Event(enable_timing=True)
                 e1 = torch.cuda.Event(enable_timing=True)
                 e0.record(stream)
-            kind = st.step(s, grads[s - 1], h, 0, stream, method=args.method)
+            if opt is None:
+                kind = st.step(s, grads[s - 1], h, 0, stream, method=args.method)
+            else:
+                kind = st.step_opt(s, grads[s - 1], opt, h.beta, h.alpha, 0, stream,
+                                   method=args.method)
             if evs is not None:
                 e1.record(stream)
                 evs.append((kind, e0, e1))
@@ -194,16 +210,20 @@ def main() -> int:
     torch.cuda.synchronize()
     copy_gbps = 2 * 4 * n_copy * reps / (c0.elapsed_time(c1) * 1e-3) / 1e9
 
-    rec_bytes = w.sync_bytes(args.method)
-    loc_bytes = w.local_step_bytes()
+    adamw = args.optimizer == "adamw"
+    rec_bytes = w.sync_bytes(args.method, adamw)
+    loc_bytes = w.local_step_bytes(adamw)
     rec_gbps = rec_bytes / (rec_ms * 1e-3) / 1e9
     wp = w.W * w.P
+
+    variant = "" if (args.method, args.optimizer) == ("cpdp", "sgd") else \
+        f"_{args.method}_{args.optimizer}"
 
     def roofline(kernel, nbytes, ms):
         ach = nbytes / (ms * 1e-3) / 1e9
         return {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS,
                 "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4),
-                "traffic": recorded_traffic(kernel, w.name),
+                "traffic": recorded_traffic(kernel, w.name, variant),
                 "kernel": kernel, "bytes_per_launch": nbytes,
                 "avg_launch_ms": round(ms, 5),
                 "frac_of_copy_ceiling": round(ach / copy_gbps, 4)}
@@ -220,7 +240,7 @@ def main() -> int:
         "config": {"workload": f"{w.name}: W={w.W} replicas, P={w.P} ({w.param_dt} params), "
                                f"K={w.K}, lr={w.lr}, mu={w.mu}, beta={w.beta}, alpha={w.alpha}",
                    "W": w.W, "P": w.P, "ld": w.ld, "K": w.K,
-                   "method": args.method,
+                   "method": args.method, "optimizer": args.optimizer,
                    "step": (f"{w.K} DDP steps (K=1 schedule), same gradients as a CPDP period"
                             if args.method == "ddp" else
                             f"one period: {w.K - 1} local steps + 1 {sync_kernel}")},

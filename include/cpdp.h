@@ -132,6 +132,75 @@ int cpdp_ddp_step(void* params, void* mom, const void* grads, int W,
                   int64_t P, int64_t ld, float lr, float mu, int param_dt,
                   int grad_dt, int mom_dt, void* stream);
 
+/* ------------------------------------------------------------------------
+ * General optimizers.  The paper trains ResNet-50 with SGD (momentum 0.9,
+ * weight decay 5e-4) and ViT-S with AdamW (lr 5e-4, weight decay 0.05)
+ * (Sec. 5.2, Table 3); optimizer state always stays per replica and is never
+ * averaged (Sec. 3.2 last paragraph, Sec. 4.2).  Update of one replica with
+ * the gradient g it uses (its own on local and LocalSGD steps, the replica
+ * mean on CPDP and DDP steps), PyTorch semantics:
+ *   CPDP_OPT_SGD    d = g + weight_decay * theta
+ *                   mom <- momentum * mom + d;   theta <- theta - lr * mom
+ *   CPDP_OPT_ADAMW  theta <- theta * (1 - lr * weight_decay)     (stored)
+ *                   mom  <- b1 mom + (1 - b1) g;  mom2 <- b2 mom2 + (1 - b2) g^2
+ *                   theta <- theta - lr / (1 - b1^step) * mom
+ *                                    / (sqrt(mom2) / sqrt(1 - b2^step) + eps)
+ *                   with b1 = momentum, b2 = beta2, step = 1-based count of
+ *                   this update (it advances on local and sync steps alike).
+ * The SlowMo step of a CPDP reconcile uses the optimizer's lr.  Validation:
+ * lr > 0 finite, 0 <= momentum < 1, weight_decay >= 0 finite; AdamW also
+ * 0 <= beta2 < 1, eps > 0 finite, step >= 1, lr * weight_decay < 1.
+ * ------------------------------------------------------------------------ */
+typedef enum { CPDP_OPT_SGD = 0, CPDP_OPT_ADAMW = 1 } cpdp_optimizer_kind;
+
+typedef struct cpdp_optimizer {
+    int kind;           /* cpdp_optimizer_kind */
+    float lr;
+    float momentum;     /* SGD momentum, or AdamW beta1 */
+    float beta2;        /* AdamW only */
+    float eps;          /* AdamW only */
+    float weight_decay; /* SGD: added to the gradient; AdamW: decoupled */
+    int64_t step;       /* AdamW only: 1-based step count of this update */
+} cpdp_optimizer;
+
+typedef enum {
+    CPDP_SYNC_CPDP = 0,     /* cpdp_reconcile's computation */
+    CPDP_SYNC_LOCALSGD = 1, /* cpdp_localsgd_sync's computation */
+    CPDP_SYNC_DDP = 2       /* cpdp_ddp_step's computation */
+} cpdp_sync_kind;
+
+/*
+ * cpdp_state_init, also zeroing mom2 ([W x ld] fp32, AdamW second moments)
+ * when it is not NULL.  Momentum families are fp32.
+ */
+int cpdp_state_init_opt(const void* theta0, void* params, void* mom,
+                        void* mom2, float* slow_mom, float* anchor, int W,
+                        int64_t P, int64_t ld, int K, int param_dt,
+                        void* stream);
+
+/*
+ * Local update phase with a general optimizer.  mom2 ([W x ld] fp32) is
+ * required for AdamW and ignored for SGD; grads and mom are fp32.
+ * Returns CPDP_ERR_NULL when opt is NULL or AdamW lacks mom2.
+ */
+int cpdp_local_step_opt(void* params, void* mom, void* mom2,
+                        const void* grads, int W, int64_t P, int64_t ld,
+                        int K, const cpdp_optimizer* opt, int param_dt,
+                        void* stream);
+
+/*
+ * Synchronisation step of a strategy (cpdp_sync_kind) with a general
+ * optimizer, in one pass over HBM.  slow_mom and anchor are required for
+ * CPDP_SYNC_CPDP (with beta, alpha as in cpdp_reconcile), anchor is optional
+ * for CPDP_SYNC_LOCALSGD, and neither is used by CPDP_SYNC_DDP (beta, alpha
+ * are then ignored).  mom2 as in cpdp_local_step_opt.
+ */
+int cpdp_sync_step_opt(int strategy, void* params, void* mom, void* mom2,
+                       const void* grads, float* slow_mom, float* anchor,
+                       int W, int64_t P, int64_t ld, int K,
+                       const cpdp_optimizer* opt, float beta, float alpha,
+                       int param_dt, void* stream);
+
 /*
  * Synchronisation indicator (Sec. 3.2) with the forced synchronisation at the
  * end of an epoch (Sec. 3.1, Sec. 4.2).  Host only, no GPU work.

@@ -256,7 +256,10 @@ void oracle_ddp_step(int W, int64_t P, int param_dt, int mom_dt, int aux_dt,
  *   AdamW  theta <- theta*(1 - lr*wd)                  (stored)
  *          m <- b1*m + (1-b1)*g;  v <- b2*v + (1-b2)*g^2
  *          theta <- theta - (lr/(1-b1^t)) * m / (sqrt(v)/sqrt(1-b2^t) + eps)
- * with t the 1-based step count of this update.
+ * with t the 1-based step count of this update.  The derived scalars
+ * 1 - lr*wd, lr/(1-b1^t) and sqrt(1-b2^t) are computed in double and then
+ * stored in the gradient storage type (fp32): that is the value an fp32
+ * tensor operation of the framework multiplies or divides by.
  * ------------------------------------------------------------------------ */
 typedef struct {
     int kind;      /* 0 = SGD, 1 = AdamW */
@@ -276,14 +279,16 @@ static void optimizer_update(const oracle_opt* o, int param_dt, int mom_dt,
         *m = store_as(mom_dt, o->mu * *m + d);
         *theta = store_as(param_dt, *theta - o->lr * *m);
     } else {
-        double th = o->wd != 0.0 ? store_as(param_dt, *theta * (1.0 - o->lr * o->wd))
-                                 : *theta;
+        double decay = store_as(grad_dt, 1.0 - o->lr * o->wd);
+        double th = o->wd != 0.0 ? store_as(param_dt, *theta * decay) : *theta;
         *m = store_as(mom_dt, o->mu * *m + (1.0 - o->mu) * g);
         *v = store_as(mom_dt, o->beta2 * *v + (1.0 - o->beta2) * g * g);
         double bc1 = 1.0 - pow(o->mu, (double)o->step);
         double bc2 = 1.0 - pow(o->beta2, (double)o->step);
-        double denom = sqrt(*v) / sqrt(bc2) + o->eps;
-        *theta = store_as(param_dt, th - (o->lr / bc1) * *m / denom);
+        double step_size = store_as(grad_dt, o->lr / bc1);
+        double sqrt_bc2 = store_as(grad_dt, sqrt(bc2));
+        double denom = sqrt(*v) / sqrt_bc2 + o->eps;
+        *theta = store_as(param_dt, th - step_size * *m / denom);
     }
 }
 

@@ -33,8 +33,25 @@ DTYPES = {"f32": CPDP_F32, "bf16": CPDP_BF16}
 
 # every symbol declared in include/cpdp.h
 EXPORTS = ("cpdp_state_init", "cpdp_local_step", "cpdp_reconcile",
-           "cpdp_localsgd_sync", "cpdp_ddp_step", "cpdp_is_sync_step",
+           "cpdp_localsgd_sync", "cpdp_ddp_step", "cpdp_state_init_opt",
+           "cpdp_local_step_opt", "cpdp_sync_step_opt", "cpdp_is_sync_step",
            "cpdp_status_str")
+
+CPDP_OPT_SGD = 0
+CPDP_OPT_ADAMW = 1
+CPDP_SYNC_CPDP = 0
+CPDP_SYNC_LOCALSGD = 1
+CPDP_SYNC_DDP = 2
+SYNC_KINDS = {"cpdp": CPDP_SYNC_CPDP, "localsgd": CPDP_SYNC_LOCALSGD,
+              "ddp": CPDP_SYNC_DDP}
+
+
+class cpdp_optimizer(ctypes.Structure):
+    """Mirror of the C struct cpdp_optimizer (include/cpdp.h)."""
+    _fields_ = [("kind", ctypes.c_int), ("lr", ctypes.c_float),
+                ("momentum", ctypes.c_float), ("beta2", ctypes.c_float),
+                ("eps", ctypes.c_float), ("weight_decay", ctypes.c_float),
+                ("step", ctypes.c_int64)]
 
 
 def _load() -> ctypes.CDLL:
@@ -55,11 +72,17 @@ def _load() -> ctypes.CDLL:
                                    i, i, i, vp]
     lib.cpdp_localsgd_sync.argtypes = [vp, vp, vp, vp, i, i64, i64, i, f, f, i, i, i, vp]
     lib.cpdp_ddp_step.argtypes = [vp, vp, vp, i, i64, i64, f, f, i, i, i, vp]
+    op = ctypes.POINTER(cpdp_optimizer)
+    lib.cpdp_state_init_opt.argtypes = [vp, vp, vp, vp, vp, vp, i, i64, i64, i, i, vp]
+    lib.cpdp_local_step_opt.argtypes = [vp, vp, vp, vp, i, i64, i64, i, op, i, vp]
+    lib.cpdp_sync_step_opt.argtypes = [i, vp, vp, vp, vp, vp, vp, i, i64, i64, i, op,
+                                       f, f, i, vp]
     lib.cpdp_is_sync_step.argtypes = [i64, i, i64]
     lib.cpdp_status_str.argtypes = [i]
     lib.cpdp_status_str.restype = ctypes.c_char_p
     for name in ("cpdp_state_init", "cpdp_local_step", "cpdp_reconcile",
-                 "cpdp_localsgd_sync", "cpdp_ddp_step", "cpdp_is_sync_step"):
+                 "cpdp_localsgd_sync", "cpdp_ddp_step", "cpdp_state_init_opt",
+                 "cpdp_local_step_opt", "cpdp_sync_step_opt", "cpdp_is_sync_step"):
         getattr(lib, name).restype = ctypes.c_int
     return lib
 
@@ -156,3 +179,34 @@ def cpdp_ddp_step(params, mom, grads, W, P, ld, lr, mu, param_dt=CPDP_F32,
                           int(P), int(ld), float(lr), float(mu), _dt(param_dt),
                           _dt(grad_dt), _dt(mom_dt), _stream(stream))
     return _done(s, "cpdp_ddp_step", check)
+
+
+def _opt(opt):
+    return None if opt is None else ctypes.byref(opt)
+
+
+def cpdp_state_init_opt(theta0, params, mom, mom2, slow_mom, anchor, W, P, ld, K,
+                        param_dt=CPDP_F32, stream=None, check=True):
+    s = lib.cpdp_state_init_opt(_addr(theta0), _addr(params), _addr(mom), _addr(mom2),
+                                _addr(slow_mom), _addr(anchor), int(W), int(P), int(ld),
+                                int(K), _dt(param_dt), _stream(stream))
+    return _done(s, "cpdp_state_init_opt", check)
+
+
+def cpdp_local_step_opt(params, mom, mom2, grads, W, P, ld, K, opt, param_dt=CPDP_F32,
+                        stream=None, check=True):
+    s = lib.cpdp_local_step_opt(_addr(params), _addr(mom), _addr(mom2), _addr(grads),
+                                int(W), int(P), int(ld), int(K), _opt(opt),
+                                _dt(param_dt), _stream(stream))
+    return _done(s, "cpdp_local_step_opt", check)
+
+
+def cpdp_sync_step_opt(strategy, params, mom, mom2, grads, slow_mom, anchor, W, P, ld, K,
+                       opt, beta=0.0, alpha=1.0, param_dt=CPDP_F32, stream=None,
+                       check=True):
+    strategy = SYNC_KINDS[strategy] if isinstance(strategy, str) else int(strategy)
+    s = lib.cpdp_sync_step_opt(strategy, _addr(params), _addr(mom), _addr(mom2),
+                               _addr(grads), _addr(slow_mom), _addr(anchor), int(W),
+                               int(P), int(ld), int(K), _opt(opt), float(beta),
+                               float(alpha), _dt(param_dt), _stream(stream))
+    return _done(s, "cpdp_sync_step_opt", check)

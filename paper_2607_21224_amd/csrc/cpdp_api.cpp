@@ -76,6 +76,49 @@ int hip_status(int err) { return err == 0 ? CPDP_OK : CPDP_ERR_HIP; }
 
 cpdp::Param param_kind(int dt) { return dt == CPDP_BF16 ? cpdp::Param::BF16 : cpdp::Param::F32; }
 
+cpdp::OptParams plain_sgd(float lr, float mu) {
+    cpdp::OptParams o{};
+    o.lr = lr;
+    o.mu = mu;
+    return o;
+}
+
+// Validates an optimizer descriptor and folds it into kernel scalars.
+int make_opt(const cpdp_optimizer* opt, cpdp::Opt* kind, cpdp::OptParams* o) {
+    if (opt == nullptr) return CPDP_ERR_NULL;
+    *o = cpdp::OptParams{};
+    const float lr = opt->lr, wd = opt->weight_decay;
+    if (!(finite(lr) && lr > 0.0f)) return CPDP_ERR_INVALID_ARG;
+    if (!(opt->momentum >= 0.0f && opt->momentum < 1.0f)) return CPDP_ERR_INVALID_ARG;
+    if (!(finite(wd) && wd >= 0.0f)) return CPDP_ERR_INVALID_ARG;
+    o->lr = lr;
+    o->mu = opt->momentum;
+    if (opt->kind == CPDP_OPT_SGD) {
+        *kind = wd != 0.0f ? cpdp::Opt::SGD_WD : cpdp::Opt::SGD;
+        o->wd = wd;
+        return CPDP_OK;
+    }
+    if (opt->kind != CPDP_OPT_ADAMW) return CPDP_ERR_INVALID_ARG;
+    const float b2 = opt->beta2, eps = opt->eps;
+    if (!(b2 >= 0.0f && b2 < 1.0f)) return CPDP_ERR_INVALID_ARG;
+    if (!(finite(eps) && eps > 0.0f)) return CPDP_ERR_INVALID_ARG;
+    if (opt->step < 1) return CPDP_ERR_INVALID_ARG;
+    if (!((double)lr * wd < 1.0)) return CPDP_ERR_INVALID_ARG;
+    *kind = cpdp::Opt::ADAMW;
+    const double t = (double)opt->step;
+    const double bc1 = 1.0 - std::pow((double)opt->momentum, t);
+    const double bc2 = 1.0 - std::pow((double)b2, t);
+    if (!(bc1 > 0.0 && bc2 > 0.0)) return CPDP_ERR_INVALID_ARG;
+    o->omb1 = 1.0f - opt->momentum;
+    o->beta2 = b2;
+    o->omb2 = 1.0f - b2;
+    o->eps = eps;
+    o->step_size = (float)((double)lr / bc1);
+    o->sqrt_bc2 = (float)std::sqrt(bc2);
+    o->decay = (float)(1.0 - (double)lr * wd);
+    return CPDP_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -94,8 +137,8 @@ int cpdp_state_init(const void* theta0, void* params, void* mom, float* slow_mom
     const size_t row_es[] = {0, sp, 4, 0, 0};
     if (int s = check_pointers(ptrs, ranges, row_es, 5, ld)) return s;
     return hip_status(cpdp::launch_state_init(param_kind(param_dt), theta0, params,
-                                              static_cast<float*>(mom), slow_mom, anchor, W, P,
-                                              ld, stream));
+                                              static_cast<float*>(mom), nullptr, slow_mom,
+                                              anchor, W, P, ld, stream));
 }
 
 int cpdp_local_step(void* params, void* mom, const void* grads, int W, int64_t P, int64_t ld,
@@ -112,10 +155,10 @@ int cpdp_local_step(void* params, void* mom, const void* grads, int W, int64_t P
                             rows(grads, W, P, ld, 4)};
     const size_t row_es[] = {sp, 4, 4};
     if (int s = check_pointers(ptrs, ranges, row_es, 3, ld)) return s;
-    return hip_status(cpdp::launch_local_step(param_kind(param_dt), params,
-                                              static_cast<float*>(mom),
-                                              static_cast<const float*>(grads), W, P, ld, lr, mu,
-                                              stream));
+    return hip_status(cpdp::launch_local_step(cpdp::Opt::SGD, plain_sgd(lr, mu),
+                                              param_kind(param_dt), params,
+                                              static_cast<float*>(mom), nullptr,
+                                              static_cast<const float*>(grads), W, P, ld, stream));
 }
 
 int cpdp_reconcile(void* params, void* mom, const void* grads, float* slow_mom, float* anchor,
@@ -134,9 +177,10 @@ int cpdp_reconcile(void* params, void* mom, const void* grads, float* slow_mom, 
                             rows(grads, W, P, ld, 4), vec(slow_mom, P, 4), vec(anchor, P, 4)};
     const size_t row_es[] = {sp, 4, 4, 0, 0};
     if (int s = check_pointers(ptrs, ranges, row_es, 5, ld)) return s;
-    return hip_status(cpdp::launch_sync(cpdp::Sync::CPDP, param_kind(param_dt), params,
-                                        static_cast<float*>(mom), static_cast<const float*>(grads),
-                                        slow_mom, anchor, W, P, ld, lr, mu, beta, alpha, stream));
+    return hip_status(cpdp::launch_sync(cpdp::Sync::CPDP, cpdp::Opt::SGD, plain_sgd(lr, mu),
+                                        param_kind(param_dt), params, static_cast<float*>(mom),
+                                        nullptr, static_cast<const float*>(grads), slow_mom,
+                                        anchor, W, P, ld, beta, alpha, stream));
 }
 
 int cpdp_localsgd_sync(void* params, void* mom, const void* grads, float* anchor, int W,
@@ -155,9 +199,10 @@ int cpdp_localsgd_sync(void* params, void* mom, const void* grads, float* anchor
                             rows(grads, W, P, ld, 4), vec(anchor, P, 4)};
     const size_t row_es[] = {sp, 4, 4, 0};
     if (int s = check_pointers(ptrs, ranges, row_es, n, ld)) return s;
-    return hip_status(cpdp::launch_sync(cpdp::Sync::LocalSGD, param_kind(param_dt), params,
-                                        static_cast<float*>(mom), static_cast<const float*>(grads),
-                                        nullptr, anchor, W, P, ld, lr, mu, 0.0f, 1.0f, stream));
+    return hip_status(cpdp::launch_sync(cpdp::Sync::LocalSGD, cpdp::Opt::SGD, plain_sgd(lr, mu),
+                                        param_kind(param_dt), params, static_cast<float*>(mom),
+                                        nullptr, static_cast<const float*>(grads), nullptr,
+                                        anchor, W, P, ld, 0.0f, 1.0f, stream));
 }
 
 int cpdp_ddp_step(void* params, void* mom, const void* grads, int W, int64_t P, int64_t ld,
@@ -173,9 +218,99 @@ int cpdp_ddp_step(void* params, void* mom, const void* grads, int W, int64_t P, 
                             rows(grads, W, P, ld, 4)};
     const size_t row_es[] = {sp, 4, 4};
     if (int s = check_pointers(ptrs, ranges, row_es, 3, ld)) return s;
-    return hip_status(cpdp::launch_sync(cpdp::Sync::DDP, param_kind(param_dt), params,
-                                        static_cast<float*>(mom), static_cast<const float*>(grads),
-                                        nullptr, nullptr, W, P, ld, lr, mu, 0.0f, 1.0f, stream));
+    return hip_status(cpdp::launch_sync(cpdp::Sync::DDP, cpdp::Opt::SGD, plain_sgd(lr, mu),
+                                        param_kind(param_dt), params, static_cast<float*>(mom),
+                                        nullptr, static_cast<const float*>(grads), nullptr,
+                                        nullptr, W, P, ld, 0.0f, 1.0f, stream));
+}
+
+int cpdp_state_init_opt(const void* theta0, void* params, void* mom, void* mom2,
+                        float* slow_mom, float* anchor, int W, int64_t P, int64_t ld, int K,
+                        int param_dt, void* stream) {
+    if (int s = check_shape(W, P, ld, K)) return s;
+    if (!is_dtype(param_dt)) return CPDP_ERR_DTYPE;
+    if (P == 0) return CPDP_OK;
+    if (!cpdp::grid_fits(1, P)) return CPDP_ERR_INVALID_ARG;
+    const size_t sp = esize(param_dt);
+    const int n = mom2 != nullptr ? 6 : 5;
+    const void* ptrs[] = {theta0, params, mom, slow_mom, anchor, mom2};
+    const Range ranges[] = {vec(theta0, P, sp),    rows(params, W, P, ld, sp),
+                            rows(mom, W, P, ld, 4), vec(slow_mom, P, 4),
+                            vec(anchor, P, 4),      rows(mom2, W, P, ld, 4)};
+    const size_t row_es[] = {0, sp, 4, 0, 0, 4};
+    if (int s = check_pointers(ptrs, ranges, row_es, n, ld)) return s;
+    return hip_status(cpdp::launch_state_init(param_kind(param_dt), theta0, params,
+                                              static_cast<float*>(mom),
+                                              static_cast<float*>(mom2), slow_mom, anchor, W, P,
+                                              ld, stream));
+}
+
+int cpdp_local_step_opt(void* params, void* mom, void* mom2, const void* grads, int W,
+                        int64_t P, int64_t ld, int K, const cpdp_optimizer* opt, int param_dt,
+                        void* stream) {
+    if (int s = check_shape(W, P, ld, K)) return s;
+    cpdp::Opt kind;
+    cpdp::OptParams o;
+    if (int s = make_opt(opt, &kind, &o)) return s;
+    if (!is_dtype(param_dt)) return CPDP_ERR_DTYPE;
+    if (P == 0) return CPDP_OK;
+    if (!cpdp::grid_fits(W, P)) return CPDP_ERR_INVALID_ARG;
+    const bool adam = kind == cpdp::Opt::ADAMW;
+    const size_t sp = esize(param_dt);
+    const void* ptrs[] = {params, mom, grads, mom2};
+    const Range ranges[] = {rows(params, W, P, ld, sp), rows(mom, W, P, ld, 4),
+                            rows(grads, W, P, ld, 4), rows(mom2, W, P, ld, 4)};
+    const size_t row_es[] = {sp, 4, 4, 4};
+    if (int s = check_pointers(ptrs, ranges, row_es, adam ? 4 : 3, ld)) return s;
+    return hip_status(cpdp::launch_local_step(kind, o, param_kind(param_dt), params,
+                                              static_cast<float*>(mom),
+                                              adam ? static_cast<float*>(mom2) : nullptr,
+                                              static_cast<const float*>(grads), W, P, ld, stream));
+}
+
+int cpdp_sync_step_opt(int strategy, void* params, void* mom, void* mom2, const void* grads,
+                       float* slow_mom, float* anchor, int W, int64_t P, int64_t ld, int K,
+                       const cpdp_optimizer* opt, float beta, float alpha, int param_dt,
+                       void* stream) {
+    if (int s = check_shape(W, P, ld, K)) return s;
+    if (strategy != CPDP_SYNC_CPDP && strategy != CPDP_SYNC_LOCALSGD &&
+        strategy != CPDP_SYNC_DDP)
+        return CPDP_ERR_INVALID_ARG;
+    cpdp::Opt kind;
+    cpdp::OptParams o;
+    if (int s = make_opt(opt, &kind, &o)) return s;
+    const bool cpdp_sync = strategy == CPDP_SYNC_CPDP;
+    if (cpdp_sync) {
+        if (!(beta >= 0.0f && beta < 1.0f)) return CPDP_ERR_INVALID_ARG;
+        if (!(finite(alpha) && alpha > 0.0f)) return CPDP_ERR_INVALID_ARG;
+    }
+    if (!is_dtype(param_dt)) return CPDP_ERR_DTYPE;
+    if (P == 0) return CPDP_OK;
+    if (!cpdp::grid_fits(1, P)) return CPDP_ERR_INVALID_ARG;
+    const bool adam = kind == cpdp::Opt::ADAMW;
+    // which optional arguments this strategy / optimizer reads or writes
+    float* slow = cpdp_sync ? slow_mom : nullptr;
+    float* anc = strategy == CPDP_SYNC_DDP ? nullptr : anchor;
+    void* m2 = adam ? mom2 : nullptr;
+    if (cpdp_sync && (slow_mom == nullptr || anchor == nullptr)) return CPDP_ERR_NULL;
+    if (adam && mom2 == nullptr) return CPDP_ERR_NULL;
+    const size_t sp = esize(param_dt);
+    const void* ptrs[6] = {params, mom, grads};
+    Range ranges[6] = {rows(params, W, P, ld, sp), rows(mom, W, P, ld, 4),
+                       rows(grads, W, P, ld, 4)};
+    size_t row_es[6] = {sp, 4, 4};
+    int n = 3;
+    if (m2) { ptrs[n] = m2; ranges[n] = rows(m2, W, P, ld, 4); row_es[n++] = 4; }
+    if (slow) { ptrs[n] = slow; ranges[n] = vec(slow, P, 4); row_es[n++] = 0; }
+    if (anc) { ptrs[n] = anc; ranges[n] = vec(anc, P, 4); row_es[n++] = 0; }
+    if (int s = check_pointers(ptrs, ranges, row_es, n, ld)) return s;
+    const cpdp::Sync mode = cpdp_sync ? cpdp::Sync::CPDP
+                            : strategy == CPDP_SYNC_LOCALSGD ? cpdp::Sync::LocalSGD
+                                                             : cpdp::Sync::DDP;
+    return hip_status(cpdp::launch_sync(mode, kind, o, param_kind(param_dt), params,
+                                        static_cast<float*>(mom), static_cast<float*>(m2),
+                                        static_cast<const float*>(grads), slow, anc, W, P, ld,
+                                        beta, alpha, stream));
 }
 
 int cpdp_is_sync_step(int64_t t, int K, int64_t T) {

@@ -1,7 +1,9 @@
-// gfx950 kernels of the CPDP reconcile hot path (state initialisation, local
-// momentum-SGD step, fused reconcile).
+// gfx950 kernels of the CPDP reconcile hot path: state initialisation, the
+// local optimizer step, and the fused synchronisation step of the three
+// strategies (CPDP reconcile, LocalSGD averaging, DDP gradient step), each for
+// momentum SGD, SGD with weight decay, or AdamW.
 //
-// All three are HBM-streaming kernels: nothing here is a dense contraction, so
+// All of them are HBM-streaming kernels: nothing here is a dense contraction, so
 // there is no MFMA and no LDS.  Every thread owns VEC = 4 consecutive
 // coordinates and moves them with 128-bit (fp32) or 64-bit (bf16) vector
 // accesses; a wavefront therefore touches 1 KiB (fp32) of each array row per
@@ -10,7 +12,7 @@
 // cross-replica sums run in a fixed order (replica 0, 1, ..., W-1) inside one
 // thread, so results are bitwise independent of the launch shape.
 //
-// Arithmetic is fp32 with explicit fmaf at the two optimizer updates and the
+// Arithmetic is fp32 with explicit fmaf in the optimizer updates and the
 // SlowMo step (the library is built with -ffp-contract=off so nothing else is
 // fused).  bf16 parameters are widened on load and rounded to nearest-even on
 // every store, including the x_i fed to the parameter mean, where the
@@ -139,8 +141,8 @@ struct ParamBF16 {
 
 template <class PS, bool FULL>
 __device__ __forceinline__ void init_chunk(const typename PS::T* theta0, typename PS::T* params,
-                                           float* mom, float* slow, float* anchor, int W,
-                                           int64_t ld, int64_t p0, int n) {
+                                           float* mom, float* mom2, float* slow, float* anchor,
+                                           int W, int64_t ld, int64_t p0, int n) {
     float th[kVec];
     const float zero[kVec] = {0.0f, 0.0f, 0.0f, 0.0f};
     PS::template load<FULL, false>(theta0 + p0, n, th);
@@ -148,6 +150,7 @@ __device__ __forceinline__ void init_chunk(const typename PS::T* theta0, typenam
         const int64_t off = (int64_t)i * ld + p0;
         PS::template store<FULL, kNTS>(params + off, n, th);
         store_f32<FULL, kNTS>(mom + off, n, zero);
+        if (mom2 != nullptr) store_f32<FULL, kNTS>(mom2 + off, n, zero);
     }
     store_f32<FULL, kNTS>(slow + p0, n, zero);
     store_f32<FULL, kNTS>(anchor + p0, n, th);
@@ -156,49 +159,83 @@ __device__ __forceinline__ void init_chunk(const typename PS::T* theta0, typenam
 template <class PS>
 __global__ __launch_bounds__(kBlock) void state_init_kernel(
     const typename PS::T* __restrict__ theta0, typename PS::T* __restrict__ params,
-    float* __restrict__ mom, float* __restrict__ slow, float* __restrict__ anchor, int W,
-    int64_t ld, int64_t P) {
+    float* __restrict__ mom, float* __restrict__ mom2, float* __restrict__ slow,
+    float* __restrict__ anchor, int W, int64_t ld, int64_t P) {
     const int64_t p0 = ((int64_t)blockIdx.x * kBlock + threadIdx.x) * kVec;
     if (p0 >= P) return;
     if (p0 + kVec <= P)
-        init_chunk<PS, true>(theta0, params, mom, slow, anchor, W, ld, p0, kVec);
+        init_chunk<PS, true>(theta0, params, mom, mom2, slow, anchor, W, ld, p0, kVec);
     else
-        init_chunk<PS, false>(theta0, params, mom, slow, anchor, W, ld, p0, (int)(P - p0));
+        init_chunk<PS, false>(theta0, params, mom, mom2, slow, anchor, W, ld, p0,
+                              (int)(P - p0));
+}
+
+// ---- the per-replica optimizer update -------------------------------------------
+//
+// One coordinate of one replica: th is the stored parameter (widened), m / v
+// the optimizer state, g the gradient the update uses.  Returns the new
+// parameter, rounded to the parameter storage type (the value the optimizer
+// writes to the parameter tensor).
+//   SGD     m <- mu m + g;              th <- th - lr m
+//   SGD_WD  d = g + wd th;  m <- mu m + d;  th <- th - lr m      (coupled L2)
+//   ADAMW   th <- round(th (1 - lr wd));  m <- b1 m + (1-b1) g;
+//           v <- b2 v + (1-b2) g^2;
+//           th <- th - (lr / (1-b1^t)) m / (sqrt(v) / sqrt(1-b2^t) + eps)
+// The AdamW bias-correction factors and the decay factor are folded into
+// OptParams on the host (they depend on the step count only) and enter the
+// arithmetic as fp32 values, as they do in the framework's fp32 tensor ops.
+
+template <Opt O, class PS>
+__device__ __forceinline__ float opt_update(const OptParams& o, float th, float& m, float& v,
+                                            float g) {
+    if constexpr (O == Opt::SGD) {
+        m = fmaf(o.mu, m, g);
+        return PS::round(fmaf(-o.lr, m, th));
+    } else if constexpr (O == Opt::SGD_WD) {
+        const float d = fmaf(o.wd, th, g);
+        m = fmaf(o.mu, m, d);
+        return PS::round(fmaf(-o.lr, m, th));
+    } else {
+        const float t = PS::round(th * o.decay);
+        m = fmaf(o.omb1, g, o.mu * m);
+        v = fmaf(o.omb2, g * g, o.beta2 * v);
+        const float denom = sqrtf(v) / o.sqrt_bc2 + o.eps;
+        return PS::round(fmaf(-o.step_size, m / denom, t));
+    }
 }
 
 // ---- local step: one replica row per block, 4 coordinates per thread -------
 
-template <class PS, bool FULL>
-__device__ __forceinline__ void local_chunk(typename PS::T* params, float* mom,
-                                            const float* grads, int64_t off, int n, float lr,
-                                            float mu) {
-    float g[kVec], m[kVec], th[kVec];
+template <Opt O, class PS, bool FULL>
+__device__ __forceinline__ void local_chunk(const OptParams& o, typename PS::T* params,
+                                            float* mom, float* mom2, const float* grads,
+                                            int64_t off, int n) {
+    float g[kVec], m[kVec], v[kVec] = {0.0f, 0.0f, 0.0f, 0.0f}, th[kVec];
     load_f32<FULL, kNTL>(grads + off, n, g);
     load_f32<FULL, kNTL>(mom + off, n, m);
+    if constexpr (O == Opt::ADAMW) load_f32<FULL, kNTL>(mom2 + off, n, v);
     PS::template load<FULL, kNTL>(params + off, n, th);
 #pragma unroll
-    for (int k = 0; k < kVec; ++k) {
-        m[k] = fmaf(mu, m[k], g[k]);
-        th[k] = fmaf(-lr, m[k], th[k]);
-    }
+    for (int k = 0; k < kVec; ++k) th[k] = opt_update<O, PS>(o, th[k], m[k], v[k], g[k]);
     store_f32<FULL, kNTS>(mom + off, n, m);
+    if constexpr (O == Opt::ADAMW) store_f32<FULL, kNTS>(mom2 + off, n, v);
     PS::template store<FULL, kNTS>(params + off, n, th);
 }
 
-template <class PS>
+template <Opt O, class PS>
 __global__ __launch_bounds__(kBlock) void local_step_kernel(
-    typename PS::T* __restrict__ params, float* __restrict__ mom,
-    const float* __restrict__ grads, int64_t ld, int64_t P, int64_t blocks_per_row, float lr,
-    float mu) {
+    OptParams o, typename PS::T* __restrict__ params, float* __restrict__ mom,
+    float* __restrict__ mom2, const float* __restrict__ grads, int64_t ld, int64_t P,
+    int64_t blocks_per_row) {
     const int64_t row = blockIdx.x / blocks_per_row;
     const int64_t col = blockIdx.x - row * blocks_per_row;
     const int64_t p0 = (col * kBlock + threadIdx.x) * kVec;
     if (p0 >= P) return;
     const int64_t off = row * ld + p0;
     if (p0 + kVec <= P)
-        local_chunk<PS, true>(params, mom, grads, off, kVec, lr, mu);
+        local_chunk<O, PS, true>(o, params, mom, mom2, grads, off, kVec);
     else
-        local_chunk<PS, false>(params, mom, grads, off, (int)(P - p0), lr, mu);
+        local_chunk<O, PS, false>(o, params, mom, mom2, grads, off, (int)(P - p0));
 }
 
 // ---- fused synchronisation steps ----------------------------------------------
@@ -222,14 +259,15 @@ __global__ __launch_bounds__(kBlock) void local_step_kernel(
 #endif
 constexpr int kChunk = CPDP_RECON_CHUNK;
 
-template <Sync M, int WT, class PS, bool FULL>
-__device__ __forceinline__ void sync_chunk(typename PS::T* params, float* mom,
-                                           const float* grads, float* slow, float* anchor,
-                                           int W, int64_t ld, int64_t p0, int n, float lr,
-                                           float mu, float beta, float alpha_lr,
+template <Sync M, Opt O, int WT, class PS, bool FULL>
+__device__ __forceinline__ void sync_chunk(const OptParams& o, typename PS::T* params,
+                                           float* mom, float* mom2, const float* grads,
+                                           float* slow, float* anchor, int W, int64_t ld,
+                                           int64_t p0, int n, float beta, float alpha_lr,
                                            float inv_w) {
     constexpr int C = WT > 0 ? (WT < kChunk ? WT : kChunk) : 1;
     static_assert(WT <= 0 || WT % C == 0, "replica batches must tile W");
+    constexpr bool kAdam = O == Opt::ADAMW;
     const int nw = WT > 0 ? WT : W;
 
     // gradient mean (the gradient AllReduce of a synchronisation step),
@@ -266,12 +304,13 @@ __device__ __forceinline__ void sync_chunk(typename PS::T* params, float* mom,
     float x0[kVec] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int i0 = 0; i0 < nw; i0 += C) {
-        float m[C][kVec], th[C][kVec], g[C][kVec];
+        float m[C][kVec], v[C][kVec], th[C][kVec], g[C][kVec];
 #pragma unroll
         for (int c = 0; c < C; ++c) {
             const int64_t off = (int64_t)(i0 + c) * ld + p0;
             if constexpr (M == Sync::LocalSGD) load_f32<FULL, kNTL>(grads + off, n, g[c]);
             load_f32<FULL, kNTL>(mom + off, n, m[c]);
+            if constexpr (kAdam) load_f32<FULL, kNTL>(mom2 + off, n, v[c]);
             PS::template load<FULL, kNTL>(params + off, n, th[c]);
         }
 #pragma unroll
@@ -279,8 +318,7 @@ __device__ __forceinline__ void sync_chunk(typename PS::T* params, float* mom,
 #pragma unroll
             for (int k = 0; k < kVec; ++k) {
                 const float gk = M == Sync::LocalSGD ? g[c][k] : gbar[k];
-                m[c][k] = fmaf(mu, m[c][k], gk);
-                const float x = PS::round(fmaf(-lr, m[c][k], th[c][k]));
+                const float x = opt_update<O, PS>(o, th[c][k], m[c][k], v[c][k], gk);
                 if constexpr (M == Sync::CPDP) {
                     s[k] += x - a[k];
                 } else if constexpr (M == Sync::LocalSGD) {
@@ -294,6 +332,7 @@ __device__ __forceinline__ void sync_chunk(typename PS::T* params, float* mom,
         for (int c = 0; c < C; ++c) {
             const int64_t off = (int64_t)(i0 + c) * ld + p0;
             store_f32<FULL, kNTS>(mom + off, n, m[c]);
+            if constexpr (kAdam) store_f32<FULL, kNTS>(mom2 + off, n, v[c]);
             if constexpr (M == Sync::DDP) PS::template store<FULL, kNTS>(params + off, n, th[c]);
         }
     }
@@ -304,7 +343,7 @@ __device__ __forceinline__ void sync_chunk(typename PS::T* params, float* mom,
 #pragma unroll
         for (int k = 0; k < kVec; ++k) {
             const float drift = s[k] * inv_w;  // avg - a
-            u[k] = fmaf(beta, u[k], -drift / lr);
+            u[k] = fmaf(beta, u[k], -drift / o.lr);
             a[k] = fmaf(-alpha_lr, u[k], a[k]);
         }
         store_f32<FULL, kNTS>(slow + p0, n, u);
@@ -321,20 +360,20 @@ __device__ __forceinline__ void sync_chunk(typename PS::T* params, float* mom,
         PS::template store<FULL, kNTS>(params + (int64_t)i * ld + p0, n, a);
 }
 
-template <Sync M, int WT, class PS>
+template <Sync M, Opt O, int WT, class PS>
 __global__ __launch_bounds__(kBlock) void sync_kernel(
-    typename PS::T* __restrict__ params, float* __restrict__ mom,
-    const float* __restrict__ grads, float* __restrict__ slow, float* __restrict__ anchor,
-    int W, int64_t ld, int64_t P, float lr, float mu, float beta, float alpha_lr,
+    OptParams o, typename PS::T* __restrict__ params, float* __restrict__ mom,
+    float* __restrict__ mom2, const float* __restrict__ grads, float* __restrict__ slow,
+    float* __restrict__ anchor, int W, int64_t ld, int64_t P, float beta, float alpha_lr,
     float inv_w) {
     const int64_t p0 = ((int64_t)blockIdx.x * kBlock + threadIdx.x) * kVec;
     if (p0 >= P) return;
     if (p0 + kVec <= P)
-        sync_chunk<M, WT, PS, true>(params, mom, grads, slow, anchor, W, ld, p0, kVec, lr, mu,
-                                    beta, alpha_lr, inv_w);
+        sync_chunk<M, O, WT, PS, true>(o, params, mom, mom2, grads, slow, anchor, W, ld, p0,
+                                       kVec, beta, alpha_lr, inv_w);
     else
-        sync_chunk<M, WT, PS, false>(params, mom, grads, slow, anchor, W, ld, p0,
-                                     (int)(P - p0), lr, mu, beta, alpha_lr, inv_w);
+        sync_chunk<M, O, WT, PS, false>(o, params, mom, mom2, grads, slow, anchor, W, ld, p0,
+                                        (int)(P - p0), beta, alpha_lr, inv_w);
 }
 
 // ---- launch helpers -------------------------------------------------------------
@@ -360,93 +399,112 @@ int launch(void (*kernel)(Args...), int64_t blocks, void* stream,
 }
 
 template <class PS>
-int state_init_t(const void* theta0, void* params, float* mom, float* slow, float* anchor,
+int state_init_t(const void* theta0, void* params, float* mom, float* mom2, float* slow,
+                 float* anchor, int W, int64_t P, int64_t ld, void* stream) {
+    using T = typename PS::T;
+    return launch(state_init_kernel<PS>, blocks_for(P), stream, static_cast<const T*>(theta0),
+                  static_cast<T*>(params), mom, mom2, slow, anchor, W, ld, P);
+}
+
+template <Opt O, class PS>
+int local_step_t(const OptParams& o, void* params, float* mom, float* mom2, const float* grads,
                  int W, int64_t P, int64_t ld, void* stream) {
     using T = typename PS::T;
-    return launch(state_init_kernel<PS>, blocks_for(P), stream,
-                  static_cast<const T*>(theta0), static_cast<T*>(params), mom, slow, anchor, W,
-                  ld, P);
-}
-
-template <class PS>
-int local_step_t(void* params, float* mom, const float* grads, int W, int64_t P, int64_t ld,
-                 float lr, float mu, void* stream) {
-    using T = typename PS::T;
     const int64_t bpr = blocks_for(P);
-    return launch(local_step_kernel<PS>, bpr * W, stream, static_cast<T*>(params), mom, grads,
-                  ld, P, bpr, lr, mu);
+    return launch(local_step_kernel<O, PS>, bpr * W, stream, o, static_cast<T*>(params), mom,
+                  mom2, grads, ld, P, bpr);
 }
 
-template <Sync M, int WT, class PS>
-int sync_w(void* params, float* mom, const float* grads, float* slow, float* anchor, int W,
-           int64_t P, int64_t ld, float lr, float mu, float beta, float alpha, void* stream) {
+template <Opt O>
+int local_step_p(const OptParams& o, Param pt, void* params, float* mom, float* mom2,
+                 const float* grads, int W, int64_t P, int64_t ld, void* stream) {
+    return pt == Param::BF16
+               ? local_step_t<O, ParamBF16>(o, params, mom, mom2, grads, W, P, ld, stream)
+               : local_step_t<O, ParamF32>(o, params, mom, mom2, grads, W, P, ld, stream);
+}
+
+struct SyncArgs {
+    void* params;
+    float* mom;
+    float* mom2;
+    const float* grads;
+    float* slow;
+    float* anchor;
+    int W;
+    int64_t P, ld;
+    float beta, alpha;
+    void* stream;
+};
+
+template <Sync M, Opt O, int WT, class PS>
+int sync_w(const OptParams& o, const SyncArgs& a) {
     using T = typename PS::T;
-    const float alpha_lr = alpha * lr;
-    const float inv_w = 1.0f / (float)W;
-    return launch(sync_kernel<M, WT, PS>, blocks_for(P), stream, static_cast<T*>(params), mom,
-                  grads, slow, anchor, W, ld, P, lr, mu, beta, alpha_lr, inv_w);
+    const float alpha_lr = a.alpha * o.lr;
+    const float inv_w = 1.0f / (float)a.W;
+    return launch(sync_kernel<M, O, WT, PS>, blocks_for(a.P), a.stream, o,
+                  static_cast<T*>(a.params), a.mom, a.mom2, a.grads, a.slow, a.anchor, a.W,
+                  a.ld, a.P, a.beta, alpha_lr, inv_w);
 }
 
-template <Sync M, class PS>
-int sync_t(void* params, float* mom, const float* grads, float* slow, float* anchor, int W,
-           int64_t P, int64_t ld, float lr, float mu, float beta, float alpha, void* stream) {
-#define CPDP_W_CASE(N)                                                                     \
-    case N:                                                                                \
-        return sync_w<M, N, PS>(params, mom, grads, slow, anchor, W, P, ld, lr, mu, beta, \
-                                alpha, stream);
-    switch (W) {
-        CPDP_W_CASE(1)
-        CPDP_W_CASE(2)
-        CPDP_W_CASE(4)
-        CPDP_W_CASE(8)
-        CPDP_W_CASE(16)
-        CPDP_W_CASE(32)
-        default:
-            return sync_w<M, 0, PS>(params, mom, grads, slow, anchor, W, P, ld, lr, mu, beta,
-                                    alpha, stream);
+template <Sync M, Opt O, class PS>
+int sync_t(const OptParams& o, const SyncArgs& a) {
+    switch (a.W) {
+        case 1: return sync_w<M, O, 1, PS>(o, a);
+        case 2: return sync_w<M, O, 2, PS>(o, a);
+        case 4: return sync_w<M, O, 4, PS>(o, a);
+        case 8: return sync_w<M, O, 8, PS>(o, a);
+        case 16: return sync_w<M, O, 16, PS>(o, a);
+        case 32: return sync_w<M, O, 32, PS>(o, a);
+        default: return sync_w<M, O, 0, PS>(o, a);
     }
-#undef CPDP_W_CASE
+}
+
+template <Sync M, Opt O>
+int sync_p(Param pt, const OptParams& o, const SyncArgs& a) {
+    return pt == Param::BF16 ? sync_t<M, O, ParamBF16>(o, a) : sync_t<M, O, ParamF32>(o, a);
 }
 
 template <Sync M>
-int sync_p(Param pt, void* params, float* mom, const float* grads, float* slow, float* anchor,
-           int W, int64_t P, int64_t ld, float lr, float mu, float beta, float alpha,
-           void* stream) {
-    return pt == Param::BF16 ? sync_t<M, ParamBF16>(params, mom, grads, slow, anchor, W, P, ld,
-                                                    lr, mu, beta, alpha, stream)
-                             : sync_t<M, ParamF32>(params, mom, grads, slow, anchor, W, P, ld,
-                                                   lr, mu, beta, alpha, stream);
+int sync_o(Opt opt, Param pt, const OptParams& o, const SyncArgs& a) {
+    switch (opt) {
+        case Opt::SGD_WD: return sync_p<M, Opt::SGD_WD>(pt, o, a);
+        case Opt::ADAMW: return sync_p<M, Opt::ADAMW>(pt, o, a);
+        default: return sync_p<M, Opt::SGD>(pt, o, a);
+    }
 }
 
 }  // namespace
 
-int launch_state_init(Param pt, const void* theta0, void* params, float* mom, float* slow,
-                      float* anchor, int W, int64_t P, int64_t ld, void* stream) {
+int launch_state_init(Param pt, const void* theta0, void* params, float* mom, float* mom2,
+                      float* slow, float* anchor, int W, int64_t P, int64_t ld, void* stream) {
     return pt == Param::BF16
-               ? state_init_t<ParamBF16>(theta0, params, mom, slow, anchor, W, P, ld, stream)
-               : state_init_t<ParamF32>(theta0, params, mom, slow, anchor, W, P, ld, stream);
+               ? state_init_t<ParamBF16>(theta0, params, mom, mom2, slow, anchor, W, P, ld,
+                                         stream)
+               : state_init_t<ParamF32>(theta0, params, mom, mom2, slow, anchor, W, P, ld,
+                                        stream);
 }
 
-int launch_local_step(Param pt, void* params, float* mom, const float* grads, int W, int64_t P,
-                      int64_t ld, float lr, float mu, void* stream) {
-    return pt == Param::BF16
-               ? local_step_t<ParamBF16>(params, mom, grads, W, P, ld, lr, mu, stream)
-               : local_step_t<ParamF32>(params, mom, grads, W, P, ld, lr, mu, stream);
-}
-
-int launch_sync(Sync mode, Param pt, void* params, float* mom, const float* grads, float* slow,
-                float* anchor, int W, int64_t P, int64_t ld, float lr, float mu, float beta,
-                float alpha, void* stream) {
-    switch (mode) {
-        case Sync::LocalSGD:
-            return sync_p<Sync::LocalSGD>(pt, params, mom, grads, slow, anchor, W, P, ld, lr, mu,
-                                          beta, alpha, stream);
-        case Sync::DDP:
-            return sync_p<Sync::DDP>(pt, params, mom, grads, slow, anchor, W, P, ld, lr, mu, beta,
-                                     alpha, stream);
+int launch_local_step(Opt opt, const OptParams& o, Param pt, void* params, float* mom,
+                      float* mom2, const float* grads, int W, int64_t P, int64_t ld,
+                      void* stream) {
+    switch (opt) {
+        case Opt::SGD_WD:
+            return local_step_p<Opt::SGD_WD>(o, pt, params, mom, mom2, grads, W, P, ld, stream);
+        case Opt::ADAMW:
+            return local_step_p<Opt::ADAMW>(o, pt, params, mom, mom2, grads, W, P, ld, stream);
         default:
-            return sync_p<Sync::CPDP>(pt, params, mom, grads, slow, anchor, W, P, ld, lr, mu, beta,
-                                      alpha, stream);
+            return local_step_p<Opt::SGD>(o, pt, params, mom, mom2, grads, W, P, ld, stream);
+    }
+}
+
+int launch_sync(Sync mode, Opt opt, const OptParams& o, Param pt, void* params, float* mom,
+                float* mom2, const float* grads, float* slow, float* anchor, int W, int64_t P,
+                int64_t ld, float beta, float alpha, void* stream) {
+    const SyncArgs a{params, mom, mom2, grads, slow, anchor, W, P, ld, beta, alpha, stream};
+    switch (mode) {
+        case Sync::LocalSGD: return sync_o<Sync::LocalSGD>(opt, pt, o, a);
+        case Sync::DDP: return sync_o<Sync::DDP>(opt, pt, o, a);
+        default: return sync_o<Sync::CPDP>(opt, pt, o, a);
     }
 }
 

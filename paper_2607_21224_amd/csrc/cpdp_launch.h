@@ -10,22 +10,42 @@ namespace cpdp {
 
 enum class Param { F32, BF16 };
 
-int launch_state_init(Param pt, const void* theta0, void* params, float* mom,
-                      float* slow, float* anchor, int W, int64_t P, int64_t ld,
-                      void* stream);
+// The per-replica optimizer update: momentum SGD, SGD with coupled weight
+// decay, or AdamW.
+enum class Opt { SGD, SGD_WD, ADAMW };
 
-int launch_local_step(Param pt, void* params, float* mom, const float* grads,
-                      int W, int64_t P, int64_t ld, float lr, float mu,
-                      void* stream);
+// Scalars of one optimizer update, in the fp32 form the kernels use.  The
+// AdamW entries that depend on the step count t are folded on the host.
+struct OptParams {
+    float lr;            // learning rate
+    float mu;            // SGD momentum, or AdamW beta1
+    float wd;            // SGD coupled weight decay
+    float omb1;          // AdamW: 1 - beta1
+    float beta2;         // AdamW
+    float omb2;          // AdamW: 1 - beta2
+    float eps;           // AdamW
+    float step_size;     // AdamW: lr / (1 - beta1^t)
+    float sqrt_bc2;      // AdamW: sqrt(1 - beta2^t)
+    float decay;         // AdamW: 1 - lr * weight_decay
+};
 
 // Synchronisation step of one of the three strategies (CPDP reconcile,
 // LocalSGD averaging, DDP gradient step).  slow/anchor are read and written
 // by CPDP; LocalSGD writes anchor only when it is not NULL; DDP uses neither.
+// mom2 (AdamW second moments) is used by Opt::ADAMW only.
 enum class Sync { CPDP, LocalSGD, DDP };
 
-int launch_sync(Sync mode, Param pt, void* params, float* mom,
-                const float* grads, float* slow, float* anchor, int W,
-                int64_t P, int64_t ld, float lr, float mu, float beta,
+int launch_state_init(Param pt, const void* theta0, void* params, float* mom,
+                      float* mom2, float* slow, float* anchor, int W, int64_t P,
+                      int64_t ld, void* stream);
+
+int launch_local_step(Opt opt, const OptParams& o, Param pt, void* params,
+                      float* mom, float* mom2, const float* grads, int W,
+                      int64_t P, int64_t ld, void* stream);
+
+int launch_sync(Sync mode, Opt opt, const OptParams& o, Param pt, void* params,
+                float* mom, float* mom2, const float* grads, float* slow,
+                float* anchor, int W, int64_t P, int64_t ld, float beta,
                 float alpha, void* stream);
 
 // True when a launch over P coordinates (rows = W for the row-parallel local

@@ -32,6 +32,24 @@ class Hyper:
         return Hyper(f(lr), f(mu), f(beta), f(alpha))
 
 
+@dataclass(frozen=True)
+class Optimizer:
+    """A per-replica optimizer (Table 3): "sgd" (momentum, coupled weight
+    decay) or "adamw" (betas (momentum, beta2), eps, decoupled weight decay).
+    Values are the fp32 numbers the kernels use."""
+    kind: str
+    lr: float
+    momentum: float = 0.0
+    beta2: float = 0.999
+    eps: float = 1e-8
+    weight_decay: float = 0.0
+
+    def c_struct(self, step: int) -> "cpdp.cpdp_optimizer":
+        k = {"sgd": cpdp.CPDP_OPT_SGD, "adamw": cpdp.CPDP_OPT_ADAMW}[self.kind]
+        return cpdp.cpdp_optimizer(k, self.lr, self.momentum, self.beta2, self.eps,
+                                   self.weight_decay, int(step))
+
+
 class CpdpState:
     """W replicas of a P-coordinate model with per-replica momentum, SlowMo
     velocity u and the reference (anchor) model, all in HBM."""
@@ -54,6 +72,8 @@ class CpdpState:
         self.mom = torch.empty((self.W, self.ld), dtype=torch.float32, device=device)
         self.slow_mom = torch.empty(max(self.P, 1), dtype=torch.float32, device=device)
         self.anchor = torch.empty(max(self.P, 1), dtype=torch.float32, device=device)
+        self.mom2 = None          # AdamW second moments, allocated by init_opt
+        self.opt_step = 0         # optimizer updates applied (AdamW bias correction)
 
     @property
     def torch_param_dtype(self):
@@ -97,6 +117,38 @@ class CpdpState:
                            stream)
 
     METHODS = ("cpdp", "localsgd", "ddp")
+
+    # ---- general optimizers (SGD with weight decay, AdamW) -------------------
+
+    def init_opt(self, theta0: torch.Tensor, opt: Optimizer, stream=None) -> None:
+        """Initialisation for a general optimizer (second-moment buffers for
+        AdamW are allocated and zeroed too)."""
+        assert theta0.dtype == self.params.dtype and theta0.numel() >= self.P
+        if opt.kind == "adamw" and self.mom2 is None:
+            self.mom2 = torch.empty_like(self.mom)
+        cpdp.cpdp_state_init_opt(theta0, self.params, self.mom,
+                                 self.mom2 if opt.kind == "adamw" else None,
+                                 self.slow_mom, self.anchor, self.W, self.P, self.ld,
+                                 self.K, self.param_dt, stream)
+        self.opt_step = 0
+
+    def step_opt(self, t: int, grads: torch.Tensor, opt: Optimizer, beta: float = 0.0,
+                 alpha: float = 1.0, T: int = 0, stream=None, method: str = "cpdp") -> str:
+        """One step of ``method`` with a general optimizer (see step())."""
+        self._check_grads(grads)
+        if method not in self.METHODS:
+            raise ValueError(method)
+        self.opt_step += 1
+        c = opt.c_struct(self.opt_step)
+        mom2 = self.mom2 if opt.kind == "adamw" else None
+        if method == "ddp" or cpdp.cpdp_is_sync_step(t, self.K, T):
+            cpdp.cpdp_sync_step_opt(method, self.params, self.mom, mom2, grads,
+                                    self.slow_mom, self.anchor, self.W, self.P, self.ld,
+                                    self.K, c, beta, alpha, self.param_dt, stream)
+            return "reconcile"
+        cpdp.cpdp_local_step_opt(self.params, self.mom, mom2, grads, self.W, self.P,
+                                 self.ld, self.K, c, self.param_dt, stream)
+        return "local"
 
     def step(self, t: int, grads: torch.Tensor, h: Hyper, T: int = 0,
              stream=None, method: str = "cpdp") -> str:

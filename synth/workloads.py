@@ -94,31 +94,32 @@ class Workload:
     def param_bytes(self) -> int:
         return 2 if self.param_dt == "bf16" else 4
 
-    def reconcile_bytes(self) -> int:
-        """Algorithmic HBM bytes of one reconcile: every state tensor read
-        once, every updated one written once (grads f32, mom f32, u/anchor f32)."""
-        sp = self.param_bytes()
-        read = self.W * (sp + 4 + 4) + 8
-        write = self.W * (sp + 4) + 8
-        return self.P * (read + write)
+    def _replica_bytes(self, adamw: bool) -> int:
+        """Per replica-coordinate bytes every step moves: the gradient read,
+        the optimizer state read and written (momentum, plus AdamW's second
+        moment), the parameter read and written."""
+        return 4 + (16 if adamw else 8) + 2 * self.param_bytes()
 
-    def sync_bytes(self, method: str = "cpdp") -> int:
+    def reconcile_bytes(self, adamw: bool = False) -> int:
+        """Algorithmic HBM bytes of one reconcile: every state tensor read
+        once, every updated one written once, plus u and anchor read and
+        written (grads, optimizer state, u and anchor are fp32)."""
+        return self.P * (self.W * self._replica_bytes(adamw) + 16)
+
+    def sync_bytes(self, method: str = "cpdp", adamw: bool = False) -> int:
         """Algorithmic HBM bytes of one synchronisation step of a strategy:
-        cpdp = the reconcile; localsgd = grads, mom, params read, mom, params
-        and the averaged model written; ddp = as a local step (grads, mom,
-        params read; mom, params written)."""
-        sp = self.param_bytes()
+        cpdp = the reconcile; localsgd = the per-replica traffic plus the
+        averaged model written once; ddp = the per-replica traffic only."""
         if method == "cpdp":
-            return self.reconcile_bytes()
+            return self.reconcile_bytes(adamw)
         if method == "localsgd":
-            return self.P * (self.W * (sp + 4 + 4) + self.W * (sp + 4) + 4)
+            return self.P * (self.W * self._replica_bytes(adamw) + 4)
         if method == "ddp":
-            return self.local_step_bytes()
+            return self.local_step_bytes(adamw)
         raise ValueError(method)
 
-    def local_step_bytes(self) -> int:
-        sp = self.param_bytes()
-        return self.P * self.W * (2 * sp + 4 + 2 * 4)
+    def local_step_bytes(self, adamw: bool = False) -> int:
+        return self.P * self.W * self._replica_bytes(adamw)
 
 
 def _make() -> dict[str, Workload]:

@@ -43,6 +43,15 @@ class Case:
     grad_sigma: float = 1e-3
     outlier_rate: float = 0.0
     method: str = "cpdp"
+    # general optimizer, e.g. dict(kind="adamw", lr=5e-4, momentum=0.9,
+    # beta2=0.999, eps=1e-8, weight_decay=0.05); None = plain momentum SGD
+    # with lr / mu above
+    opt: dict | None = None
+
+    def opt32(self) -> dict:
+        f = lambda x: float(np.float32(x))  # noqa: E731
+        o = {**dict(beta2=0.999, eps=1e-8, weight_decay=0.0, momentum=0.0), **self.opt}
+        return {k: (f(v) if k != "kind" else v) for k, v in o.items()}
 
     def hyper32(self):
         f = lambda x: float(np.float32(x))  # noqa: E731
@@ -78,35 +87,55 @@ def oracle_inputs(c: Case, idx: np.ndarray):
 
 
 def run_oracle(c: Case, idx: np.ndarray, on_step):
-    """on_step(step, kind, oracle_state)"""
+    """on_step(step, kind, oracle_state, mom2 or None)"""
     h = c.hyper32()
     th0, grads = oracle_inputs(c, idx)
-    oracle.run(th0, grads, c.W, c.K, c.steps, *h, T=c.T, param_dt=c.param_dt,
-               mom_dt="f32", aux_dt="f32", callback=on_step, method=c.method)
+    if c.opt is None:
+        oracle.run(th0, grads, c.W, c.K, c.steps, *h, T=c.T, param_dt=c.param_dt,
+                   mom_dt="f32", aux_dt="f32", method=c.method,
+                   callback=lambda s, k, st: on_step(s, k, st, None))
+        return
+    o = c.opt32()
+    if o["kind"] == "sgd":
+        make = lambda s: oracle.sgd(o["lr"], o["momentum"], o["weight_decay"])  # noqa: E731
+    else:
+        make = lambda s: oracle.adamw(o["lr"], o["momentum"], o["beta2"], o["eps"],  # noqa: E731
+                                      o["weight_decay"], s)
+    oracle.run_opt(th0, grads, c.W, c.K, c.steps, make, h[2], h[3], T=c.T,
+                   method=c.method, param_dt=c.param_dt, mom_dt="f32", aux_dt="f32",
+                   callback=lambda s, k, st, m2: on_step(
+                       s, k, st, m2.copy() if o["kind"] == "adamw" else None))
 
 
 class GpuRun:
     """The GPU side of a Case: state in HBM, inputs from the device generator."""
 
     def __init__(self, c: Case, stream=None):
-        from paper_2607_21224_amd.state import CpdpState, Hyper
+        from paper_2607_21224_amd.state import CpdpState, Hyper, Optimizer
         self.c = c
         self.stream = stream
         self.st = CpdpState(c.W, c.P, c.ld, c.K, c.param_dt, device="cuda")
         self.h = Hyper(*c.hyper32())
+        self.opt = Optimizer(**c.opt32()) if c.opt is not None else None
         self.grads = torch.empty((c.W, self.st.ld), dtype=torch.float32,
                                  device="cuda")
         th = torch.empty(max(c.P, 1), dtype=torch.float32, device="cuda")
         sdev.fill_theta0(th, c.P, c.seed, c.theta_sigma, stream=stream)
         if c.param_dt == "bf16":
             th = th.to(torch.bfloat16)
-        self.st.init(th, stream=stream)
+        if self.opt is None:
+            self.st.init(th, stream=stream)
+        else:
+            self.st.init_opt(th, self.opt, stream=stream)
 
     def step(self, step: int) -> str:
         c = self.c
         sdev.fill_grads(self.grads, c.P, c.seed, step, c.grad_sigma,
                         c.outlier_rate, stream=self.stream)
         t = ((step - 1) % c.T) + 1 if c.T > 0 else step
+        if self.opt is not None:
+            return self.st.step_opt(t, self.grads, self.opt, self.h.beta, self.h.alpha,
+                                    c.T, stream=self.stream, method=c.method)
         return self.st.step(t, self.grads, self.h, c.T, stream=self.stream,
                             method=c.method)
 
@@ -119,20 +148,43 @@ class GpuRun:
         else:
             ti = torch.from_numpy(idx).to("cuda")
             get = lambda x: x.index_select(x.dim() - 1, ti)  # noqa: E731
+        names = ["params", "mom", "slow_mom", "anchor"]
+        if self.st.mom2 is not None:
+            names.append("mom2")
         out = {k: get(getattr(self.st, k)).float().cpu().numpy().astype(np.float64)
-               for k in ("params", "mom", "slow_mom", "anchor")}
+               for k in names}
         return out
 
 
-def compare(gpu: dict, ref: "oracle.OracleState", param_dt: str, tag: str):
-    """Assert the GPU snapshot matches the oracle state within tolerance."""
-    pairs = [("params", ref.params), ("mom", ref.mom), ("slow_mom", ref.slow),
+def compare(gpu: dict, ref: "oracle.OracleState", param_dt: str, tag: str,
+            mom2=None, scaled: bool = False, velocity_lr: float | None = None):
+    """Assert the GPU snapshot matches the oracle state within tolerance.
+    scaled=True additionally tightens the fp32 absolute tolerance of the
+    optimizer-state families (mom, mom2) to 1e-6 of their RMS: AdamW moments
+    are orders of magnitude below the parameters, where a fixed 1e-7 would be
+    vacuous.  Parameters, u and anchor keep the stated tolerance (u carries
+    the 1/lr amplification of one-ulp differences in the replicas).
+    velocity_lr=lr compares the SlowMo state as the paper's velocity
+    v = -lr*u (Sec. 3.3) instead of u: with a small lr (AdamW's 5e-4) a
+    single one-ulp difference of one fp32 replica moves u by ulp/(W*lr), above
+    a 1e-6 relative gate on u, while v is unaffected by the amplification."""
+    slow_got, slow_want = gpu["slow_mom"], ref.slow
+    if velocity_lr is not None:
+        gpu = dict(gpu, slow_mom=-velocity_lr * slow_got)
+        slow_want = -velocity_lr * slow_want
+    pairs = [("params", ref.params), ("mom", ref.mom), ("slow_mom", slow_want),
              ("anchor", ref.anchor)]
+    if mom2 is not None:
+        pairs.append(("mom2", mom2))
     for name, want in pairs:
         got = gpu[name]
         assert got.shape == want.shape, (tag, name, got.shape, want.shape)
         if param_dt == "f32":
             rtol, atol = RTOL_F32, ATOL_F32
+            if scaled and name in ("mom", "mom2"):
+                fw = want[np.isfinite(want)]
+                rms = float(np.sqrt(np.mean(fw ** 2))) if fw.size else 0.0
+                atol = min(ATOL_F32, 1e-6 * rms) if rms > 0 else ATOL_F32
         elif name == "params":
             rtol, atol = RTOL_BF16, ATOL_BF16
         else:
@@ -169,17 +221,20 @@ def run_parity(c: Case, idx: np.ndarray | None = None, stream=None):
     """Run a Case on both sides and compare after every step."""
     P = c.P
     sel = np.arange(P) if idx is None else idx
-    log(f"[parity] {c.method} W={c.W} P={P} K={c.K} steps={c.steps} dt={c.param_dt} "
+    log(f"[parity] {c.method} {c.opt['kind'] if c.opt else 'sgd'} W={c.W} P={P} K={c.K} "
+        f"steps={c.steps} dt={c.param_dt} "
         f"seed={c.seed} ld={c.ld} coords={sel.size}")
     refs = {}
-    run_oracle(c, sel, lambda s, kind, st: refs.__setitem__(s, (kind, st.copy())))
+    run_oracle(c, sel, lambda s, kind, st, m2: refs.__setitem__(s, (kind, st.copy(), m2)))
     g = GpuRun(c, stream)
     for s in range(1, c.steps + 1):
         kind = g.step(s)
         snap = g.snapshot(idx)
-        rk, ref = refs[s]
+        rk, ref, m2 = refs[s]
         assert kind == rk, (s, kind, rk)
-        compare(snap, ref, c.param_dt, f"step {s} ({kind})")
+        vlr = c.opt32()["lr"] if c.opt is not None and c.opt["kind"] == "adamw" else None
+        compare(snap, ref, c.param_dt, f"step {s} ({kind})", mom2=m2,
+                scaled=c.opt is not None, velocity_lr=vlr)
         if kind == "reconcile" and c.method != "ddp":
             check_replicas_reconciled(snap, c.param_dt, f"step {s}")
     log(f"[parity] ok: {c.steps} steps")

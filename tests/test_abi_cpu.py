@@ -203,3 +203,68 @@ def test_localsgd_anchor_checks():
     assert lsgd(K=0) == E.CPDP_ERR_INVALID_ARG
     assert lsgd(anchor=V + 4) == E.CPDP_ERR_MISALIGNED
     assert lsgd(anchor=A + 64) == E.CPDP_ERR_OVERLAP
+
+
+def opt_struct(kind=0, lr=0.1, momentum=0.9, beta2=0.999, eps=1e-8, wd=0.0, step=1):
+    return cpdp.cpdp_optimizer(kind, lr, momentum, beta2, eps, wd, step)
+
+
+M2 = A + 6 * (1 << 36)
+
+
+def lopt(opt=None, **kw):
+    a = dict(GOOD, params=A, mom=B, mom2=M2, grads=C, pdt=0)
+    a.update(kw)
+    return cpdp.cpdp_local_step_opt(a["params"], a["mom"], a["mom2"], a["grads"], a["W"],
+                                    a["P"], a["ld"], a["K"], opt, a["pdt"], None, check=False)
+
+
+def sopt(strategy=0, opt=None, **kw):
+    a = dict(GOOD, params=A, mom=B, mom2=M2, grads=C, slow=U, anchor=V, pdt=0)
+    a.update(kw)
+    return cpdp.cpdp_sync_step_opt(strategy, a["params"], a["mom"], a["mom2"], a["grads"],
+                                   a["slow"], a["anchor"], a["W"], a["P"], a["ld"], a["K"],
+                                   opt, a["beta"], a["alpha"], a["pdt"], None, check=False)
+
+
+BAD_OPTS = [dict(kind=2), dict(lr=0.0), dict(lr=float("nan")), dict(momentum=1.0),
+            dict(wd=-1.0), dict(wd=float("inf")),
+            dict(kind=1, beta2=1.0), dict(kind=1, eps=0.0), dict(kind=1, step=0),
+            dict(kind=1, lr=1.0, wd=1.0), dict(kind=1, momentum=0.0, beta2=0.0, step=1,
+                                               eps=float("nan"))]
+
+
+@pytest.mark.parametrize("bad", BAD_OPTS)
+def test_opt_validation(bad):
+    o = opt_struct(**bad)
+    assert lopt(o) == E.CPDP_ERR_INVALID_ARG
+    assert sopt(0, o) == E.CPDP_ERR_INVALID_ARG
+
+
+def test_opt_null_and_pointers():
+    assert lopt(None) == E.CPDP_ERR_NULL
+    assert sopt(0, None) == E.CPDP_ERR_NULL
+    adam = opt_struct(kind=1)
+    sgd = opt_struct(kind=0, wd=5e-4)
+    assert lopt(adam, mom2=None) == E.CPDP_ERR_NULL
+    assert sopt(1, adam, mom2=None) == E.CPDP_ERR_NULL
+    assert sopt(0, sgd, slow=None) == E.CPDP_ERR_NULL
+    assert sopt(0, sgd, anchor=None) == E.CPDP_ERR_NULL
+    assert lopt(adam, mom2=B) == E.CPDP_ERR_OVERLAP
+    assert lopt(adam, mom2=M2 + 4) == E.CPDP_ERR_MISALIGNED
+    assert sopt(7, sgd) == E.CPDP_ERR_INVALID_ARG
+    assert sopt(0, sgd, beta=1.0) == E.CPDP_ERR_INVALID_ARG
+    assert sopt(0, sgd, pdt=5) == E.CPDP_ERR_DTYPE
+    # SGD ignores mom2 and DDP ignores slow/anchor: only validated when used
+    assert sopt(2, sgd, P=0) == E.CPDP_OK
+    assert lopt(sgd, P=0, mom2=None) == E.CPDP_OK
+
+
+def test_state_init_opt_validation():
+    f = lambda **kw: cpdp.cpdp_state_init_opt(  # noqa: E731
+        kw.get("theta0", T0), A, B, kw.get("mom2", M2), U, V, kw.get("W", 4), 1000, 1024, 2,
+        kw.get("pdt", 0), None, check=False)
+    assert f(W=0) == E.CPDP_ERR_INVALID_ARG
+    assert f(pdt=3) == E.CPDP_ERR_DTYPE
+    assert f(theta0=None) == E.CPDP_ERR_NULL
+    assert f(mom2=A + 256) == E.CPDP_ERR_OVERLAP

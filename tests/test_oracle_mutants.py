@@ -55,12 +55,12 @@ MUTANTS = [
     ("ddp_drops_mu", "mu * mom[k] + gbar", "mom[k] + gbar", 2),
     ("sgd_wd_sign", "g + o->wd * *theta", "g - o->wd * *theta", 0),
     ("sgd_wd_dropped", "g + o->wd * *theta", "g", 0),
-    ("adamw_decay_dropped", "*theta * (1.0 - o->lr * o->wd)", "*theta", 0),
-    ("adamw_bc1_dropped", "(o->lr / bc1)", "o->lr", 0),
-    ("adamw_bc2_dropped", "sqrt(*v) / sqrt(bc2)", "sqrt(*v)", 0),
+    ("adamw_decay_dropped", "*theta * decay", "*theta", 0),
+    ("adamw_bc1_dropped", "o->lr / bc1", "o->lr", 0),
+    ("adamw_bc2_dropped", "sqrt(*v) / sqrt_bc2", "sqrt(*v)", 0),
     ("adamw_m_weight", "(1.0 - o->mu) * g", "g", 0),
     ("adamw_v_not_squared", "(1.0 - o->beta2) * g * g", "(1.0 - o->beta2) * g", 0),
-    ("adamw_eps_inside_sqrt", "sqrt(*v) / sqrt(bc2) + o->eps", "sqrt(*v / bc2 + o->eps)", 0),
+    ("adamw_eps_inside_sqrt", "sqrt(*v) / sqrt_bc2 + o->eps", "sqrt(*v / bc2 + o->eps)", 0),
     ("adamw_step_off_by_one", "pow(o->mu, (double)o->step)", "pow(o->mu, (double)(o->step + 1))", 0),
     ("opt_sync_local_grad", "strategy == 1 ? grads[k] : gbar", "grads[k]", 0),
     ("opt_sync_drops_beta", "beta * slow[p] + (ref - avg) / o->lr", "(ref - avg) / o->lr", 0),
