@@ -63,7 +63,7 @@ def load(path: str = _LIB_PATH) -> ctypes.CDLL:
     lib.oracle_local_step_opt.argtypes = [i, i64, i, i, i, _D, _D, _D, _D, _OPTP]
     lib.oracle_local_step_opt.restype = None
     lib.oracle_sync_opt.argtypes = [i, i, i64, i, i, i, _D, _D, _D, _D, _D, _D,
-                                    _OPTP, d, d]
+                                    _OPTP, d, d, ctypes.c_uint]
     lib.oracle_sync_opt.restype = None
     return lib
 
@@ -214,21 +214,28 @@ def local_step_opt(st: OracleState, grads, opt: OracleOpt, mom2=None) -> None:
                                 _ptr(g), ctypes.byref(opt))
 
 
+SYNC_WRITE_GBAR = 1       # write the gradient mean back into every gradient row
+SYNC_AVERAGE_STATE = 2    # optimizer-state reconciliation
+
+
 def sync_opt(st: OracleState, method: str, grads, opt: OracleOpt, beta=0.0,
-             alpha=1.0, mom2=None, write_anchor=True) -> None:
-    """Synchronisation step of ``method`` with a general optimizer."""
-    g = _grads(st, grads)
+             alpha=1.0, mom2=None, write_anchor=True, flags: int = 0):
+    """Synchronisation step of ``method`` with a general optimizer.  Returns
+    the gradient array (updated in place when SYNC_WRITE_GBAR is set)."""
+    g = np.array(grads, dtype=np.float64, order="C", copy=True)
+    assert g.shape == (st.W, st.P)
     st._l.oracle_sync_opt(_STRATEGY[method], st.W, st.P, _DT[st.param_dt],
                           _DT[st.mom_dt], _DT[st.aux_dt], _ptr(st.params),
                           _ptr(st.mom), _ptr(mom2) if mom2 is not None else None,
                           _ptr(g), _ptr(st.slow),
                           _ptr(st.anchor) if write_anchor else None,
-                          ctypes.byref(opt), float(beta), float(alpha))
+                          ctypes.byref(opt), float(beta), float(alpha), int(flags))
+    return g
 
 
 def run_opt(theta0, grad_fn, W: int, K: int, n_steps: int, make_opt, beta=0.0,
             alpha=1.0, T: int = 0, method="cpdp", param_dt="f32", mom_dt="f32",
-            aux_dt="f32", callback=None, use=None):
+            aux_dt="f32", callback=None, use=None, flags: int = 0):
     """Algorithm 1 (or a Sec. 5.3 baseline) with a general optimizer.
     make_opt(step) returns the OracleOpt of 1-based global step ``step`` (the
     AdamW step count advances on every step, local or synchronising).
@@ -242,7 +249,7 @@ def run_opt(theta0, grad_fn, W: int, K: int, n_steps: int, make_opt, beta=0.0,
         g = grad_fn(step, W, st.P)
         opt = make_opt(step)
         if method == "ddp" or is_sync_step(t, K, T):
-            sync_opt(st, method, g, opt, beta, alpha, mom2)
+            sync_opt(st, method, g, opt, beta, alpha, mom2, flags=flags)
             kind = "reconcile"
         else:
             local_step_opt(st, g, opt, mom2)

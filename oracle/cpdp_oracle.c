@@ -314,11 +314,18 @@ void oracle_local_step_opt(int W, int64_t P, int param_dt, int mom_dt,
  *                      mean, copy-back (anchor <- mean if anchor != NULL).
  *   strategy 2 (DDP): gradient mean, optimizer step with it; no averaging.
  * The SlowMo step length is the optimizer's lr, as in the SGD reconcile.
+ * flags (variants the paper names but does not use):
+ *   1  write the gradient mean back into every replica's gradient row, as a
+ *      DDP AllReduce leaves it in .grad (CPDP and DDP; LocalSGD has none).
+ *   2  optimizer-state reconciliation (Sec. 4.2 "Implication for Optimizer
+ *      State", Sec. 7 future work): after the optimizer step every replica's
+ *      momentum (and AdamW second moment) is replaced by the replica mean.
  */
 void oracle_sync_opt(int strategy, int W, int64_t P, int param_dt, int mom_dt,
                      int aux_dt, double* params, double* mom, double* mom2,
-                     const double* grads, double* slow, double* anchor,
-                     const oracle_opt* o, double beta, double alpha) {
+                     double* grads, double* slow, double* anchor,
+                     const oracle_opt* o, double beta, double alpha,
+                     unsigned flags) {
     for (int64_t p = 0; p < P; ++p) {
         double gbar = 0.0;
         if (strategy != 1) {
@@ -333,6 +340,19 @@ void oracle_sync_opt(int strategy, int W, int64_t P, int param_dt, int mom_dt,
                              mom2 ? &mom2[k] : NULL,
                              strategy == 1 ? grads[k] : gbar);
             xsum += params[k];
+        }
+        if ((flags & 1u) && strategy != 1)
+            for (int i = 0; i < W; ++i) grads[(int64_t)i * P + p] = gbar;
+        if (flags & 2u) {
+            double msum = 0.0, vsum = 0.0;
+            for (int i = 0; i < W; ++i) {
+                msum += mom[(int64_t)i * P + p];
+                if (mom2) vsum += mom2[(int64_t)i * P + p];
+            }
+            for (int i = 0; i < W; ++i) {
+                mom[(int64_t)i * P + p] = store_as(mom_dt, msum / (double)W);
+                if (mom2) mom2[(int64_t)i * P + p] = store_as(mom_dt, vsum / (double)W);
+            }
         }
         if (strategy == 2) continue;
         double avg = xsum / (double)W;

@@ -381,11 +381,13 @@ def pin_localsgd_closed_form(use=None):
 ALL_PINS += [pin_torch_baselines, pin_brute_force_baselines, pin_localsgd_closed_form]
 
 
-def _torch_opt_reference(theta0, grads, W, K, method, make_torch_opt):
+def _torch_opt_reference(theta0, grads, W, K, method, make_torch_opt,
+                         average_state=False):
     """Per-worker torch optimizers (fp64) driven like the Sec. 4.2
     implementation: averaged gradient on CPDP/DDP sync steps, local gradient
     otherwise; parameter averaging on CPDP (beta = 0, alpha = 1) and LocalSGD
-    sync steps; optimizer states never averaged."""
+    sync steps; optimizer states averaged across workers on sync steps only
+    when ``average_state`` (the optimizer-state-reconciliation variant)."""
     import torch
     ps = [torch.nn.Parameter(torch.tensor(theta0, dtype=torch.float64)) for _ in range(W)]
     opts = [make_torch_opt([p]) for p in ps]
@@ -401,6 +403,13 @@ def _torch_opt_reference(theta0, grads, W, K, method, make_torch_opt):
             avg = torch.stack([p.detach() for p in ps]).mean(0)
             for p in ps:
                 p.data.copy_(avg)
+        if sync and average_state:
+            for key in opts[0].state[ps[0]]:
+                if key == "step":
+                    continue
+                mean = torch.stack([opts[i].state[ps[i]][key] for i in range(W)]).mean(0)
+                for i in range(W):
+                    opts[i].state[ps[i]][key].copy_(mean)
         out.append(np.stack([p.detach().numpy().copy() for p in ps]))
     return out
 
@@ -490,3 +499,56 @@ def pin_general_sgd_matches_plain(use=None):
 
 ALL_PINS += [pin_torch_optimizers, pin_adamw_closed_form,
              pin_sgd_weight_decay_closed_form, pin_general_sgd_matches_plain]
+
+
+def pin_torch_state_averaging(use=None):
+    """Optimizer-state reconciliation: momentum buffers (SGD) or both AdamW
+    moments replaced by the worker mean on sync steps, against per-worker torch
+    optimizers whose states are averaged the same way."""
+    import torch
+    rng = np.random.default_rng(29)
+    for method in ("cpdp", "localsgd", "ddp"):
+        for kind in ("sgd", "adamw"):
+            W, K, P = 4, 2, 3
+            n = 3 * K + 1
+            theta0 = rng.normal(0, 1, P)
+            grads = [rng.normal(0, 1, (W, P)) for _ in range(n)]
+            if kind == "sgd":
+                topt = lambda ps: torch.optim.SGD(ps, lr=0.1, momentum=0.9, weight_decay=1e-3)  # noqa: E731
+                mk = lambda s: oracle.sgd(0.1, 0.9, 1e-3)  # noqa: E731
+            else:
+                topt = lambda ps: torch.optim.AdamW(ps, lr=1e-2, betas=(0.9, 0.99), eps=1e-6,  # noqa: E731
+                                                    weight_decay=0.01)
+                mk = lambda s: oracle.adamw(1e-2, 0.9, 0.99, 1e-6, 0.01, s)  # noqa: E731
+            ref = _torch_opt_reference(theta0, grads, W, K, method, topt, average_state=True)
+            rec = []
+            oracle.run_opt(theta0, lambda s, W_, P_: grads[s - 1], W, K, n, mk, 0.0, 1.0,
+                           method=method, param_dt="f64", mom_dt="f64", aux_dt="f64",
+                           use=use, flags=oracle.SYNC_AVERAGE_STATE,
+                           callback=lambda s, k, st, m2: rec.append(st.copy()))
+            for s, (st, p_ref) in enumerate(zip(rec, ref), start=1):
+                _close(st.params, p_ref, 1e-11, 1e-12, f"avg state {kind} {method} s={s}")
+
+
+def pin_gradient_write_back(use=None):
+    """With the write-back flag the gradient rows leave a CPDP or DDP sync
+    holding the replica-mean gradient (what a DDP AllReduce leaves in .grad),
+    LocalSGD leaves them untouched, and the rest of the state is unchanged."""
+    rng = np.random.default_rng(37)
+    W, P = 3, 5
+    theta0 = rng.normal(0, 1, P)
+    g = rng.normal(0, 1, (W, P))
+    for method in ("cpdp", "localsgd", "ddp"):
+        a = oracle.state_init(theta0, W, "f64", "f64", "f64", use=use)
+        b = a.copy()
+        ga = oracle.sync_opt(a, method, g, oracle.sgd(0.1, 0.9), 0.5, 1.0, flags=0)
+        gb = oracle.sync_opt(b, method, g, oracle.sgd(0.1, 0.9), 0.5, 1.0,
+                             flags=oracle.SYNC_WRITE_GBAR)
+        assert np.array_equal(ga, g), method
+        want = g if method == "localsgd" else np.tile(g.mean(axis=0), (W, 1))
+        _close(gb, want, 1e-15, 1e-15, f"write-back {method}")
+        for name in ("params", "mom", "slow", "anchor"):
+            assert np.array_equal(getattr(a, name), getattr(b, name)), (method, name)
+
+
+ALL_PINS += [pin_torch_state_averaging, pin_gradient_write_back]

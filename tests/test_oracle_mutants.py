@@ -65,6 +65,10 @@ MUTANTS = [
     ("opt_sync_local_grad", "strategy == 1 ? grads[k] : gbar", "grads[k]", 0),
     ("opt_sync_drops_beta", "beta * slow[p] + (ref - avg) / o->lr", "(ref - avg) / o->lr", 0),
     ("opt_sync_sign", "ref - alpha * o->lr * u", "ref + alpha * o->lr * u", 0),
+    ("avg_state_divisor", "msum / (double)W", "msum", 0),
+    ("avg_state_skips_mom2", "if (mom2) mom2[(int64_t)i * P + p] = store_as(mom_dt, vsum / (double)W);", "", 0),
+    ("write_back_wrong_value", "grads[(int64_t)i * P + p] = gbar;", "grads[(int64_t)i * P + p] = 2.0 * gbar;", 0),
+    ("write_back_for_localsgd", "if ((flags & 1u) && strategy != 1)", "if (flags & 1u)", 0),
 ]
 
 
