@@ -188,18 +188,32 @@ int cpdp_local_step_opt(void* params, void* mom, void* mom2,
                         int K, const cpdp_optimizer* opt, int param_dt,
                         void* stream);
 
+/* Optional variants of a synchronisation step (bit flags). */
+enum {
+    /* Write the replica-mean gradient into every replica's gradient row, as a
+     * DDP AllReduce leaves it in .grad (CPDP and DDP steps; LocalSGD has no
+     * gradient mean and ignores the flag).  Costs 4*W bytes per coordinate. */
+    CPDP_SYNC_WRITE_GRAD_MEAN = 1,
+    /* Optimizer-state reconciliation, the variant Sec. 4.2 names and Sec. 7
+     * leaves to future work: after the step every replica's momentum (and
+     * AdamW second moment) is replaced by the replica mean.  No extra bytes. */
+    CPDP_SYNC_AVERAGE_OPT_STATE = 2
+};
+
 /*
  * Synchronisation step of a strategy (cpdp_sync_kind) with a general
  * optimizer, in one pass over HBM.  slow_mom and anchor are required for
  * CPDP_SYNC_CPDP (with beta, alpha as in cpdp_reconcile), anchor is optional
  * for CPDP_SYNC_LOCALSGD, and neither is used by CPDP_SYNC_DDP (beta, alpha
- * are then ignored).  mom2 as in cpdp_local_step_opt.
+ * are then ignored).  mom2 as in cpdp_local_step_opt.  grads are read only
+ * unless flags has CPDP_SYNC_WRITE_GRAD_MEAN.  Unknown flag bits return
+ * CPDP_ERR_INVALID_ARG.
  */
 int cpdp_sync_step_opt(int strategy, void* params, void* mom, void* mom2,
-                       const void* grads, float* slow_mom, float* anchor,
-                       int W, int64_t P, int64_t ld, int K,
+                       void* grads, float* slow_mom, float* anchor, int W,
+                       int64_t P, int64_t ld, int K,
                        const cpdp_optimizer* opt, float beta, float alpha,
-                       int param_dt, void* stream);
+                       unsigned flags, int param_dt, void* stream);
 
 /*
  * Synchronisation indicator (Sec. 3.2) with the forced synchronisation at the

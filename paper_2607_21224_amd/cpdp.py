@@ -44,6 +44,8 @@ CPDP_SYNC_LOCALSGD = 1
 CPDP_SYNC_DDP = 2
 SYNC_KINDS = {"cpdp": CPDP_SYNC_CPDP, "localsgd": CPDP_SYNC_LOCALSGD,
               "ddp": CPDP_SYNC_DDP}
+CPDP_SYNC_WRITE_GRAD_MEAN = 1
+CPDP_SYNC_AVERAGE_OPT_STATE = 2
 
 
 class cpdp_optimizer(ctypes.Structure):
@@ -76,7 +78,7 @@ def _load() -> ctypes.CDLL:
     lib.cpdp_state_init_opt.argtypes = [vp, vp, vp, vp, vp, vp, i, i64, i64, i, i, vp]
     lib.cpdp_local_step_opt.argtypes = [vp, vp, vp, vp, i, i64, i64, i, op, i, vp]
     lib.cpdp_sync_step_opt.argtypes = [i, vp, vp, vp, vp, vp, vp, i, i64, i64, i, op,
-                                       f, f, i, vp]
+                                       f, f, ctypes.c_uint, i, vp]
     lib.cpdp_is_sync_step.argtypes = [i64, i, i64]
     lib.cpdp_status_str.argtypes = [i]
     lib.cpdp_status_str.restype = ctypes.c_char_p
@@ -202,11 +204,11 @@ def cpdp_local_step_opt(params, mom, mom2, grads, W, P, ld, K, opt, param_dt=CPD
 
 
 def cpdp_sync_step_opt(strategy, params, mom, mom2, grads, slow_mom, anchor, W, P, ld, K,
-                       opt, beta=0.0, alpha=1.0, param_dt=CPDP_F32, stream=None,
+                       opt, beta=0.0, alpha=1.0, flags=0, param_dt=CPDP_F32, stream=None,
                        check=True):
     strategy = SYNC_KINDS[strategy] if isinstance(strategy, str) else int(strategy)
     s = lib.cpdp_sync_step_opt(strategy, _addr(params), _addr(mom), _addr(mom2),
                                _addr(grads), _addr(slow_mom), _addr(anchor), int(W),
                                int(P), int(ld), int(K), _opt(opt), float(beta),
-                               float(alpha), _dt(param_dt), _stream(stream))
+                               float(alpha), int(flags), _dt(param_dt), _stream(stream))
     return _done(s, "cpdp_sync_step_opt", check)

@@ -180,7 +180,7 @@ int cpdp_reconcile(void* params, void* mom, const void* grads, float* slow_mom, 
     return hip_status(cpdp::launch_sync(cpdp::Sync::CPDP, cpdp::Opt::SGD, plain_sgd(lr, mu),
                                         param_kind(param_dt), params, static_cast<float*>(mom),
                                         nullptr, static_cast<const float*>(grads), slow_mom,
-                                        anchor, W, P, ld, beta, alpha, stream));
+                                        anchor, W, P, ld, beta, alpha, 0u, stream));
 }
 
 int cpdp_localsgd_sync(void* params, void* mom, const void* grads, float* anchor, int W,
@@ -202,7 +202,7 @@ int cpdp_localsgd_sync(void* params, void* mom, const void* grads, float* anchor
     return hip_status(cpdp::launch_sync(cpdp::Sync::LocalSGD, cpdp::Opt::SGD, plain_sgd(lr, mu),
                                         param_kind(param_dt), params, static_cast<float*>(mom),
                                         nullptr, static_cast<const float*>(grads), nullptr,
-                                        anchor, W, P, ld, 0.0f, 1.0f, stream));
+                                        anchor, W, P, ld, 0.0f, 1.0f, 0u, stream));
 }
 
 int cpdp_ddp_step(void* params, void* mom, const void* grads, int W, int64_t P, int64_t ld,
@@ -221,7 +221,7 @@ int cpdp_ddp_step(void* params, void* mom, const void* grads, int W, int64_t P, 
     return hip_status(cpdp::launch_sync(cpdp::Sync::DDP, cpdp::Opt::SGD, plain_sgd(lr, mu),
                                         param_kind(param_dt), params, static_cast<float*>(mom),
                                         nullptr, static_cast<const float*>(grads), nullptr,
-                                        nullptr, W, P, ld, 0.0f, 1.0f, stream));
+                                        nullptr, W, P, ld, 0.0f, 1.0f, 0u, stream));
 }
 
 int cpdp_state_init_opt(const void* theta0, void* params, void* mom, void* mom2,
@@ -268,11 +268,13 @@ int cpdp_local_step_opt(void* params, void* mom, void* mom2, const void* grads, 
                                               static_cast<const float*>(grads), W, P, ld, stream));
 }
 
-int cpdp_sync_step_opt(int strategy, void* params, void* mom, void* mom2, const void* grads,
+int cpdp_sync_step_opt(int strategy, void* params, void* mom, void* mom2, void* grads,
                        float* slow_mom, float* anchor, int W, int64_t P, int64_t ld, int K,
-                       const cpdp_optimizer* opt, float beta, float alpha, int param_dt,
-                       void* stream) {
+                       const cpdp_optimizer* opt, float beta, float alpha, unsigned flags,
+                       int param_dt, void* stream) {
     if (int s = check_shape(W, P, ld, K)) return s;
+    if (flags & ~(unsigned)(CPDP_SYNC_WRITE_GRAD_MEAN | CPDP_SYNC_AVERAGE_OPT_STATE))
+        return CPDP_ERR_INVALID_ARG;
     if (strategy != CPDP_SYNC_CPDP && strategy != CPDP_SYNC_LOCALSGD &&
         strategy != CPDP_SYNC_DDP)
         return CPDP_ERR_INVALID_ARG;
@@ -310,7 +312,7 @@ int cpdp_sync_step_opt(int strategy, void* params, void* mom, void* mom2, const 
     return hip_status(cpdp::launch_sync(mode, kind, o, param_kind(param_dt), params,
                                         static_cast<float*>(mom), static_cast<float*>(m2),
                                         static_cast<const float*>(grads), slow, anc, W, P, ld,
-                                        beta, alpha, stream));
+                                        beta, alpha, flags, stream));
 }
 
 int cpdp_is_sync_step(int64_t t, int K, int64_t T) {

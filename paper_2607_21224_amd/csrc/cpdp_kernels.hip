@@ -259,16 +259,23 @@ __global__ __launch_bounds__(kBlock) void local_step_kernel(
 #endif
 constexpr int kChunk = CPDP_RECON_CHUNK;
 
-template <Sync M, Opt O, int WT, class PS, bool FULL>
+// EXTRA = true enables the optional variants selected by `flags` (run-time W
+// only): kSyncWriteGbar stores the gradient mean into every gradient row;
+// kSyncAverageState replaces every replica's optimizer state by the replica
+// mean after the step.
+template <Sync M, Opt O, int WT, class PS, bool FULL, bool EXTRA>
 __device__ __forceinline__ void sync_chunk(const OptParams& o, typename PS::T* params,
                                            float* mom, float* mom2, const float* grads,
                                            float* slow, float* anchor, int W, int64_t ld,
                                            int64_t p0, int n, float beta, float alpha_lr,
-                                           float inv_w) {
+                                           float inv_w, unsigned flags) {
     constexpr int C = WT > 0 ? (WT < kChunk ? WT : kChunk) : 1;
     static_assert(WT <= 0 || WT % C == 0, "replica batches must tile W");
+    static_assert(!EXTRA || WT == 0, "variants run on the run-time-W kernel");
     constexpr bool kAdam = O == Opt::ADAMW;
     const int nw = WT > 0 ? WT : W;
+    const bool avg_state = EXTRA && (flags & kSyncAverageState);
+    float msum[kVec] = {0.0f, 0.0f, 0.0f, 0.0f}, vsum[kVec] = {0.0f, 0.0f, 0.0f, 0.0f};
 
     // gradient mean (the gradient AllReduce of a synchronisation step),
     // summed in the fixed order i = 0, 1, ..., W-1
@@ -288,6 +295,11 @@ __device__ __forceinline__ void sync_chunk(const OptParams& o, typename PS::T* p
         }
 #pragma unroll
         for (int k = 0; k < kVec; ++k) gbar[k] = acc[k] * inv_w;
+        if (EXTRA && (flags & kSyncWriteGbar)) {
+            // the gradient rows are the caller's; this variant overwrites them
+            float* g_out = const_cast<float*>(grads);
+            for (int i = 0; i < nw; ++i) store_f32<FULL, kNTS>(g_out + (int64_t)i * ld + p0, n, gbar);
+        }
     }
 
     float a[kVec], u[kVec];
@@ -331,9 +343,29 @@ __device__ __forceinline__ void sync_chunk(const OptParams& o, typename PS::T* p
 #pragma unroll
         for (int c = 0; c < C; ++c) {
             const int64_t off = (int64_t)(i0 + c) * ld + p0;
-            store_f32<FULL, kNTS>(mom + off, n, m[c]);
-            if constexpr (kAdam) store_f32<FULL, kNTS>(mom2 + off, n, v[c]);
+            if (avg_state) {
+#pragma unroll
+                for (int k = 0; k < kVec; ++k) {
+                    msum[k] += m[c][k];
+                    if constexpr (kAdam) vsum[k] += v[c][k];
+                }
+            } else {
+                store_f32<FULL, kNTS>(mom + off, n, m[c]);
+                if constexpr (kAdam) store_f32<FULL, kNTS>(mom2 + off, n, v[c]);
+            }
             if constexpr (M == Sync::DDP) PS::template store<FULL, kNTS>(params + off, n, th[c]);
+        }
+    }
+    if (avg_state) {
+#pragma unroll
+        for (int k = 0; k < kVec; ++k) {
+            msum[k] *= inv_w;
+            vsum[k] *= inv_w;
+        }
+        for (int i = 0; i < nw; ++i) {
+            const int64_t off = (int64_t)i * ld + p0;
+            store_f32<FULL, kNTS>(mom + off, n, msum);
+            if constexpr (kAdam) store_f32<FULL, kNTS>(mom2 + off, n, vsum);
         }
     }
     if constexpr (M == Sync::DDP) return;
@@ -360,20 +392,21 @@ __device__ __forceinline__ void sync_chunk(const OptParams& o, typename PS::T* p
         PS::template store<FULL, kNTS>(params + (int64_t)i * ld + p0, n, a);
 }
 
-template <Sync M, Opt O, int WT, class PS>
+template <Sync M, Opt O, int WT, class PS, bool EXTRA>
 __global__ __launch_bounds__(kBlock) void sync_kernel(
     OptParams o, typename PS::T* __restrict__ params, float* __restrict__ mom,
     float* __restrict__ mom2, const float* __restrict__ grads, float* __restrict__ slow,
     float* __restrict__ anchor, int W, int64_t ld, int64_t P, float beta, float alpha_lr,
-    float inv_w) {
+    float inv_w, unsigned flags) {
     const int64_t p0 = ((int64_t)blockIdx.x * kBlock + threadIdx.x) * kVec;
     if (p0 >= P) return;
     if (p0 + kVec <= P)
-        sync_chunk<M, O, WT, PS, true>(o, params, mom, mom2, grads, slow, anchor, W, ld, p0,
-                                       kVec, beta, alpha_lr, inv_w);
+        sync_chunk<M, O, WT, PS, true, EXTRA>(o, params, mom, mom2, grads, slow, anchor, W, ld,
+                                              p0, kVec, beta, alpha_lr, inv_w, flags);
     else
-        sync_chunk<M, O, WT, PS, false>(o, params, mom, mom2, grads, slow, anchor, W, ld, p0,
-                                        (int)(P - p0), beta, alpha_lr, inv_w);
+        sync_chunk<M, O, WT, PS, false, EXTRA>(o, params, mom, mom2, grads, slow, anchor, W,
+                                               ld, p0, (int)(P - p0), beta, alpha_lr, inv_w,
+                                               flags);
 }
 
 // ---- launch helpers -------------------------------------------------------------
@@ -433,21 +466,23 @@ struct SyncArgs {
     int W;
     int64_t P, ld;
     float beta, alpha;
+    unsigned flags;
     void* stream;
 };
 
-template <Sync M, Opt O, int WT, class PS>
+template <Sync M, Opt O, int WT, class PS, bool EXTRA = false>
 int sync_w(const OptParams& o, const SyncArgs& a) {
     using T = typename PS::T;
     const float alpha_lr = a.alpha * o.lr;
     const float inv_w = 1.0f / (float)a.W;
-    return launch(sync_kernel<M, O, WT, PS>, blocks_for(a.P), a.stream, o,
+    return launch(sync_kernel<M, O, WT, PS, EXTRA>, blocks_for(a.P), a.stream, o,
                   static_cast<T*>(a.params), a.mom, a.mom2, a.grads, a.slow, a.anchor, a.W,
-                  a.ld, a.P, a.beta, alpha_lr, inv_w);
+                  a.ld, a.P, a.beta, alpha_lr, inv_w, a.flags);
 }
 
 template <Sync M, Opt O, class PS>
 int sync_t(const OptParams& o, const SyncArgs& a) {
+    if (a.flags != 0) return sync_w<M, O, 0, PS, true>(o, a);
     switch (a.W) {
         case 1: return sync_w<M, O, 1, PS>(o, a);
         case 2: return sync_w<M, O, 2, PS>(o, a);
@@ -499,8 +534,8 @@ int launch_local_step(Opt opt, const OptParams& o, Param pt, void* params, float
 
 int launch_sync(Sync mode, Opt opt, const OptParams& o, Param pt, void* params, float* mom,
                 float* mom2, const float* grads, float* slow, float* anchor, int W, int64_t P,
-                int64_t ld, float beta, float alpha, void* stream) {
-    const SyncArgs a{params, mom, mom2, grads, slow, anchor, W, P, ld, beta, alpha, stream};
+                int64_t ld, float beta, float alpha, unsigned flags, void* stream) {
+    const SyncArgs a{params, mom, mom2, grads, slow, anchor, W, P, ld, beta, alpha, flags, stream};
     switch (mode) {
         case Sync::LocalSGD: return sync_o<Sync::LocalSGD>(opt, pt, o, a);
         case Sync::DDP: return sync_o<Sync::DDP>(opt, pt, o, a);

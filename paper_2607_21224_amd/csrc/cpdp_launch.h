@@ -35,6 +35,12 @@ struct OptParams {
 // mom2 (AdamW second moments) is used by Opt::ADAMW only.
 enum class Sync { CPDP, LocalSGD, DDP };
 
+// Optional variants of a synchronisation step (bit flags): write the gradient
+// mean back into every gradient row; average the optimizer state over the
+// replicas after the step.
+constexpr unsigned kSyncWriteGbar = 1u;
+constexpr unsigned kSyncAverageState = 2u;
+
 int launch_state_init(Param pt, const void* theta0, void* params, float* mom,
                       float* mom2, float* slow, float* anchor, int W, int64_t P,
                       int64_t ld, void* stream);
@@ -46,7 +52,7 @@ int launch_local_step(Opt opt, const OptParams& o, Param pt, void* params,
 int launch_sync(Sync mode, Opt opt, const OptParams& o, Param pt, void* params,
                 float* mom, float* mom2, const float* grads, float* slow,
                 float* anchor, int W, int64_t P, int64_t ld, float beta,
-                float alpha, void* stream);
+                float alpha, unsigned flags, void* stream);
 
 // True when a launch over P coordinates (rows = W for the row-parallel local
 // step, 1 otherwise) fits in one grid.

@@ -133,8 +133,11 @@ class CpdpState:
         self.opt_step = 0
 
     def step_opt(self, t: int, grads: torch.Tensor, opt: Optimizer, beta: float = 0.0,
-                 alpha: float = 1.0, T: int = 0, stream=None, method: str = "cpdp") -> str:
-        """One step of ``method`` with a general optimizer (see step())."""
+                 alpha: float = 1.0, T: int = 0, stream=None, method: str = "cpdp",
+                 flags: int = 0) -> str:
+        """One step of ``method`` with a general optimizer (see step()).
+        ``flags`` selects sync-step variants (cpdp.CPDP_SYNC_WRITE_GRAD_MEAN,
+        cpdp.CPDP_SYNC_AVERAGE_OPT_STATE)."""
         self._check_grads(grads)
         if method not in self.METHODS:
             raise ValueError(method)
@@ -144,7 +147,7 @@ class CpdpState:
         if method == "ddp" or cpdp.cpdp_is_sync_step(t, self.K, T):
             cpdp.cpdp_sync_step_opt(method, self.params, self.mom, mom2, grads,
                                     self.slow_mom, self.anchor, self.W, self.P, self.ld,
-                                    self.K, c, beta, alpha, self.param_dt, stream)
+                                    self.K, c, beta, alpha, flags, self.param_dt, stream)
             return "reconcile"
         cpdp.cpdp_local_step_opt(self.params, self.mom, mom2, grads, self.W, self.P,
                                  self.ld, self.K, c, self.param_dt, stream)

@@ -47,6 +47,7 @@ class Case:
     # beta2=0.999, eps=1e-8, weight_decay=0.05); None = plain momentum SGD
     # with lr / mu above
     opt: dict | None = None
+    flags: int = 0            # sync-step variants (general-optimizer path only)
 
     def opt32(self) -> dict:
         f = lambda x: float(np.float32(x))  # noqa: E731
@@ -103,6 +104,7 @@ def run_oracle(c: Case, idx: np.ndarray, on_step):
                                       o["weight_decay"], s)
     oracle.run_opt(th0, grads, c.W, c.K, c.steps, make, h[2], h[3], T=c.T,
                    method=c.method, param_dt=c.param_dt, mom_dt="f32", aux_dt="f32",
+                   flags=c.flags,
                    callback=lambda s, k, st, m2: on_step(
                        s, k, st, m2.copy() if o["kind"] == "adamw" else None))
 
@@ -135,7 +137,7 @@ class GpuRun:
         t = ((step - 1) % c.T) + 1 if c.T > 0 else step
         if self.opt is not None:
             return self.st.step_opt(t, self.grads, self.opt, self.h.beta, self.h.alpha,
-                                    c.T, stream=self.stream, method=c.method)
+                                    c.T, stream=self.stream, method=c.method, flags=c.flags)
         return self.st.step(t, self.grads, self.h, c.T, stream=self.stream,
                             method=c.method)
 

@@ -224,7 +224,8 @@ def sopt(strategy=0, opt=None, **kw):
     a.update(kw)
     return cpdp.cpdp_sync_step_opt(strategy, a["params"], a["mom"], a["mom2"], a["grads"],
                                    a["slow"], a["anchor"], a["W"], a["P"], a["ld"], a["K"],
-                                   opt, a["beta"], a["alpha"], a["pdt"], None, check=False)
+                                   opt, a["beta"], a["alpha"], a.get("flags", 0), a["pdt"],
+                                   None, check=False)
 
 
 BAD_OPTS = [dict(kind=2), dict(lr=0.0), dict(lr=float("nan")), dict(momentum=1.0),
@@ -255,6 +256,8 @@ def test_opt_null_and_pointers():
     assert sopt(7, sgd) == E.CPDP_ERR_INVALID_ARG
     assert sopt(0, sgd, beta=1.0) == E.CPDP_ERR_INVALID_ARG
     assert sopt(0, sgd, pdt=5) == E.CPDP_ERR_DTYPE
+    assert sopt(0, sgd, flags=4) == E.CPDP_ERR_INVALID_ARG
+    assert sopt(0, sgd, flags=3, P=0) == E.CPDP_OK
     # SGD ignores mom2 and DDP ignores slow/anchor: only validated when used
     assert sopt(2, sgd, P=0) == E.CPDP_OK
     assert lopt(sgd, P=0, mom2=None) == E.CPDP_OK

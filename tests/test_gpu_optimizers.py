@@ -49,3 +49,49 @@ def test_r50_sgd_wd_full_size_sampled():
     c = Case(W=w.W, P=w.P, K=w.K, lr=w.lr, mu=w.mu, beta=w.beta, alpha=w.alpha, steps=8,
              ld=w.ld, opt=SGD_WD)
     run_parity(c, sample_indices(w.P, w.boundaries()[1:], n_random=1 << 14, seed=4))
+
+
+AVG = 2  # optimizer-state reconciliation
+WB = 1   # gradient-mean write-back
+
+FLAG_CASES = []
+for method in ("cpdp", "localsgd", "ddp"):
+    for opt in (SGD_WD, ADAMW):
+        FLAG_CASES.append(Case(W=8, P=4_099, K=4, lr=opt["lr"], mu=0.9, beta=0.5, alpha=1.0,
+                               steps=8, method=method, opt=opt, flags=AVG))
+        FLAG_CASES.append(Case(W=6, P=1_001, K=2, lr=opt["lr"], mu=0.9, beta=0.5, alpha=1.0,
+                               steps=6, method=method, opt=opt, flags=AVG | WB,
+                               param_dt="bf16"))
+
+
+@pytest.mark.parametrize(
+    "c", FLAG_CASES, ids=lambda c: f"{c.method}-{c.opt['kind']}-flags{c.flags}-W{c.W}-{c.param_dt}")
+def test_sync_variants_parity(c):
+    """Optimizer-state reconciliation (and write-back) variants, every step."""
+    run_parity(c)
+
+
+@pytest.mark.parametrize("method", ["cpdp", "localsgd", "ddp"])
+def test_gradient_mean_write_back(method):
+    """After a sync step with the write-back flag every gradient row holds the
+    fp32 replica mean (CPDP, DDP); LocalSGD leaves the gradients untouched."""
+    import numpy as np
+    import torch
+
+    import oracle
+    from gpu_harness import GpuRun, oracle_inputs
+    c = Case(W=8, P=20_003, K=1, lr=0.1, mu=0.9, beta=0.5, alpha=1.0, steps=1,
+             method=method, opt=SGD_WD, flags=WB)
+    g = GpuRun(c)
+    g.step(1)
+    torch.cuda.synchronize()
+    got = g.grads[:, :c.P].cpu().numpy().astype(np.float64)
+    th0, grads = oracle_inputs(c, np.arange(c.P))
+    st = oracle.state_init(th0, c.W)
+    o = c.opt32()
+    want = oracle.sync_opt(st, method, grads(1, c.W, c.P),
+                           oracle.sgd(o["lr"], o["momentum"], o["weight_decay"]), 0.5, 1.0,
+                           flags=oracle.SYNC_WRITE_GBAR)
+    assert np.allclose(got, want, rtol=1e-6, atol=1e-9)
+    if method != "localsgd":
+        assert (got == got[0:1]).all()
