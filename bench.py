@@ -197,6 +197,11 @@ def main() -> int:
     rec_ms = sum(dur["reconcile"]) / len(dur["reconcile"])
     loc_ms = sum(dur["local"]) / len(dur["local"]) if dur["local"] else None
 
+    def spread(xs):
+        xs = sorted(xs)
+        return {"median_ms": round(xs[len(xs) // 2], 5), "min_ms": round(xs[0], 5),
+                "max_ms": round(xs[-1], 5), "launches": len(xs)}
+
     # copy ceiling
     for _ in range(3):
         sdev.copy_f32(cdst, csrc, n_copy, stream=stream)
@@ -249,12 +254,12 @@ def main() -> int:
         sync_kernel: {"replica_params_per_s": wp / (rec_ms * 1e-3),
                       "GB_per_s": round(rec_gbps, 1),
                       "frac_of_hbm_peak": round(rec_gbps / HBM_PEAK_GBPS, 4),
-                      "ms": round(rec_ms, 5)},
+                      "ms": round(rec_ms, 5), **spread(dur["reconcile"])},
         "local_step": None if loc_ms is None else {
             "replica_params_per_s": wp / (loc_ms * 1e-3),
             "GB_per_s": round(loc_bytes / (loc_ms * 1e-3) / 1e9, 1),
             "frac_of_hbm_peak": round(loc_bytes / (loc_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
-            "ms": round(loc_ms, 5)},
+            "ms": round(loc_ms, 5), **spread(dur["local"])},
         "roofline": roofline(sync_kernel, rec_bytes, rec_ms),
         "roofline_local_step": None if loc_ms is None else roofline("local_step", loc_bytes, loc_ms),
         "copy_ceiling_GBps": round(copy_gbps, 1),
