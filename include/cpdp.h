@@ -225,6 +225,28 @@ int cpdp_sync_step_opt(int strategy, void* params, void* mom, void* mom2,
  */
 int cpdp_is_sync_step(int64_t t, int K, int64_t T);
 
+/*
+ * Synchronisation period in force during 0-based epoch `epoch`: 1 for the
+ * first warmup_epochs epochs (CPDP and LocalSGD run fully synchronously during
+ * warmup, Sec. 3.4, Sec. 4.3, Sec. 5.3), K afterwards.  Host only.
+ * Returns -CPDP_ERR_INVALID_ARG if epoch < 0, warmup_epochs < 0 or K < 1.
+ */
+int cpdp_period_for_epoch(int64_t epoch, int64_t warmup_epochs, int K);
+
+/*
+ * Learning rate of 0-based step `step` of a run of total_steps steps: linear
+ * warmup, lr = base_lr * (step + 1) / warmup_steps for step < warmup_steps,
+ * then cosine annealing from base_lr to min_lr over the remaining steps,
+ * lr = min_lr + (base_lr - min_lr) * (1 + cos(pi * s / S)) / 2 with
+ * s = step - warmup_steps, S = max(1, total_steps - warmup_steps)
+ * (Sec. 4.3 names cosine annealing with linear warmup; the exact curve is
+ * this build's reading).  Host only.  Returns NaN if step < 0,
+ * step >= total_steps, warmup_steps < 0, warmup_steps > total_steps,
+ * base_lr <= 0, min_lr < 0 or min_lr > base_lr.
+ */
+float cpdp_lr_at(int64_t step, int64_t total_steps, int64_t warmup_steps,
+                 float base_lr, float min_lr);
+
 /* Static, human-readable name of a status code (never NULL). */
 const char* cpdp_status_str(int status);
 

@@ -272,7 +272,31 @@ def is_sync_step(t: int, K: int, T: int = 0) -> bool:
     return t % K == 0 or (T > 0 and t == T)
 
 
-def run(theta0, grad_fn, W: int, K: int, n_steps: int, lr: float, mu: float,
+def period_for_epoch(epoch: int, warmup_epochs: int, K: int) -> int:
+    """Sec. 3.4 / Sec. 4.3 / Sec. 5.3: during the warmup epochs CPDP and
+    LocalSGD synchronise every step (K = 1); afterwards the configured K."""
+    if epoch < 0 or warmup_epochs < 0 or K < 1:
+        raise ValueError("need epoch >= 0, warmup_epochs >= 0, K >= 1")
+    return 1 if epoch < warmup_epochs else K
+
+
+def lr_at(step: int, total_steps: int, warmup_steps: int, base_lr: float,
+          min_lr: float = 0.0) -> float:
+    """Sec. 4.3 cosine annealing with linear warmup (the curve is a reading):
+    base_lr * (step+1)/warmup_steps during warmup, then
+    min_lr + (base_lr - min_lr)(1 + cos(pi s/S))/2, s = step - warmup_steps,
+    S = max(1, total_steps - warmup_steps).  Returned in double."""
+    import math
+    if not (0 <= step < total_steps and 0 <= warmup_steps <= total_steps
+            and base_lr > 0 and 0 <= min_lr <= base_lr):
+        raise ValueError("invalid schedule arguments")
+    if step < warmup_steps:
+        return base_lr * (step + 1) / warmup_steps
+    S = max(1, total_steps - warmup_steps)
+    return min_lr + (base_lr - min_lr) * (1 + math.cos(math.pi * (step - warmup_steps) / S)) / 2
+
+
+def run(theta0, grad_fn, W: int, K: int, n_steps: int, lr, mu: float,
         beta: float, alpha: float, T: int = 0, param_dt="f32", mom_dt="f32",
         aux_dt="f32", callback=None, use=None, method: str = "cpdp") -> OracleState:
     """Algorithm 1 driven for n_steps steps.
@@ -280,7 +304,9 @@ def run(theta0, grad_fn, W: int, K: int, n_steps: int, lr: float, mu: float,
     grad_fn(step, W, P) returns the (W, P) gradients of 1-based global step
     ``step`` (the stand-in for the backward pass).  With T > 0 the within-epoch
     step counter restarts every T steps.  callback(step, kind, state) is called
-    after every step with kind "local" or "reconcile".  ``method`` selects the
+    after every step with kind "local" or "reconcile".  ``lr`` is a number or
+    a function of the 1-based step; ``K`` likewise may be a function of the
+    0-based epoch (the warmup schedule).  ``method`` selects the
     synchronisation step: "cpdp" (Algorithm 1), "localsgd" (parameter
     averaging only) or "ddp" (gradient averaging at every step; K is ignored,
     DDP being the K = 1 schedule).
@@ -290,18 +316,21 @@ def run(theta0, grad_fn, W: int, K: int, n_steps: int, lr: float, mu: float,
     st = state_init(theta0, W, param_dt, mom_dt, aux_dt, use)
     for step in range(1, n_steps + 1):
         t = ((step - 1) % T) + 1 if T > 0 else step
+        epoch = (step - 1) // T if T > 0 else 0
+        k = K(epoch) if callable(K) else K
+        lr_s = lr(step) if callable(lr) else lr
         g = grad_fn(step, W, st.P)
         if method == "ddp":
-            ddp_step(st, g, lr, mu)
+            ddp_step(st, g, lr_s, mu)
             kind = "reconcile"
-        elif is_sync_step(t, K, T):
+        elif is_sync_step(t, k, T):
             if method == "cpdp":
-                reconcile(st, g, lr, mu, beta, alpha)
+                reconcile(st, g, lr_s, mu, beta, alpha)
             else:
-                localsgd_sync(st, g, lr, mu)
+                localsgd_sync(st, g, lr_s, mu)
             kind = "reconcile"
         else:
-            local_step(st, g, lr, mu)
+            local_step(st, g, lr_s, mu)
             kind = "local"
         if callback is not None:
             callback(step, kind, st)

@@ -35,7 +35,7 @@ DTYPES = {"f32": CPDP_F32, "bf16": CPDP_BF16}
 EXPORTS = ("cpdp_state_init", "cpdp_local_step", "cpdp_reconcile",
            "cpdp_localsgd_sync", "cpdp_ddp_step", "cpdp_state_init_opt",
            "cpdp_local_step_opt", "cpdp_sync_step_opt", "cpdp_is_sync_step",
-           "cpdp_status_str")
+           "cpdp_period_for_epoch", "cpdp_lr_at", "cpdp_status_str")
 
 CPDP_OPT_SGD = 0
 CPDP_OPT_ADAMW = 1
@@ -80,6 +80,10 @@ def _load() -> ctypes.CDLL:
     lib.cpdp_sync_step_opt.argtypes = [i, vp, vp, vp, vp, vp, vp, i, i64, i64, i, op,
                                        f, f, ctypes.c_uint, i, vp]
     lib.cpdp_is_sync_step.argtypes = [i64, i, i64]
+    lib.cpdp_period_for_epoch.argtypes = [i64, i64, i]
+    lib.cpdp_period_for_epoch.restype = i
+    lib.cpdp_lr_at.argtypes = [i64, i64, i64, f, f]
+    lib.cpdp_lr_at.restype = f
     lib.cpdp_status_str.argtypes = [i]
     lib.cpdp_status_str.restype = ctypes.c_char_p
     for name in ("cpdp_state_init", "cpdp_local_step", "cpdp_reconcile",
@@ -212,3 +216,21 @@ def cpdp_sync_step_opt(strategy, params, mom, mom2, grads, slow_mom, anchor, W, 
                                int(P), int(ld), int(K), _opt(opt), float(beta),
                                float(alpha), int(flags), _dt(param_dt), _stream(stream))
     return _done(s, "cpdp_sync_step_opt", check)
+
+
+def cpdp_period_for_epoch(epoch: int, warmup_epochs: int, K: int) -> int:
+    r = lib.cpdp_period_for_epoch(int(epoch), int(warmup_epochs), int(K))
+    if r < 0:
+        raise CpdpError(-r, "cpdp_period_for_epoch")
+    return r
+
+
+def cpdp_lr_at(step: int, total_steps: int, warmup_steps: int, base_lr: float,
+               min_lr: float = 0.0) -> float:
+    """Learning rate of 0-based ``step``; raises ValueError on invalid input."""
+    import math
+    r = lib.cpdp_lr_at(int(step), int(total_steps), int(warmup_steps), float(base_lr),
+                       float(min_lr))
+    if math.isnan(r):
+        raise ValueError("cpdp_lr_at: invalid arguments")
+    return r

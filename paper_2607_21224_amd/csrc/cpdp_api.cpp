@@ -5,8 +5,10 @@
 // include/cpdp.h.
 #include "cpdp.h"
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
+#include <limits>
 
 #include "cpdp_launch.h"
 
@@ -318,6 +320,26 @@ int cpdp_sync_step_opt(int strategy, void* params, void* mom, void* mom2, void* 
 int cpdp_is_sync_step(int64_t t, int K, int64_t T) {
     if (t < 1 || K < 1 || T < 0 || (T > 0 && t > T)) return -CPDP_ERR_INVALID_ARG;
     return (t % K == 0 || (T > 0 && t == T)) ? 1 : 0;
+}
+
+int cpdp_period_for_epoch(int64_t epoch, int64_t warmup_epochs, int K) {
+    if (epoch < 0 || warmup_epochs < 0 || K < 1) return -CPDP_ERR_INVALID_ARG;
+    return epoch < warmup_epochs ? 1 : K;
+}
+
+float cpdp_lr_at(int64_t step, int64_t total_steps, int64_t warmup_steps, float base_lr,
+                 float min_lr) {
+    const float nan = std::numeric_limits<float>::quiet_NaN();
+    if (step < 0 || step >= total_steps || warmup_steps < 0 || warmup_steps > total_steps)
+        return nan;
+    if (!(finite(base_lr) && base_lr > 0.0f && finite(min_lr) && min_lr >= 0.0f &&
+          min_lr <= base_lr))
+        return nan;
+    if (step < warmup_steps) return (float)((double)base_lr * (double)(step + 1) / (double)warmup_steps);
+    const double span = (double)std::max<int64_t>(1, total_steps - warmup_steps);
+    const double frac = (double)(step - warmup_steps) / span;
+    const double pi = 3.14159265358979323846;
+    return (float)((double)min_lr + ((double)base_lr - (double)min_lr) * 0.5 * (1.0 + std::cos(pi * frac)));
 }
 
 const char* cpdp_status_str(int status) {

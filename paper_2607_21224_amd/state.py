@@ -175,6 +175,31 @@ class CpdpState:
         self.local_step(grads, h, stream)
         return "local"
 
+    # ---- checkpoint / resume ---------------------------------------------------
+
+    def state_dict(self) -> dict:
+        """Host copy of the whole CPDP state (replicas, optimizer state, SlowMo
+        state, reference model, step counter), enough to resume bitwise."""
+        d = {"W": self.W, "P": self.P, "ld": self.ld, "K": self.K,
+             "param_dt": self.param_dt, "opt_step": self.opt_step,
+             "params": self.params.cpu(), "mom": self.mom.cpu(),
+             "slow_mom": self.slow_mom.cpu(), "anchor": self.anchor.cpu()}
+        if self.mom2 is not None:
+            d["mom2"] = self.mom2.cpu()
+        return d
+
+    @classmethod
+    def from_state_dict(cls, d: dict, device="cuda") -> "CpdpState":
+        st = cls(d["W"], d["P"], d["ld"], d["K"], d["param_dt"], device=device)
+        st.params.copy_(d["params"])
+        st.mom.copy_(d["mom"])
+        st.slow_mom.copy_(d["slow_mom"])
+        st.anchor.copy_(d["anchor"])
+        if "mom2" in d:
+            st.mom2 = d["mom2"].to(device)
+        st.opt_step = int(d["opt_step"])
+        return st
+
     def _check_grads(self, g: torch.Tensor) -> None:
         assert g.dtype == torch.float32 and g.is_contiguous()
         assert g.shape == (self.W, self.ld), (tuple(g.shape), self.W, self.ld)

@@ -271,3 +271,28 @@ def test_state_init_opt_validation():
     assert f(pdt=3) == E.CPDP_ERR_DTYPE
     assert f(theta0=None) == E.CPDP_ERR_NULL
     assert f(mom2=A + 256) == E.CPDP_ERR_OVERLAP
+
+
+def test_period_for_epoch_matches_oracle():
+    for K in (1, 2, 4, 7):
+        for warm in (0, 1, 3):
+            for epoch in range(6):
+                assert cpdp.cpdp_period_for_epoch(epoch, warm, K) == \
+                    oracle.period_for_epoch(epoch, warm, K)
+    for bad in [(-1, 0, 2), (0, -1, 2), (0, 0, 0)]:
+        with pytest.raises(cpdp.CpdpError):
+            cpdp.cpdp_period_for_epoch(*bad)
+
+
+def test_lr_at_matches_oracle():
+    import numpy as np
+    for (total, warm, base, low) in [(100, 10, 0.1, 0.0), (37, 0, 0.4, 0.01), (5, 5, 1e-3, 0.0),
+                                     (1, 0, 0.1, 0.1)]:
+        for s in range(total):
+            got = cpdp.cpdp_lr_at(s, total, warm, base, low)
+            want = oracle.lr_at(s, total, warm, float(np.float32(base)), float(np.float32(low)))
+            assert got == pytest.approx(want, rel=1e-6, abs=1e-12)
+    for bad in [(-1, 10, 0, 0.1, 0.0), (10, 10, 0, 0.1, 0.0), (0, 10, 11, 0.1, 0.0),
+                (0, 10, 0, 0.0, 0.0), (0, 10, 0, 0.1, 0.2), (0, 10, 0, 0.1, -1.0)]:
+        with pytest.raises(ValueError):
+            cpdp.cpdp_lr_at(*bad)

@@ -41,3 +41,28 @@ def test_no_epoch_boundary():
 def test_invalid(bad):
     with pytest.raises(ValueError):
         oracle.is_sync_step(*bad)
+
+
+@pytest.mark.parametrize("K", [2, 3, 4, 8])
+def test_warmup_then_table2_counts(K):
+    # Sec. 3.4: Table 2's counts apply after warmup; during warmup CPDP and
+    # LocalSGD synchronise every step.
+    T, warm = 13, 2
+    for epoch in range(5):
+        k = oracle.period_for_epoch(epoch, warm, K)
+        syncs = sum(oracle.is_sync_step(t, k, T) for t in range(1, T + 1))
+        assert syncs == (T if epoch < warm else math.ceil(T / K))
+
+
+def test_lr_schedule_shape():
+    base, low, total, warm = 0.4, 0.001, 110, 10
+    lrs = [oracle.lr_at(s, total, warm, base, low) for s in range(total)]
+    assert lrs[0] == pytest.approx(base / warm)
+    assert lrs[warm - 1] == pytest.approx(base)
+    assert lrs[warm] == pytest.approx(base)            # cosine starts at base
+    assert lrs[warm + 50] == pytest.approx((base + low) / 2)
+    assert all(a > b for a, b in zip(lrs[warm:], lrs[warm + 1:]))   # decreasing
+    assert all(a < b for a, b in zip(lrs[:warm - 1], lrs[1:warm]))  # increasing
+    assert low < lrs[-1] < low + 1e-3
+    with pytest.raises(ValueError):
+        oracle.lr_at(total, total, warm, base, low)

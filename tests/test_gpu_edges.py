@@ -131,3 +131,30 @@ def test_invalid_call_leaves_state_untouched():
         st.reconcile(g, Hyper(0.1, 0.9, 1.5, 1.0))  # beta >= 1
     torch.cuda.synchronize()
     assert torch.equal(before, st.params)
+
+
+@pytest.mark.parametrize("opt", [None, dict(kind="adamw", lr=5e-4, momentum=0.9,
+                                            beta2=0.999, eps=1e-8, weight_decay=0.05)])
+def test_checkpoint_resume_bitwise(tmp_path, opt):
+    """Two periods, a checkpoint through a file, a fresh state restored from
+    it, three more periods: bitwise equal to five uninterrupted periods."""
+    c = Case(W=8, P=50_021, K=4, lr=0.1 if opt is None else 5e-4, mu=0.9, beta=0.5,
+             alpha=1.0, steps=20, opt=opt)
+    ref = GpuRun(c)
+    for s in range(1, 21):
+        ref.step(s)
+    want = ref.snapshot()
+
+    a = GpuRun(c)
+    for s in range(1, 9):
+        a.step(s)
+    torch.cuda.synchronize()
+    path = tmp_path / "cpdp_state.pt"
+    torch.save(a.st.state_dict(), path)
+    b = GpuRun(c)                       # fresh buffers, re-initialised
+    b.st = CpdpState.from_state_dict(torch.load(path, weights_only=True))
+    for s in range(9, 21):
+        b.step(s)
+    got = b.snapshot()
+    for k in want:
+        assert np.array_equal(got[k], want[k], equal_nan=True), k
