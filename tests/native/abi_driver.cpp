@@ -1,0 +1,76 @@
+// Drives every C-ABI entry point through valid and invalid arguments on the
+// host (fake, never dereferenced device addresses) and checks the returned
+// status and whether a launch was reached.  Built with sanitizers by
+// tests/test_native_sanitizers.py; exits non-zero on the first mismatch.
+#include <cmath>
+#include <cstdint>
+#include <cstdio>
+
+#include "cpdp.h"
+
+extern int g_launches;
+
+static int failures = 0;
+#define EXPECT(call, want_status, want_launch)                                            \
+    do {                                                                                  \
+        int before = g_launches;                                                          \
+        int got = (call);                                                                 \
+        bool launched = g_launches != before;                                             \
+        if (got != (want_status) || launched != (want_launch)) {                          \
+            std::printf("FAIL line %d: status %d (want %d) launched %d (want %d)\n",      \
+                        __LINE__, got, (int)(want_status), (int)launched, (int)(want_launch)); \
+            ++failures;                                                                   \
+        }                                                                                 \
+    } while (0)
+
+int main() {
+    auto at = [](int k) { return reinterpret_cast<void*>((uintptr_t)(1ull << 40) + ((uintptr_t)k << 36)); };
+    void *pa = at(0), *mo = at(1), *gr = at(2), *m2 = at(6), *th = at(5);
+    float *u = static_cast<float*>(at(3)), *an = static_cast<float*>(at(4));
+    const int W = 8;
+    const int64_t P = 1000, ld = 1024;
+
+    EXPECT(cpdp_reconcile(pa, mo, gr, u, an, W, P, ld, 4, 0.1f, 0.9f, 0.5f, 1.0f, 0, 0, 0, nullptr), CPDP_OK, true);
+    EXPECT(cpdp_reconcile(pa, mo, gr, u, an, W, P, ld, 4, 0.1f, 0.9f, 1.0f, 1.0f, 0, 0, 0, nullptr), CPDP_ERR_INVALID_ARG, false);
+    EXPECT(cpdp_reconcile(pa, mo, gr, u, an, W, P, ld, 4, NAN, 0.9f, 0.5f, 1.0f, 0, 0, 0, nullptr), CPDP_ERR_INVALID_ARG, false);
+    EXPECT(cpdp_reconcile(pa, pa, gr, u, an, W, P, ld, 4, 0.1f, 0.9f, 0.5f, 1.0f, 0, 0, 0, nullptr), CPDP_ERR_OVERLAP, false);
+    EXPECT(cpdp_reconcile(nullptr, mo, gr, u, an, W, P, ld, 4, 0.1f, 0.9f, 0.5f, 1.0f, 0, 0, 0, nullptr), CPDP_ERR_NULL, false);
+    EXPECT(cpdp_reconcile(pa, mo, gr, u, an, W, 0, ld, 4, 0.1f, 0.9f, 0.5f, 1.0f, 0, 0, 0, nullptr), CPDP_OK, false);
+    EXPECT(cpdp_reconcile(pa, mo, gr, u, an, W, P, ld, 4, 0.1f, 0.9f, 0.5f, 1.0f, 1, 0, 0, nullptr), CPDP_OK, true);
+    EXPECT(cpdp_reconcile(pa, mo, gr, u, an, W, P, 1004, 4, 0.1f, 0.9f, 0.5f, 1.0f, 1, 0, 0, nullptr), CPDP_ERR_MISALIGNED, false);
+    EXPECT(cpdp_reconcile(pa, mo, gr, u, an, W, (int64_t)1 << 42, (int64_t)1 << 42, 4, 0.1f, 0.9f, 0.5f, 1.0f, 0, 0, 0, nullptr), CPDP_ERR_INVALID_ARG, false);
+    EXPECT(cpdp_reconcile(pa, mo, gr, u, an, 1 << 30, P, (int64_t)1 << 40, 4, 0.1f, 0.9f, 0.5f, 1.0f, 0, 0, 0, nullptr), CPDP_ERR_INVALID_ARG, false);
+    EXPECT(cpdp_local_step(pa, mo, gr, W, P, ld, 4, 0.1f, 0.9f, 0, 0, 0, nullptr), CPDP_OK, true);
+    EXPECT(cpdp_local_step(pa, mo, gr, W, P, ld, 4, 0.1f, 1.0f, 0, 0, 0, nullptr), CPDP_ERR_INVALID_ARG, false);
+    EXPECT(cpdp_state_init(th, pa, mo, u, an, W, P, ld, 4, 0, 0, nullptr), CPDP_OK, true);
+    EXPECT(cpdp_state_init(th, pa, mo, u, an, W, P, ld, 4, 0, 1, nullptr), CPDP_ERR_DTYPE, false);
+    EXPECT(cpdp_localsgd_sync(pa, mo, gr, nullptr, W, P, ld, 4, 0.1f, 0.9f, 0, 0, 0, nullptr), CPDP_OK, true);
+    EXPECT(cpdp_ddp_step(pa, mo, gr, W, P, ld, 0.1f, 0.9f, 0, 0, 0, nullptr), CPDP_OK, true);
+    EXPECT(cpdp_ddp_step(pa, mo, gr, W, P, ld, 0.1f, 0.9f, 0, 1, 0, nullptr), CPDP_ERR_DTYPE, false);
+
+    cpdp_optimizer adam = {CPDP_OPT_ADAMW, 5e-4f, 0.9f, 0.999f, 1e-8f, 0.05f, 1};
+    cpdp_optimizer sgd = {CPDP_OPT_SGD, 0.1f, 0.9f, 0.0f, 0.0f, 5e-4f, 0};
+    EXPECT(cpdp_state_init_opt(th, pa, mo, m2, u, an, W, P, ld, 4, 0, nullptr), CPDP_OK, true);
+    EXPECT(cpdp_local_step_opt(pa, mo, m2, gr, W, P, ld, 4, &adam, 0, nullptr), CPDP_OK, true);
+    EXPECT(cpdp_local_step_opt(pa, mo, nullptr, gr, W, P, ld, 4, &adam, 0, nullptr), CPDP_ERR_NULL, false);
+    EXPECT(cpdp_local_step_opt(pa, mo, nullptr, gr, W, P, ld, 4, &sgd, 0, nullptr), CPDP_OK, true);
+    EXPECT(cpdp_local_step_opt(pa, mo, m2, gr, W, P, ld, 4, nullptr, 0, nullptr), CPDP_ERR_NULL, false);
+    for (int s = 0; s < 3; ++s)
+        for (unsigned f = 0; f < 4; ++f)
+            EXPECT(cpdp_sync_step_opt(s, pa, mo, m2, gr, u, an, W, P, ld, 4, &adam, 0.5f, 1.0f, f, 0, nullptr), CPDP_OK, true);
+    EXPECT(cpdp_sync_step_opt(0, pa, mo, m2, gr, u, an, W, P, ld, 4, &adam, 0.5f, 1.0f, 8u, 0, nullptr), CPDP_ERR_INVALID_ARG, false);
+    EXPECT(cpdp_sync_step_opt(3, pa, mo, m2, gr, u, an, W, P, ld, 4, &adam, 0.5f, 1.0f, 0u, 0, nullptr), CPDP_ERR_INVALID_ARG, false);
+    EXPECT(cpdp_sync_step_opt(2, pa, mo, nullptr, gr, nullptr, nullptr, W, P, ld, 4, &sgd, 0.5f, 1.0f, 0u, 0, nullptr), CPDP_OK, true);
+    adam.step = 0;
+    EXPECT(cpdp_local_step_opt(pa, mo, m2, gr, W, P, ld, 4, &adam, 0, nullptr), CPDP_ERR_INVALID_ARG, false);
+
+    EXPECT(cpdp_is_sync_step(4, 4, 0), 1, false);
+    EXPECT(cpdp_is_sync_step(3, 4, 0), 0, false);
+    EXPECT(cpdp_is_sync_step(0, 4, 0), -CPDP_ERR_INVALID_ARG, false);
+    EXPECT(cpdp_period_for_epoch(0, 2, 4), 1, false);
+    EXPECT(cpdp_period_for_epoch(2, 2, 4), 4, false);
+    if (!std::isnan(cpdp_lr_at(10, 10, 0, 0.1f, 0.0f))) { std::printf("FAIL lr_at range\n"); ++failures; }
+    for (int s = -3; s < 12; ++s) (void)cpdp_status_str(s);
+    std::printf("%s (%d launches)\n", failures ? "FAILED" : "OK", g_launches);
+    return failures ? 1 : 0;
+}

@@ -1,0 +1,23 @@
+// Host-only stand-ins for the gfx950 launchers, so the C-ABI validation layer
+// (cpdp_api.cpp) can be built with g++ under AddressSanitizer/UBSan on a
+// machine without a GPU.  Every launcher records that it was reached.
+#include "cpdp_launch.h"
+
+int g_launches = 0;
+
+namespace cpdp {
+int launch_state_init(Param, const void*, void*, float*, float*, float*, float*, int, int64_t,
+                      int64_t, void*) {
+    return ++g_launches, 0;
+}
+int launch_local_step(Opt, const OptParams&, Param, void*, float*, float*, const float*, int,
+                      int64_t, int64_t, void*) {
+    return ++g_launches, 0;
+}
+int launch_sync(Sync, Opt, const OptParams&, Param, void*, float*, float*, const float*, float*,
+                float*, int, int64_t, int64_t, float, float, unsigned, void*) {
+    return ++g_launches, 0;
+}
+bool grid_fits(int rows, int64_t P) { return rows >= 1 && (P + 1023) / 1024 <= 0x7FFFFFFF / rows; }
+const char* hip_error_string(int) { return "stub"; }
+}  // namespace cpdp
