@@ -102,6 +102,9 @@ def main() -> int:
                     help="per-replica optimizer (Table 3): sgd = momentum SGD of the "
                          "workload; sgd_wd adds weight decay 5e-4; adamw = AdamW "
                          "(lr 5e-4, betas 0.9/0.999, eps 1e-8, weight decay 0.05)")
+    ap.add_argument("--graph", action="store_true",
+                    help="also replay the period as one captured HIP graph and time that "
+                         "(SGD only; removes per-launch host overhead, matters for small P)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=10.0)
     ap.add_argument("--row-align-bytes", type=int, default=0,
@@ -216,6 +219,23 @@ def main() -> int:
     copy_gbps = 2 * 4 * n_copy * reps / (c0.elapsed_time(c1) * 1e-3) / 1e9
 
     adamw = args.optimizer == "adamw"
+    graph_ms = None
+    if args.graph:
+        if opt is not None:
+            raise SystemExit("--graph replays fixed-scalar steps: use --optimizer sgd")
+        graph, _ = st.capture_period(grads, h, method=args.method)
+        for _ in range(args.warmup):
+            graph.replay()
+        torch.cuda.synchronize()
+        g0 = torch.cuda.Event(enable_timing=True)
+        g1 = torch.cuda.Event(enable_timing=True)
+        g0.record()
+        for _ in range(args.steps):
+            graph.replay()
+        g1.record()
+        torch.cuda.synchronize()
+        graph_ms = g0.elapsed_time(g1) / args.steps
+
     rec_bytes = w.sync_bytes(args.method, adamw)
     loc_bytes = w.local_step_bytes(adamw)
     rec_gbps = rec_bytes / (rec_ms * 1e-3) / 1e9
@@ -262,6 +282,9 @@ def main() -> int:
             "ms": round(loc_ms, 5), **spread(dur["local"])},
         "roofline": roofline(sync_kernel, rec_bytes, rec_ms),
         "roofline_local_step": None if loc_ms is None else roofline("local_step", loc_bytes, loc_ms),
+        "graph_replay": None if graph_ms is None else {
+            "ms_per_step": round(graph_ms, 5),
+            "replica_params_per_s": wp * w.K / (graph_ms * 1e-3)},
         "copy_ceiling_GBps": round(copy_gbps, 1),
         "wall_s_timed_region": round(wall, 4),
     }

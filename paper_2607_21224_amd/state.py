@@ -175,6 +175,31 @@ class CpdpState:
         self.local_step(grads, h, stream)
         return "local"
 
+    # ---- HIP graph capture of a period --------------------------------------------
+
+    def capture_period(self, grads: list, h: Hyper, method: str = "cpdp", T: int = 0,
+                       t0: int = 1):
+        """Capture steps t0 .. t0+len(grads)-1 (cadence decided now, from
+        ``self.K``) into a HIP graph; replaying it runs those steps on the
+        gradient buffers ``grads`` (refill them between replays).  For
+        fixed-scalar steps only: the hyperparameters are baked into the graph.
+        Returns (graph, kinds)."""
+        import torch
+        for g in grads:
+            self._check_grads(g)
+        graph = torch.cuda.CUDAGraph()
+        kinds = []
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            torch.cuda.synchronize()
+            with torch.cuda.graph(graph, stream=side):
+                cs = torch.cuda.current_stream()
+                for j, g in enumerate(grads):
+                    kinds.append(self.step(t0 + j, g, h, T, stream=cs, method=method))
+        torch.cuda.current_stream().wait_stream(side)
+        return graph, kinds
+
     # ---- checkpoint / resume ---------------------------------------------------
 
     def state_dict(self) -> dict:
