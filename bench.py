@@ -105,6 +105,10 @@ def main() -> int:
     ap.add_argument("--graph", action="store_true",
                     help="also replay the period as one captured HIP graph and time that "
                          "(SGD only; removes per-launch host overhead, matters for small P)")
+    ap.add_argument("--plan", action="store_true",
+                    help="hold the model as one allocation per (replica, tensor), as a "
+                         "framework does, and drive it through a multi-tensor plan "
+                         "(ResNet-50 / ViT-S tensor lists) instead of the flat buffer")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=10.0)
     ap.add_argument("--row-align-bytes", type=int, default=0,
@@ -132,7 +136,10 @@ def main() -> int:
     torch.cuda.set_device(dev)
     stream = torch.cuda.Stream(device=dev)  # default priority
 
-    st = CpdpState(w.W, w.P, w.ld, w.K, w.param_dt, device=dev)
+    adamw = args.optimizer == "adamw"
+    if args.plan and args.graph:
+        raise SystemExit("--graph captures the flat-buffer path; drop --plan")
+    st = None if args.plan else CpdpState(w.W, w.P, w.ld, w.K, w.param_dt, device=dev)
     h = Hyper.fp32(w.lr, w.mu, w.beta, w.alpha)
     with torch.cuda.stream(stream):
         th = torch.empty(w.P, dtype=torch.float32, device=dev)
@@ -149,7 +156,23 @@ def main() -> int:
             opt = Optimizer("sgd", h.lr, h.mu, weight_decay=5e-4)
         elif args.optimizer == "adamw":
             opt = Optimizer("adamw", 5e-4, 0.9, 0.999, 1e-8, 0.05)
-        if opt is None:
+        multi = None
+        if args.plan:
+            from paper_2607_21224_amd.multi import CpdpMultiState
+            numels = [x for _, x in w.tensors]
+            offs = [0]
+            for x in numels:
+                offs.append(offs[-1] + x)
+            multi = CpdpMultiState(w.W, numels, w.K, w.param_dt, adamw, device=dev)
+            multi.init([th[offs[t]:offs[t + 1]] for t in range(len(numels))], stream=stream)
+            # one gradient set (step 1's) serves every step: the kernels' cost does not
+            # depend on the values, and per-step copies would add traffic to the period
+            for i in range(w.W):
+                for t in range(len(numels)):
+                    multi.grads[i][t][:numels[t]].copy_(grads[0][i, offs[t]:offs[t + 1]])
+            if opt is None:
+                opt = Optimizer("sgd", h.lr, h.mu)
+        elif opt is None:
             st.init(th, stream=stream)
         else:
             st.init_opt(th, opt, stream=stream)
@@ -166,7 +189,9 @@ def main() -> int:
                 e0 = torch.cuda.Event(enable_timing=True)
                 e1 = torch.cuda.Event(enable_timing=True)
                 e0.record(stream)
-            if opt is None:
+            if multi is not None:
+                kind = multi.step(s, opt, h.beta, h.alpha, 0, stream, method=args.method)
+            elif opt is None:
                 kind = st.step(s, grads[s - 1], h, 0, stream, method=args.method)
             else:
                 kind = st.step_opt(s, grads[s - 1], opt, h.beta, h.alpha, 0, stream,
@@ -218,7 +243,6 @@ def main() -> int:
     torch.cuda.synchronize()
     copy_gbps = 2 * 4 * n_copy * reps / (c0.elapsed_time(c1) * 1e-3) / 1e9
 
-    adamw = args.optimizer == "adamw"
     graph_ms = None
     if args.graph:
         if opt is not None:
@@ -243,6 +267,8 @@ def main() -> int:
 
     variant = "" if (args.method, args.optimizer) == ("cpdp", "sgd") else \
         f"_{args.method}_{args.optimizer}"
+    if args.plan:
+        variant += "_plan"
 
     def roofline(kernel, nbytes, ms):
         ach = nbytes / (ms * 1e-3) / 1e9
@@ -266,6 +292,9 @@ def main() -> int:
                                f"K={w.K}, lr={w.lr}, mu={w.mu}, beta={w.beta}, alpha={w.alpha}",
                    "W": w.W, "P": w.P, "ld": w.ld, "K": w.K,
                    "method": args.method, "optimizer": args.optimizer,
+                   "layout": (f"multi-tensor plan: {len(w.tensors)} tensors x {w.W} replicas, "
+                              "one allocation each; step 1's gradients every step"
+                              if args.plan else "flat buffer, one row per replica"),
                    "step": (f"{w.K} DDP steps (K=1 schedule), same gradients as a CPDP period"
                             if args.method == "ddp" else
                             f"one period: {w.K - 1} local steps + 1 {sync_kernel}")},

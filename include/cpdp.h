@@ -215,6 +215,73 @@ int cpdp_sync_step_opt(int strategy, void* params, void* mom, void* mom2,
                        const cpdp_optimizer* opt, float beta, float alpha,
                        unsigned flags, int param_dt, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Multi-tensor plans.  A framework holds a model as separate parameter
+ * tensors (ResNet-50: 161, ViT-S blocks + head: 146), and the paper's
+ * implementation updates them tensor by tensor (Sec. 4.2).  A plan describes
+ * n_tensors tensors per replica, each family's tensors anywhere in device
+ * memory, so one launch per step covers all of them with the same arithmetic
+ * as the flat entry points (coordinates are independent, so the result of a
+ * tensor equals that of the same values in a flat buffer).
+ *
+ * The table lives in device memory the caller allocates (cpdp_plan_bytes
+ * bytes, 8-byte aligned) and keeps alive while the plan is used;
+ * cpdp_plan_build fills it once with a synchronous copy.  The cpdp_plan
+ * struct is the host handle the step calls take.
+ * ------------------------------------------------------------------------ */
+typedef struct cpdp_plan {
+    void* table;          /* device memory, >= cpdp_plan_bytes(W, n_tensors)  */
+    int W;                /* replicas                                           */
+    int n_tensors;
+    int param_dt;         /* storage type of every parameter tensor             */
+    int has_mom2;         /* second-moment tensors given (AdamW)                */
+    int has_slow_mom;     /* SlowMo state tensors given (CPDP)                  */
+    int has_anchor;       /* reference-model tensors given (CPDP, LocalSGD)     */
+    int64_t total_chunks; /* filled by cpdp_plan_build                          */
+    int64_t total_numel;  /* filled by cpdp_plan_build: sum of numel            */
+} cpdp_plan;
+
+/* Device bytes of a plan table for W replicas of n_tensors tensors. */
+int64_t cpdp_plan_bytes(int W, int n_tensors);
+
+/*
+ * Fill plan->table (and plan's total_* fields) from host arrays:
+ *   numel[n]                     elements of tensor t (>= 0)
+ *   params, mom, grads [W*n]     device pointer of replica i, tensor t at
+ *                                [i*n + t]; params in param_dt, the rest fp32
+ *   mom2 [W*n] or NULL           AdamW second moments (fp32)
+ *   slow_mom, anchor [n] or NULL SlowMo state and reference model (fp32)
+ * Every pointer of a non-empty tensor must be non-NULL and 16-byte aligned,
+ * and no two of the described ranges may overlap (CPDP_ERR_NULL,
+ * CPDP_ERR_MISALIGNED, CPDP_ERR_OVERLAP).  W, n_tensors >= 1 and plan_bytes
+ * >= cpdp_plan_bytes, else CPDP_ERR_INVALID_ARG.  The copy is synchronous.
+ */
+int cpdp_plan_build(cpdp_plan* plan, int64_t plan_bytes, int W, int n_tensors,
+                    const int64_t* numel, void* const* params,
+                    void* const* mom, void* const* mom2, void* const* grads,
+                    float* const* slow_mom, float* const* anchor,
+                    int param_dt);
+
+/*
+ * Initialisation of Algorithm 1 over a plan: the reference model (the plan's
+ * anchor tensors, fp32, filled by the caller with the initial parameters) is
+ * copied into every replica (rounded to param_dt), the momentum, second-
+ * moment (if any) and SlowMo (if any) tensors are zeroed.  Needs anchor.
+ */
+int cpdp_state_init_plan(const cpdp_plan* plan, void* stream);
+
+/* cpdp_local_step_opt over every tensor of a plan (one launch). */
+int cpdp_local_step_plan(const cpdp_plan* plan, int K,
+                         const cpdp_optimizer* opt, void* stream);
+
+/*
+ * cpdp_sync_step_opt over every tensor of a plan (one launch).  CPDP needs
+ * a plan with slow_mom and anchor; AdamW needs mom2 (else CPDP_ERR_NULL).
+ */
+int cpdp_sync_step_plan(int strategy, const cpdp_plan* plan, int K,
+                        const cpdp_optimizer* opt, float beta, float alpha,
+                        unsigned flags, void* stream);
+
 /*
  * Synchronisation indicator (Sec. 3.2) with the forced synchronisation at the
  * end of an epoch (Sec. 3.1, Sec. 4.2).  Host only, no GPU work.

@@ -35,7 +35,9 @@ DTYPES = {"f32": CPDP_F32, "bf16": CPDP_BF16}
 EXPORTS = ("cpdp_state_init", "cpdp_local_step", "cpdp_reconcile",
            "cpdp_localsgd_sync", "cpdp_ddp_step", "cpdp_state_init_opt",
            "cpdp_local_step_opt", "cpdp_sync_step_opt", "cpdp_is_sync_step",
-           "cpdp_period_for_epoch", "cpdp_lr_at", "cpdp_status_str")
+           "cpdp_period_for_epoch", "cpdp_lr_at", "cpdp_plan_bytes", "cpdp_plan_build",
+           "cpdp_state_init_plan", "cpdp_local_step_plan", "cpdp_sync_step_plan",
+           "cpdp_status_str")
 
 CPDP_OPT_SGD = 0
 CPDP_OPT_ADAMW = 1
@@ -46,6 +48,14 @@ SYNC_KINDS = {"cpdp": CPDP_SYNC_CPDP, "localsgd": CPDP_SYNC_LOCALSGD,
               "ddp": CPDP_SYNC_DDP}
 CPDP_SYNC_WRITE_GRAD_MEAN = 1
 CPDP_SYNC_AVERAGE_OPT_STATE = 2
+
+
+class cpdp_plan(ctypes.Structure):
+    """Mirror of the C struct cpdp_plan (include/cpdp.h)."""
+    _fields_ = [("table", ctypes.c_void_p), ("W", ctypes.c_int), ("n_tensors", ctypes.c_int),
+                ("param_dt", ctypes.c_int), ("has_mom2", ctypes.c_int),
+                ("has_slow_mom", ctypes.c_int), ("has_anchor", ctypes.c_int),
+                ("total_chunks", ctypes.c_int64), ("total_numel", ctypes.c_int64)]
 
 
 class cpdp_optimizer(ctypes.Structure):
@@ -79,6 +89,19 @@ def _load() -> ctypes.CDLL:
     lib.cpdp_local_step_opt.argtypes = [vp, vp, vp, vp, i, i64, i64, i, op, i, vp]
     lib.cpdp_sync_step_opt.argtypes = [i, vp, vp, vp, vp, vp, vp, i, i64, i64, i, op,
                                        f, f, ctypes.c_uint, i, vp]
+    pp = ctypes.POINTER(cpdp_plan)
+    lib.cpdp_plan_bytes.argtypes = [i, i]
+    lib.cpdp_plan_bytes.restype = i64
+    lib.cpdp_plan_build.argtypes = [pp, i64, i, i, ctypes.POINTER(i64), ctypes.POINTER(vp),
+                                    ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp),
+                                    ctypes.POINTER(vp), ctypes.POINTER(vp), i]
+    lib.cpdp_plan_build.restype = i
+    lib.cpdp_state_init_plan.argtypes = [pp, vp]
+    lib.cpdp_state_init_plan.restype = i
+    lib.cpdp_local_step_plan.argtypes = [pp, i, op, vp]
+    lib.cpdp_local_step_plan.restype = i
+    lib.cpdp_sync_step_plan.argtypes = [i, pp, i, op, f, f, ctypes.c_uint, vp]
+    lib.cpdp_sync_step_plan.restype = i
     lib.cpdp_is_sync_step.argtypes = [i64, i, i64]
     lib.cpdp_period_for_epoch.argtypes = [i64, i64, i]
     lib.cpdp_period_for_epoch.restype = i
@@ -234,3 +257,51 @@ def cpdp_lr_at(step: int, total_steps: int, warmup_steps: int, base_lr: float,
     if math.isnan(r):
         raise ValueError("cpdp_lr_at: invalid arguments")
     return r
+
+
+def cpdp_plan_bytes(W: int, n_tensors: int) -> int:
+    return int(lib.cpdp_plan_bytes(int(W), int(n_tensors)))
+
+
+def _ptr_array(xs):
+    if xs is None:
+        return None
+    arr = (ctypes.c_void_p * len(xs))(*[_addr(x) for x in xs])
+    return ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p)), arr
+
+
+def cpdp_plan_build(plan: cpdp_plan, plan_bytes, W, n_tensors, numel, params, mom, mom2,
+                    grads, slow_mom, anchor, param_dt=CPDP_F32, check=True):
+    """numel: n ints; params/mom/grads/mom2: W*n tensors or addresses,
+    replica-major ([i*n + t]); slow_mom/anchor: n tensors or None."""
+    keep = []
+
+    def arr(xs):
+        r = _ptr_array(xs)
+        if r is None:
+            return None
+        keep.append(r[1])
+        return r[0]
+    nm = (ctypes.c_int64 * len(numel))(*[int(x) for x in numel])
+    s = lib.cpdp_plan_build(ctypes.byref(plan), int(plan_bytes), int(W), int(n_tensors), nm,
+                            arr(params), arr(mom), arr(mom2), arr(grads), arr(slow_mom),
+                            arr(anchor), _dt(param_dt))
+    return _done(s, "cpdp_plan_build", check)
+
+
+def cpdp_state_init_plan(plan: cpdp_plan, stream=None, check=True):
+    return _done(lib.cpdp_state_init_plan(ctypes.byref(plan), _stream(stream)),
+                 "cpdp_state_init_plan", check)
+
+
+def cpdp_local_step_plan(plan: cpdp_plan, K, opt, stream=None, check=True):
+    s = lib.cpdp_local_step_plan(ctypes.byref(plan), int(K), _opt(opt), _stream(stream))
+    return _done(s, "cpdp_local_step_plan", check)
+
+
+def cpdp_sync_step_plan(strategy, plan: cpdp_plan, K, opt, beta=0.0, alpha=1.0, flags=0,
+                        stream=None, check=True):
+    strategy = SYNC_KINDS[strategy] if isinstance(strategy, str) else int(strategy)
+    s = lib.cpdp_sync_step_plan(int(strategy), ctypes.byref(plan), int(K), _opt(opt),
+                                float(beta), float(alpha), int(flags), _stream(stream))
+    return _done(s, "cpdp_sync_step_plan", check)

@@ -9,6 +9,8 @@
 #include <cmath>
 #include <cstdint>
 #include <limits>
+#include <utility>
+#include <vector>
 
 #include "cpdp_launch.h"
 
@@ -315,6 +317,152 @@ int cpdp_sync_step_opt(int strategy, void* params, void* mom, void* mom2, void* 
                                         static_cast<float*>(mom), static_cast<float*>(m2),
                                         static_cast<const float*>(grads), slow, anc, W, P, ld,
                                         beta, alpha, flags, stream));
+}
+
+int64_t cpdp_plan_bytes(int W, int n_tensors) {
+    if (W < 1 || n_tensors < 1) return 0;
+    return cpdp::plan_words(W, n_tensors) * (int64_t)sizeof(int64_t);
+}
+
+int cpdp_plan_build(cpdp_plan* plan, int64_t plan_bytes, int W, int n, const int64_t* numel,
+                    void* const* params, void* const* mom, void* const* mom2,
+                    void* const* grads, float* const* slow_mom, float* const* anchor,
+                    int param_dt) {
+    if (plan == nullptr || numel == nullptr || params == nullptr || mom == nullptr ||
+        grads == nullptr)
+        return CPDP_ERR_NULL;
+    if (W < 1 || n < 1 || W > 4096 || n > (1 << 24)) return CPDP_ERR_INVALID_ARG;
+    if (!is_dtype(param_dt)) return CPDP_ERR_DTYPE;
+    if (plan->table == nullptr) return CPDP_ERR_NULL;
+    if ((reinterpret_cast<uintptr_t>(plan->table) & 7u) != 0) return CPDP_ERR_MISALIGNED;
+    const int64_t words = cpdp::plan_words(W, n);
+    if (plan_bytes < words * (int64_t)sizeof(int64_t)) return CPDP_ERR_INVALID_ARG;
+
+    const int64_t per_block = cpdp::coords_per_block();
+    const size_t sp = esize(param_dt);
+    std::vector<int64_t> tab((size_t)words, 0);
+    int64_t* start = tab.data() + cpdp::kPlanHeaderWords;
+    int64_t* cnt = start + (n + 1);
+    int64_t* tp = cnt + n;
+    int64_t* tm = tp + (int64_t)W * n;
+    int64_t* tv = tm + (int64_t)W * n;
+    int64_t* tg = tv + (int64_t)W * n;
+    int64_t* ts = tg + (int64_t)W * n;
+    int64_t* ta = ts + n;
+    std::vector<std::pair<uintptr_t, uintptr_t>> ranges;
+    auto add = [&](const void* p, int64_t elems, size_t es) -> int {
+        if (p == nullptr) return CPDP_ERR_NULL;
+        if (!aligned16(p)) return CPDP_ERR_MISALIGNED;
+        const uintptr_t lo = reinterpret_cast<uintptr_t>(p);
+        ranges.emplace_back(lo, lo + (uintptr_t)(elems * (int64_t)es));
+        return CPDP_OK;
+    };
+    int64_t chunks = 0, total = 0;
+    for (int t = 0; t < n; ++t) {
+        const int64_t P = numel[t];
+        if (P < 0 || P > kMaxElems) return CPDP_ERR_INVALID_ARG;
+        start[t] = chunks;
+        cnt[t] = P;
+        chunks += (P + per_block - 1) / per_block;
+        total += P;
+        for (int i = 0; i < W; ++i) {
+            const int64_t k = (int64_t)i * n + t;
+            tp[k] = (int64_t)reinterpret_cast<uintptr_t>(params[k]);
+            tm[k] = (int64_t)reinterpret_cast<uintptr_t>(mom[k]);
+            tg[k] = (int64_t)reinterpret_cast<uintptr_t>(grads[k]);
+            if (mom2 != nullptr) tv[k] = (int64_t)reinterpret_cast<uintptr_t>(mom2[k]);
+            if (P == 0) continue;
+            if (int s = add(params[k], P, sp)) return s;
+            if (int s = add(mom[k], P, 4)) return s;
+            if (int s = add(grads[k], P, 4)) return s;
+            if (mom2 != nullptr)
+                if (int s = add(mom2[k], P, 4)) return s;
+        }
+        if (slow_mom != nullptr) ts[t] = (int64_t)reinterpret_cast<uintptr_t>(slow_mom[t]);
+        if (anchor != nullptr) ta[t] = (int64_t)reinterpret_cast<uintptr_t>(anchor[t]);
+        if (P == 0) continue;
+        if (slow_mom != nullptr)
+            if (int s = add(slow_mom[t], P, 4)) return s;
+        if (anchor != nullptr)
+            if (int s = add(anchor[t], P, 4)) return s;
+    }
+    start[n] = chunks;
+    if (chunks > (int64_t)0x7FFFFFFF / W) return CPDP_ERR_INVALID_ARG;
+    std::sort(ranges.begin(), ranges.end());
+    for (size_t k = 1; k < ranges.size(); ++k)
+        if (ranges[k].first < ranges[k - 1].second) return CPDP_ERR_OVERLAP;
+    tab[0] = W;
+    tab[1] = n;
+    tab[2] = chunks;
+    if (cpdp::upload_plan(plan->table, tab.data(), words) != 0) return CPDP_ERR_HIP;
+    plan->W = W;
+    plan->n_tensors = n;
+    plan->param_dt = param_dt;
+    plan->has_mom2 = mom2 != nullptr;
+    plan->has_slow_mom = slow_mom != nullptr;
+    plan->has_anchor = anchor != nullptr;
+    plan->total_chunks = chunks;
+    plan->total_numel = total;
+    return CPDP_OK;
+}
+
+static int check_plan(const cpdp_plan* plan) {
+    if (plan == nullptr || plan->table == nullptr) return CPDP_ERR_NULL;
+    if (plan->W < 1 || plan->n_tensors < 1 || plan->total_chunks < 0) return CPDP_ERR_INVALID_ARG;
+    if (!is_dtype(plan->param_dt)) return CPDP_ERR_DTYPE;
+    return CPDP_OK;
+}
+
+int cpdp_state_init_plan(const cpdp_plan* plan, void* stream) {
+    if (int s = check_plan(plan)) return s;
+    if (!plan->has_anchor) return CPDP_ERR_NULL;
+    if (plan->total_chunks == 0) return CPDP_OK;
+    return hip_status(cpdp::launch_state_init_plan(param_kind(plan->param_dt),
+                                                   static_cast<const int64_t*>(plan->table),
+                                                   plan->W, plan->n_tensors, plan->total_chunks,
+                                                   stream));
+}
+
+int cpdp_local_step_plan(const cpdp_plan* plan, int K, const cpdp_optimizer* opt, void* stream) {
+    if (int s = check_plan(plan)) return s;
+    if (K < 1) return CPDP_ERR_INVALID_ARG;
+    cpdp::Opt kind;
+    cpdp::OptParams o;
+    if (int s = make_opt(opt, &kind, &o)) return s;
+    if (kind == cpdp::Opt::ADAMW && !plan->has_mom2) return CPDP_ERR_NULL;
+    if (plan->total_chunks == 0) return CPDP_OK;
+    return hip_status(cpdp::launch_local_step_plan(kind, o, param_kind(plan->param_dt),
+                                                   static_cast<const int64_t*>(plan->table),
+                                                   plan->W, plan->n_tensors, plan->total_chunks,
+                                                   stream));
+}
+
+int cpdp_sync_step_plan(int strategy, const cpdp_plan* plan, int K, const cpdp_optimizer* opt,
+                        float beta, float alpha, unsigned flags, void* stream) {
+    if (int s = check_plan(plan)) return s;
+    if (K < 1) return CPDP_ERR_INVALID_ARG;
+    if (strategy != CPDP_SYNC_CPDP && strategy != CPDP_SYNC_LOCALSGD &&
+        strategy != CPDP_SYNC_DDP)
+        return CPDP_ERR_INVALID_ARG;
+    if (flags & ~(unsigned)(CPDP_SYNC_WRITE_GRAD_MEAN | CPDP_SYNC_AVERAGE_OPT_STATE))
+        return CPDP_ERR_INVALID_ARG;
+    cpdp::Opt kind;
+    cpdp::OptParams o;
+    if (int s = make_opt(opt, &kind, &o)) return s;
+    if (strategy == CPDP_SYNC_CPDP) {
+        if (!(beta >= 0.0f && beta < 1.0f)) return CPDP_ERR_INVALID_ARG;
+        if (!(finite(alpha) && alpha > 0.0f)) return CPDP_ERR_INVALID_ARG;
+        if (!plan->has_slow_mom || !plan->has_anchor) return CPDP_ERR_NULL;
+    }
+    if (kind == cpdp::Opt::ADAMW && !plan->has_mom2) return CPDP_ERR_NULL;
+    if (plan->total_chunks == 0) return CPDP_OK;
+    const cpdp::Sync mode = strategy == CPDP_SYNC_CPDP       ? cpdp::Sync::CPDP
+                            : strategy == CPDP_SYNC_LOCALSGD ? cpdp::Sync::LocalSGD
+                                                             : cpdp::Sync::DDP;
+    return hip_status(cpdp::launch_sync_plan(mode, kind, o, param_kind(plan->param_dt),
+                                             static_cast<const int64_t*>(plan->table), plan->W,
+                                             plan->n_tensors, plan->total_chunks, beta, alpha,
+                                             flags, stream));
 }
 
 int cpdp_is_sync_step(int64_t t, int K, int64_t T) {

@@ -204,22 +204,142 @@ __device__ __forceinline__ float opt_update(const OptParams& o, float th, float&
     }
 }
 
+// ---- replica addressing ------------------------------------------------------------
+//
+// Where replica i's row of each family starts.  Strided is the flat layout of
+// the C ABI (base + i*ld); Table is a multi-tensor plan (one device pointer
+// per replica and tensor, replica-major).  Both expose the same accessors, so
+// the step code below is written once.
+
+template <class PS>
+struct Strided {
+    typename PS::T* params;
+    float* mom;
+    float* mom2;
+    float* grads;
+    int64_t ld;
+    __device__ __forceinline__ typename PS::T* prm(int i) const { return params + (int64_t)i * ld; }
+    __device__ __forceinline__ float* m(int i) const { return mom + (int64_t)i * ld; }
+    __device__ __forceinline__ float* v(int i) const { return mom2 + (int64_t)i * ld; }
+    __device__ __forceinline__ float* g(int i) const { return grads + (int64_t)i * ld; }
+};
+
+template <class PS>
+struct Table {
+    const int64_t* params;  // 64-bit device addresses, entry i*n + t
+    const int64_t* mom;
+    const int64_t* mom2;
+    const int64_t* grads;
+    int64_t n, t;
+    __device__ __forceinline__ typename PS::T* prm(int i) const {
+        return reinterpret_cast<typename PS::T*>(params[i * n + t]);
+    }
+    __device__ __forceinline__ float* m(int i) const { return reinterpret_cast<float*>(mom[i * n + t]); }
+    __device__ __forceinline__ float* v(int i) const { return reinterpret_cast<float*>(mom2[i * n + t]); }
+    __device__ __forceinline__ float* g(int i) const { return reinterpret_cast<float*>(grads[i * n + t]); }
+};
+
+// The sections of a plan table (layout documented in cpdp_launch.h).
+struct PlanView {
+    const int64_t* chunk_start;
+    const int64_t* numel;
+    const int64_t* params;
+    const int64_t* mom;
+    const int64_t* mom2;
+    const int64_t* grads;
+    const int64_t* slow;
+    const int64_t* anchor;
+};
+
+__device__ __forceinline__ PlanView plan_view(const int64_t* plan, int64_t W, int64_t n) {
+    PlanView v;
+    v.chunk_start = plan + kPlanHeaderWords;
+    v.numel = v.chunk_start + (n + 1);
+    v.params = v.numel + n;
+    v.mom = v.params + W * n;
+    v.mom2 = v.mom + W * n;
+    v.grads = v.mom2 + W * n;
+    v.slow = v.grads + W * n;
+    v.anchor = v.slow + n;
+    return v;
+}
+
+// tensor holding chunk b: the largest t < n with chunk_start[t] <= b (an
+// empty tensor never qualifies as the last such t, since b < chunk_start[n])
+__device__ __forceinline__ int64_t plan_tensor(const PlanView& v, int64_t n, int64_t b) {
+    int64_t lo = 0, hi = n;
+    while (hi - lo > 1) {
+        const int64_t mid = (lo + hi) >> 1;
+        if (v.chunk_start[mid] <= b) lo = mid;
+        else hi = mid;
+    }
+    return lo;
+}
+
+// ---- plan initialisation: every replica <- the reference model ----------------
+
+template <class PS, bool FULL>
+__device__ __forceinline__ void init_plan_chunk(const float* anchor, typename PS::T* params,
+                                                float* mom, float* mom2, float* slow, int n) {
+    float a[kVec];
+    const float zero[kVec] = {0.0f, 0.0f, 0.0f, 0.0f};
+    load_f32<FULL, false>(anchor, n, a);
+    PS::template store<FULL, kNTS>(params, n, a);
+    store_f32<FULL, kNTS>(mom, n, zero);
+    if (mom2 != nullptr) store_f32<FULL, kNTS>(mom2, n, zero);
+    if (slow != nullptr) store_f32<FULL, kNTS>(slow, n, zero);
+}
+
+template <class PS>
+__global__ __launch_bounds__(kBlock) void state_init_plan_kernel(const int64_t* __restrict__ plan,
+                                                                 int W, int n,
+                                                                 int64_t total_chunks) {
+    const PlanView v = plan_view(plan, W, n);
+    const int64_t row = blockIdx.x / total_chunks;
+    const int64_t b = blockIdx.x - row * total_chunks;
+    const int64_t t = plan_tensor(v, n, b);
+    const int64_t P = v.numel[t];
+    const int64_t p0 = ((b - v.chunk_start[t]) * kBlock + threadIdx.x) * kVec;
+    if (p0 >= P) return;
+    const int64_t k = row * n + t;
+    auto at = [&](int64_t addr) { return reinterpret_cast<float*>(addr) + p0; };
+    const float* anchor = at(v.anchor[t]);
+    auto* params = reinterpret_cast<typename PS::T*>(v.params[k]) + p0;
+    float* mom2 = v.mom2[k] != 0 ? at(v.mom2[k]) : nullptr;
+    float* slow = row == 0 && v.slow[t] != 0 ? at(v.slow[t]) : nullptr;
+    if (p0 + kVec <= P)
+        init_plan_chunk<PS, true>(anchor, params, at(v.mom[k]), mom2, slow, kVec);
+    else
+        init_plan_chunk<PS, false>(anchor, params, at(v.mom[k]), mom2, slow, (int)(P - p0));
+}
+
 // ---- local step: one replica row per block, 4 coordinates per thread -------
 
 template <Opt O, class PS, bool FULL>
 __device__ __forceinline__ void local_chunk(const OptParams& o, typename PS::T* params,
                                             float* mom, float* mom2, const float* grads,
-                                            int64_t off, int n) {
+                                            int n) {
     float g[kVec], m[kVec], v[kVec] = {0.0f, 0.0f, 0.0f, 0.0f}, th[kVec];
-    load_f32<FULL, kNTL>(grads + off, n, g);
-    load_f32<FULL, kNTL>(mom + off, n, m);
-    if constexpr (O == Opt::ADAMW) load_f32<FULL, kNTL>(mom2 + off, n, v);
-    PS::template load<FULL, kNTL>(params + off, n, th);
+    load_f32<FULL, kNTL>(grads, n, g);
+    load_f32<FULL, kNTL>(mom, n, m);
+    if constexpr (O == Opt::ADAMW) load_f32<FULL, kNTL>(mom2, n, v);
+    PS::template load<FULL, kNTL>(params, n, th);
 #pragma unroll
     for (int k = 0; k < kVec; ++k) th[k] = opt_update<O, PS>(o, th[k], m[k], v[k], g[k]);
-    store_f32<FULL, kNTS>(mom + off, n, m);
-    if constexpr (O == Opt::ADAMW) store_f32<FULL, kNTS>(mom2 + off, n, v);
-    PS::template store<FULL, kNTS>(params + off, n, th);
+    store_f32<FULL, kNTS>(mom, n, m);
+    if constexpr (O == Opt::ADAMW) store_f32<FULL, kNTS>(mom2, n, v);
+    PS::template store<FULL, kNTS>(params, n, th);
+}
+
+template <Opt O, class PS>
+__device__ __forceinline__ void local_dispatch(const OptParams& o, typename PS::T* params,
+                                               float* mom, float* mom2, const float* grads,
+                                               int64_t p0, int64_t P) {
+    if (p0 + kVec <= P)
+        local_chunk<O, PS, true>(o, params + p0, mom + p0, mom2 + p0, grads + p0, kVec);
+    else
+        local_chunk<O, PS, false>(o, params + p0, mom + p0, mom2 + p0, grads + p0,
+                                  (int)(P - p0));
 }
 
 template <Opt O, class PS>
@@ -231,21 +351,37 @@ __global__ __launch_bounds__(kBlock) void local_step_kernel(
     const int64_t col = blockIdx.x - row * blocks_per_row;
     const int64_t p0 = (col * kBlock + threadIdx.x) * kVec;
     if (p0 >= P) return;
-    const int64_t off = row * ld + p0;
-    if (p0 + kVec <= P)
-        local_chunk<O, PS, true>(o, params, mom, mom2, grads, off, kVec);
-    else
-        local_chunk<O, PS, false>(o, params, mom, mom2, grads, off, (int)(P - p0));
+    const int64_t off = row * ld;
+    local_dispatch<O, PS>(o, params + off, mom + off, mom2 + off, grads + off, p0, P);
+}
+
+// multi-tensor plan: block (row, chunk b) -> replica row, tensor t, its chunk
+template <Opt O, class PS>
+__global__ __launch_bounds__(kBlock) void local_step_plan_kernel(OptParams o,
+                                                                 const int64_t* __restrict__ plan,
+                                                                 int W, int n,
+                                                                 int64_t total_chunks) {
+    const PlanView v = plan_view(plan, W, n);
+    const int64_t row = blockIdx.x / total_chunks;
+    const int64_t b = blockIdx.x - row * total_chunks;
+    const int64_t t = plan_tensor(v, n, b);
+    const int64_t P = v.numel[t];
+    const int64_t p0 = ((b - v.chunk_start[t]) * kBlock + threadIdx.x) * kVec;
+    if (p0 >= P) return;
+    const Table<PS> r{v.params, v.mom, v.mom2, v.grads, n, t};
+    const int i = (int)row;
+    local_dispatch<O, PS>(o, r.prm(i), r.m(i), O == Opt::ADAMW ? r.v(i) : nullptr, r.g(i), p0, P);
 }
 
 // ---- fused synchronisation steps ----------------------------------------------
 //
 // One thread owns 4 coordinates across all W replicas.  WT > 0 fixes W at
-// compile time (fully unrolled); WT == 0 takes W at run time.  Replicas are
-// visited in batches of kChunk: all loads of a batch are issued before any of
-// its stores.  The batching matters because the compiler cannot prove that
-// mom + i*ld and mom + j*ld never alias (ld is a run-time value), so a store
-// for replica i would otherwise hold back the loads of replica i+1.
+// compile time (fully unrolled); WT == 0 takes W at run time (batches of
+// kChunk, then single replicas).  Within a batch all loads are issued before
+// any store.  The batching matters because the compiler cannot prove that two
+// replica rows never alias (ld is a run-time value, plan pointers are data),
+// so a store for replica i would otherwise hold back the loads of replica
+// i+1 and the thread would wait one round trip to HBM per replica.
 //
 // Sync::CPDP      gradient mean, synchronized optimizer step, parameter mean,
 //                 SlowMo, copy-back (the reconcile).
@@ -253,119 +389,142 @@ __global__ __launch_bounds__(kBlock) void local_step_kernel(
 //                 mean is copied back (no gradient mean, no SlowMo).
 // Sync::DDP       gradient mean and the same optimizer step on every replica,
 //                 no parameter mean.
+//
+// EXTRA = true enables the optional variants selected by `flags` (run-time W
+// only): kSyncWriteGbar stores the gradient mean into every gradient row;
+// kSyncAverageState replaces every replica's optimizer state by the replica
+// mean after the step.
 
 #ifndef CPDP_RECON_CHUNK
 #define CPDP_RECON_CHUNK 8
 #endif
 constexpr int kChunk = CPDP_RECON_CHUNK;
 
-// EXTRA = true enables the optional variants selected by `flags` (run-time W
-// only): kSyncWriteGbar stores the gradient mean into every gradient row;
-// kSyncAverageState replaces every replica's optimizer state by the replica
-// mean after the step.
-template <Sync M, Opt O, int WT, class PS, bool FULL, bool EXTRA>
-__device__ __forceinline__ void sync_chunk(const OptParams& o, typename PS::T* params,
-                                           float* mom, float* mom2, const float* grads,
-                                           float* slow, float* anchor, int W, int64_t ld,
-                                           int64_t p0, int n, float beta, float alpha_lr,
-                                           float inv_w, unsigned flags) {
-    constexpr int C = WT > 0 ? (WT < kChunk ? WT : kChunk) : 1;
-    static_assert(WT <= 0 || WT % C == 0, "replica batches must tile W");
+// per-thread values carried across replica batches
+struct SyncAcc {
+    float gbar[kVec];  // gradient mean
+    float a[kVec];     // anchor (CPDP) / averaged model (LocalSGD)
+    float u[kVec];     // SlowMo state
+    float s[kVec];     // sum of x_i - reference
+    float x0[kVec];    // LocalSGD reference: replica 0's x
+    float msum[kVec];  // optimizer-state sums (state reconciliation)
+    float vsum[kVec];
+};
+
+template <int C, bool FULL, class Rows>
+__device__ __forceinline__ void grad_batch(const Rows& r, int i0, int64_t p0, int n,
+                                           float (&acc)[kVec]) {
+    float g[C][kVec];
+#pragma unroll
+    for (int c = 0; c < C; ++c) load_f32<FULL, kNTL>(r.g(i0 + c) + p0, n, g[c]);
+#pragma unroll
+    for (int c = 0; c < C; ++c)
+#pragma unroll
+        for (int k = 0; k < kVec; ++k) acc[k] += g[c][k];
+}
+
+template <Sync M, Opt O, int C, class PS, bool FULL, class Rows>
+__device__ __forceinline__ void step_batch(const OptParams& o, const Rows& r, int i0, int64_t p0,
+                                           int n, SyncAcc& z, bool avg_state) {
+    constexpr bool kAdam = O == Opt::ADAMW;
+    float m[C][kVec], v[C][kVec], th[C][kVec], g[C][kVec];
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        if constexpr (M == Sync::LocalSGD) load_f32<FULL, kNTL>(r.g(i0 + c) + p0, n, g[c]);
+        load_f32<FULL, kNTL>(r.m(i0 + c) + p0, n, m[c]);
+        if constexpr (kAdam) load_f32<FULL, kNTL>(r.v(i0 + c) + p0, n, v[c]);
+        PS::template load<FULL, kNTL>(r.prm(i0 + c) + p0, n, th[c]);
+    }
+#pragma unroll
+    for (int c = 0; c < C; ++c)
+#pragma unroll
+        for (int k = 0; k < kVec; ++k) {
+            const float gk = M == Sync::LocalSGD ? g[c][k] : z.gbar[k];
+            const float x = opt_update<O, PS>(o, th[c][k], m[c][k], v[c][k], gk);
+            if constexpr (M == Sync::CPDP) {
+                z.s[k] += x - z.a[k];
+            } else if constexpr (M == Sync::LocalSGD) {
+                if (i0 + c == 0) z.x0[k] = x;
+                z.s[k] += x - z.x0[k];
+            } else {
+                th[c][k] = x;
+            }
+        }
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        if (avg_state) {
+#pragma unroll
+            for (int k = 0; k < kVec; ++k) {
+                z.msum[k] += m[c][k];
+                if constexpr (kAdam) z.vsum[k] += v[c][k];
+            }
+        } else {
+            store_f32<FULL, kNTS>(r.m(i0 + c) + p0, n, m[c]);
+            if constexpr (kAdam) store_f32<FULL, kNTS>(r.v(i0 + c) + p0, n, v[c]);
+        }
+        if constexpr (M == Sync::DDP) PS::template store<FULL, kNTS>(r.prm(i0 + c) + p0, n, th[c]);
+    }
+}
+
+template <Sync M, Opt O, int WT, class PS, bool FULL, bool EXTRA, class Rows>
+__device__ __forceinline__ void sync_chunk(const OptParams& o, const Rows& r, float* slow,
+                                           float* anchor, int W, int64_t p0, int n, float beta,
+                                           float alpha_lr, float inv_w, unsigned flags) {
     static_assert(!EXTRA || WT == 0, "variants run on the run-time-W kernel");
+    constexpr int C = WT > 0 ? (WT < kChunk ? WT : kChunk) : kChunk;
+    static_assert(WT <= 0 || WT % C == 0, "replica batches must tile W");
     constexpr bool kAdam = O == Opt::ADAMW;
     const int nw = WT > 0 ? WT : W;
     const bool avg_state = EXTRA && (flags & kSyncAverageState);
-    float msum[kVec] = {0.0f, 0.0f, 0.0f, 0.0f}, vsum[kVec] = {0.0f, 0.0f, 0.0f, 0.0f};
+    SyncAcc z;
+#pragma unroll
+    for (int k = 0; k < kVec; ++k)
+        z.gbar[k] = z.a[k] = z.u[k] = z.s[k] = z.x0[k] = z.msum[k] = z.vsum[k] = 0.0f;
 
     // gradient mean (the gradient AllReduce of a synchronisation step),
     // summed in the fixed order i = 0, 1, ..., W-1
-    float gbar[kVec] = {0.0f, 0.0f, 0.0f, 0.0f};
     if constexpr (M != Sync::LocalSGD) {
         float acc[kVec] = {0.0f, 0.0f, 0.0f, 0.0f};
+        if constexpr (WT > 0) {
 #pragma unroll
-        for (int i0 = 0; i0 < nw; i0 += C) {
-            float g[C][kVec];
-#pragma unroll
-            for (int c = 0; c < C; ++c)
-                load_f32<FULL, kNTL>(grads + (int64_t)(i0 + c) * ld + p0, n, g[c]);
-#pragma unroll
-            for (int c = 0; c < C; ++c)
-#pragma unroll
-                for (int k = 0; k < kVec; ++k) acc[k] += g[c][k];
+            for (int i0 = 0; i0 < WT; i0 += C) grad_batch<C, FULL>(r, i0, p0, n, acc);
+        } else {
+            int i0 = 0;
+            for (; i0 + C <= nw; i0 += C) grad_batch<C, FULL>(r, i0, p0, n, acc);
+            for (; i0 < nw; ++i0) grad_batch<1, FULL>(r, i0, p0, n, acc);
         }
 #pragma unroll
-        for (int k = 0; k < kVec; ++k) gbar[k] = acc[k] * inv_w;
-        if (EXTRA && (flags & kSyncWriteGbar)) {
-            // the gradient rows are the caller's; this variant overwrites them
-            float* g_out = const_cast<float*>(grads);
-            for (int i = 0; i < nw; ++i) store_f32<FULL, kNTS>(g_out + (int64_t)i * ld + p0, n, gbar);
-        }
+        for (int k = 0; k < kVec; ++k) z.gbar[k] = acc[k] * inv_w;
+        if (EXTRA && (flags & kSyncWriteGbar))
+            for (int i = 0; i < nw; ++i) store_f32<FULL, kNTS>(r.g(i) + p0, n, z.gbar);
     }
 
-    float a[kVec], u[kVec];
     if constexpr (M == Sync::CPDP) {
-        load_f32<FULL, kNTL>(anchor + p0, n, a);
-        load_f32<FULL, kNTL>(slow + p0, n, u);
+        load_f32<FULL, kNTL>(anchor + p0, n, z.a);
+        load_f32<FULL, kNTL>(slow + p0, n, z.u);
     }
 
     // optimizer step of every replica.  The parameter mean is accumulated as
     // a sum of differences to a reference that is close to every x_i (the
     // anchor for CPDP, replica 0's x for LocalSGD), so the small deviations
     // keep their precision.
-    float s[kVec] = {0.0f, 0.0f, 0.0f, 0.0f};
-    float x0[kVec] = {0.0f, 0.0f, 0.0f, 0.0f};
+    if constexpr (WT > 0) {
 #pragma unroll
-    for (int i0 = 0; i0 < nw; i0 += C) {
-        float m[C][kVec], v[C][kVec], th[C][kVec], g[C][kVec];
-#pragma unroll
-        for (int c = 0; c < C; ++c) {
-            const int64_t off = (int64_t)(i0 + c) * ld + p0;
-            if constexpr (M == Sync::LocalSGD) load_f32<FULL, kNTL>(grads + off, n, g[c]);
-            load_f32<FULL, kNTL>(mom + off, n, m[c]);
-            if constexpr (kAdam) load_f32<FULL, kNTL>(mom2 + off, n, v[c]);
-            PS::template load<FULL, kNTL>(params + off, n, th[c]);
-        }
-#pragma unroll
-        for (int c = 0; c < C; ++c)
-#pragma unroll
-            for (int k = 0; k < kVec; ++k) {
-                const float gk = M == Sync::LocalSGD ? g[c][k] : gbar[k];
-                const float x = opt_update<O, PS>(o, th[c][k], m[c][k], v[c][k], gk);
-                if constexpr (M == Sync::CPDP) {
-                    s[k] += x - a[k];
-                } else if constexpr (M == Sync::LocalSGD) {
-                    if (i0 + c == 0) x0[k] = x;
-                    s[k] += x - x0[k];
-                } else {
-                    th[c][k] = x;
-                }
-            }
-#pragma unroll
-        for (int c = 0; c < C; ++c) {
-            const int64_t off = (int64_t)(i0 + c) * ld + p0;
-            if (avg_state) {
-#pragma unroll
-                for (int k = 0; k < kVec; ++k) {
-                    msum[k] += m[c][k];
-                    if constexpr (kAdam) vsum[k] += v[c][k];
-                }
-            } else {
-                store_f32<FULL, kNTS>(mom + off, n, m[c]);
-                if constexpr (kAdam) store_f32<FULL, kNTS>(mom2 + off, n, v[c]);
-            }
-            if constexpr (M == Sync::DDP) PS::template store<FULL, kNTS>(params + off, n, th[c]);
-        }
+        for (int i0 = 0; i0 < WT; i0 += C) step_batch<M, O, C, PS, FULL>(o, r, i0, p0, n, z, avg_state);
+    } else {
+        int i0 = 0;
+        for (; i0 + C <= nw; i0 += C) step_batch<M, O, C, PS, FULL>(o, r, i0, p0, n, z, avg_state);
+        for (; i0 < nw; ++i0) step_batch<M, O, 1, PS, FULL>(o, r, i0, p0, n, z, avg_state);
     }
     if (avg_state) {
 #pragma unroll
         for (int k = 0; k < kVec; ++k) {
-            msum[k] *= inv_w;
-            vsum[k] *= inv_w;
+            z.msum[k] *= inv_w;
+            z.vsum[k] *= inv_w;
         }
         for (int i = 0; i < nw; ++i) {
-            const int64_t off = (int64_t)i * ld + p0;
-            store_f32<FULL, kNTS>(mom + off, n, msum);
-            if constexpr (kAdam) store_f32<FULL, kNTS>(mom2 + off, n, vsum);
+            store_f32<FULL, kNTS>(r.m(i) + p0, n, z.msum);
+            if constexpr (kAdam) store_f32<FULL, kNTS>(r.v(i) + p0, n, z.vsum);
         }
     }
     if constexpr (M == Sync::DDP) return;
@@ -374,22 +533,21 @@ __device__ __forceinline__ void sync_chunk(const OptParams& o, typename PS::T* p
         // SlowMo outer step: u <- beta u + (a - avg)/lr ; new = a - alpha lr u
 #pragma unroll
         for (int k = 0; k < kVec; ++k) {
-            const float drift = s[k] * inv_w;  // avg - a
-            u[k] = fmaf(beta, u[k], -drift / o.lr);
-            a[k] = fmaf(-alpha_lr, u[k], a[k]);
+            const float drift = z.s[k] * inv_w;  // avg - a
+            z.u[k] = fmaf(beta, z.u[k], -drift / o.lr);
+            z.a[k] = fmaf(-alpha_lr, z.u[k], z.a[k]);
         }
-        store_f32<FULL, kNTS>(slow + p0, n, u);
-        store_f32<FULL, kNTS>(anchor + p0, n, a);
+        store_f32<FULL, kNTS>(slow + p0, n, z.u);
+        store_f32<FULL, kNTS>(anchor + p0, n, z.a);
     } else {
 #pragma unroll
-        for (int k = 0; k < kVec; ++k) a[k] = fmaf(s[k], inv_w, x0[k]);
-        if (anchor != nullptr) store_f32<FULL, kNTS>(anchor + p0, n, a);
+        for (int k = 0; k < kVec; ++k) z.a[k] = fmaf(z.s[k], inv_w, z.x0[k]);
+        if (anchor != nullptr) store_f32<FULL, kNTS>(anchor + p0, n, z.a);
     }
 
     // copy the reconciled model back into every replica
 #pragma unroll
-    for (int i = 0; i < nw; ++i)
-        PS::template store<FULL, kNTS>(params + (int64_t)i * ld + p0, n, a);
+    for (int i = 0; i < nw; ++i) PS::template store<FULL, kNTS>(r.prm(i) + p0, n, z.a);
 }
 
 template <Sync M, Opt O, int WT, class PS, bool EXTRA>
@@ -400,13 +558,37 @@ __global__ __launch_bounds__(kBlock) void sync_kernel(
     float inv_w, unsigned flags) {
     const int64_t p0 = ((int64_t)blockIdx.x * kBlock + threadIdx.x) * kVec;
     if (p0 >= P) return;
+    // grads are written only by the write-back variant
+    const Strided<PS> r{params, mom, mom2, const_cast<float*>(grads), ld};
     if (p0 + kVec <= P)
-        sync_chunk<M, O, WT, PS, true, EXTRA>(o, params, mom, mom2, grads, slow, anchor, W, ld,
-                                              p0, kVec, beta, alpha_lr, inv_w, flags);
+        sync_chunk<M, O, WT, PS, true, EXTRA>(o, r, slow, anchor, W, p0, kVec, beta, alpha_lr,
+                                              inv_w, flags);
     else
-        sync_chunk<M, O, WT, PS, false, EXTRA>(o, params, mom, mom2, grads, slow, anchor, W,
-                                               ld, p0, (int)(P - p0), beta, alpha_lr, inv_w,
-                                               flags);
+        sync_chunk<M, O, WT, PS, false, EXTRA>(o, r, slow, anchor, W, p0, (int)(P - p0), beta,
+                                               alpha_lr, inv_w, flags);
+}
+
+// multi-tensor plan: block b -> tensor t and its chunk; run-time W
+template <Sync M, Opt O, class PS, bool EXTRA>
+__global__ __launch_bounds__(kBlock) void sync_plan_kernel(OptParams o,
+                                                           const int64_t* __restrict__ plan, int W,
+                                                           int n, float beta, float alpha_lr,
+                                                           float inv_w, unsigned flags) {
+    const PlanView v = plan_view(plan, W, n);
+    const int64_t b = blockIdx.x;
+    const int64_t t = plan_tensor(v, n, b);
+    const int64_t P = v.numel[t];
+    const int64_t p0 = ((b - v.chunk_start[t]) * kBlock + threadIdx.x) * kVec;
+    if (p0 >= P) return;
+    const Table<PS> r{v.params, v.mom, v.mom2, v.grads, n, t};
+    float* slow = reinterpret_cast<float*>(v.slow[t]);
+    float* anchor = reinterpret_cast<float*>(v.anchor[t]);
+    if (p0 + kVec <= P)
+        sync_chunk<M, O, 0, PS, true, EXTRA>(o, r, slow, anchor, W, p0, kVec, beta, alpha_lr,
+                                             inv_w, flags);
+    else
+        sync_chunk<M, O, 0, PS, false, EXTRA>(o, r, slow, anchor, W, p0, (int)(P - p0), beta,
+                                              alpha_lr, inv_w, flags);
 }
 
 // ---- launch helpers -------------------------------------------------------------
@@ -508,7 +690,94 @@ int sync_o(Opt opt, Param pt, const OptParams& o, const SyncArgs& a) {
     }
 }
 
+template <Opt O>
+int local_plan_o(Param pt, const OptParams& o, const int64_t* plan, int W, int n,
+                 int64_t total_chunks, void* stream) {
+    const int64_t blocks = total_chunks * W;
+    return pt == Param::BF16 ? launch(local_step_plan_kernel<O, ParamBF16>, blocks, stream, o, plan,
+                                      W, n, total_chunks)
+                             : launch(local_step_plan_kernel<O, ParamF32>, blocks, stream, o, plan,
+                                      W, n, total_chunks);
+}
+
+template <Sync M, Opt O, class PS>
+int sync_plan_t(const OptParams& o, const int64_t* plan, int W, int n, int64_t total_chunks,
+                float beta, float alpha, unsigned flags, void* stream) {
+    const float alpha_lr = alpha * o.lr;
+    const float inv_w = 1.0f / (float)W;
+    if (flags != 0)
+        return launch(sync_plan_kernel<M, O, PS, true>, total_chunks, stream, o, plan, W, n, beta,
+                      alpha_lr, inv_w, flags);
+    return launch(sync_plan_kernel<M, O, PS, false>, total_chunks, stream, o, plan, W, n, beta,
+                  alpha_lr, inv_w, flags);
+}
+
+template <Sync M, Opt O>
+int sync_plan_p(Param pt, const OptParams& o, const int64_t* plan, int W, int n,
+                int64_t total_chunks, float beta, float alpha, unsigned flags, void* stream) {
+    return pt == Param::BF16
+               ? sync_plan_t<M, O, ParamBF16>(o, plan, W, n, total_chunks, beta, alpha, flags,
+                                              stream)
+               : sync_plan_t<M, O, ParamF32>(o, plan, W, n, total_chunks, beta, alpha, flags,
+                                             stream);
+}
+
+template <Sync M>
+int sync_plan_o(Opt opt, Param pt, const OptParams& o, const int64_t* plan, int W, int n,
+                int64_t total_chunks, float beta, float alpha, unsigned flags, void* stream) {
+    switch (opt) {
+        case Opt::SGD_WD:
+            return sync_plan_p<M, Opt::SGD_WD>(pt, o, plan, W, n, total_chunks, beta, alpha,
+                                               flags, stream);
+        case Opt::ADAMW:
+            return sync_plan_p<M, Opt::ADAMW>(pt, o, plan, W, n, total_chunks, beta, alpha, flags,
+                                              stream);
+        default:
+            return sync_plan_p<M, Opt::SGD>(pt, o, plan, W, n, total_chunks, beta, alpha, flags,
+                                            stream);
+    }
+}
+
 }  // namespace
+
+int launch_state_init_plan(Param pt, const int64_t* plan, int W, int n, int64_t total_chunks,
+                           void* stream) {
+    const int64_t blocks = total_chunks * W;
+    return pt == Param::BF16
+               ? launch(state_init_plan_kernel<ParamBF16>, blocks, stream, plan, W, n, total_chunks)
+               : launch(state_init_plan_kernel<ParamF32>, blocks, stream, plan, W, n, total_chunks);
+}
+
+int launch_local_step_plan(Opt opt, const OptParams& o, Param pt, const int64_t* plan, int W,
+                           int n, int64_t total_chunks, void* stream) {
+    switch (opt) {
+        case Opt::SGD_WD: return local_plan_o<Opt::SGD_WD>(pt, o, plan, W, n, total_chunks, stream);
+        case Opt::ADAMW: return local_plan_o<Opt::ADAMW>(pt, o, plan, W, n, total_chunks, stream);
+        default: return local_plan_o<Opt::SGD>(pt, o, plan, W, n, total_chunks, stream);
+    }
+}
+
+int launch_sync_plan(Sync mode, Opt opt, const OptParams& o, Param pt, const int64_t* plan, int W,
+                     int n, int64_t total_chunks, float beta, float alpha, unsigned flags,
+                     void* stream) {
+    switch (mode) {
+        case Sync::LocalSGD:
+            return sync_plan_o<Sync::LocalSGD>(opt, pt, o, plan, W, n, total_chunks, beta, alpha,
+                                               flags, stream);
+        case Sync::DDP:
+            return sync_plan_o<Sync::DDP>(opt, pt, o, plan, W, n, total_chunks, beta, alpha, flags,
+                                          stream);
+        default:
+            return sync_plan_o<Sync::CPDP>(opt, pt, o, plan, W, n, total_chunks, beta, alpha,
+                                           flags, stream);
+    }
+}
+
+int64_t coords_per_block() { return (int64_t)kBlock * kVec; }
+
+int upload_plan(void* dev, const int64_t* host, int64_t words) {
+    return (int)hipMemcpy(dev, host, (size_t)words * sizeof(int64_t), hipMemcpyHostToDevice);
+}
 
 int launch_state_init(Param pt, const void* theta0, void* params, float* mom, float* mom2,
                       float* slow, float* anchor, int W, int64_t P, int64_t ld, void* stream) {

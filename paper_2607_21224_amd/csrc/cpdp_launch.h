@@ -54,6 +54,33 @@ int launch_sync(Sync mode, Opt opt, const OptParams& o, Param pt, void* params,
                 float* anchor, int W, int64_t P, int64_t ld, float beta,
                 float alpha, unsigned flags, void* stream);
 
+// Multi-tensor plan table in device memory, as 64-bit words:
+//   [0] W  [1] n  [2] total chunks  [3] reserved
+//   chunk_start[n + 1]   first chunk of every tensor (chunk = coords_per_block())
+//   numel[n]
+//   params[W*n], mom[W*n], mom2[W*n], grads[W*n]   device addresses, [i*n + t]
+//   slow[n], anchor[n]                              device addresses (0 = none)
+constexpr int64_t kPlanHeaderWords = 4;
+inline int64_t plan_words(int W, int n) {
+    return kPlanHeaderWords + (int64_t)(n + 1) + n + 4 * (int64_t)W * n + 2 * (int64_t)n;
+}
+
+int launch_state_init_plan(Param pt, const int64_t* plan, int W, int n,
+                           int64_t total_chunks, void* stream);
+
+int launch_local_step_plan(Opt opt, const OptParams& o, Param pt, const int64_t* plan,
+                           int W, int n, int64_t total_chunks, void* stream);
+
+int launch_sync_plan(Sync mode, Opt opt, const OptParams& o, Param pt,
+                     const int64_t* plan, int W, int n, int64_t total_chunks,
+                     float beta, float alpha, unsigned flags, void* stream);
+
+// Coordinates one block of the flat and plan kernels covers.
+int64_t coords_per_block();
+
+// Synchronous host-to-device copy of a plan table; returns the HIP status.
+int upload_plan(void* dev, const int64_t* host, int64_t words);
+
 // True when a launch over P coordinates (rows = W for the row-parallel local
 // step, 1 otherwise) fits in one grid.
 bool grid_fits(int rows, int64_t P);

@@ -1,0 +1,67 @@
+"""Multi-tensor CPDP state: the model as a list of separate tensors per
+replica (as a framework holds it), driven through a device-resident plan so
+each step is one launch over all tensors."""
+from __future__ import annotations
+
+import torch
+
+from . import cpdp
+from .state import Hyper, Optimizer
+
+
+class CpdpMultiState:
+    """W replicas of a model given as tensor sizes ``numels``; every
+    (replica, tensor) of params / mom (/ mom2) / grads is its own allocation;
+    slow_mom and anchor are one tensor per model tensor."""
+
+    def __init__(self, W: int, numels, K: int = 1, param_dt: str = "f32",
+                 adamw: bool = False, device="cuda"):
+        self.W, self.K, self.param_dt = int(W), int(K), param_dt
+        self.numels = [int(x) for x in numels]
+        n = self.n = len(self.numels)
+        tdt = torch.bfloat16 if param_dt == "bf16" else torch.float32
+        mk = lambda dt: [[torch.empty(max(x, 1), dtype=dt, device=device)  # noqa: E731
+                          for x in self.numels] for _ in range(W)]
+        self.params, self.mom, self.grads = mk(tdt), mk(torch.float32), mk(torch.float32)
+        self.mom2 = mk(torch.float32) if adamw else None
+        self.slow_mom = [torch.empty(max(x, 1), device=device) for x in self.numels]
+        self.anchor = [torch.empty(max(x, 1), device=device) for x in self.numels]
+        nbytes = cpdp.cpdp_plan_bytes(W, n)
+        self.table = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        self.plan = cpdp.cpdp_plan()
+        self.plan.table = self.table.data_ptr()
+        flat = lambda fam: [fam[i][t] for i in range(W) for t in range(n)]  # noqa: E731
+        cpdp.cpdp_plan_build(self.plan, nbytes, W, n, self.numels, flat(self.params),
+                             flat(self.mom), flat(self.mom2) if adamw else None,
+                             flat(self.grads), self.slow_mom, self.anchor, param_dt)
+        self.opt_step = 0
+
+    def init(self, theta0_list, stream=None) -> None:
+        """Algorithm 1 initialisation from per-tensor initial values."""
+        for a, th in zip(self.anchor, theta0_list):
+            a[: th.numel()].copy_(th.float())
+        torch.cuda.synchronize()
+        cpdp.cpdp_state_init_plan(self.plan, stream)
+        self.opt_step = 0
+
+    def step(self, t: int, opt: Optimizer, beta: float = 0.0, alpha: float = 1.0, T: int = 0,
+             stream=None, method: str = "cpdp", flags: int = 0) -> str:
+        """Step t on the gradients currently in self.grads (see
+        CpdpState.step_opt)."""
+        self.opt_step += 1
+        c = opt.c_struct(self.opt_step)
+        if method == "ddp" or cpdp.cpdp_is_sync_step(t, self.K, T):
+            cpdp.cpdp_sync_step_plan(method, self.plan, self.K, c, beta, alpha, flags, stream)
+            return "reconcile"
+        cpdp.cpdp_local_step_plan(self.plan, self.K, c, stream)
+        return "local"
+
+    def sgd(self, h: Hyper) -> Optimizer:
+        return Optimizer("sgd", h.lr, h.mu)
+
+    def gather(self, fam: str, i: int | None = None) -> torch.Tensor:
+        """Concatenate replica i's tensors of a family (or a per-model family
+        when i is None) into one flat tensor, in model order."""
+        src = getattr(self, fam)
+        parts = src if i is None else src[i]
+        return torch.cat([p[:x] for p, x in zip(parts, self.numels)])

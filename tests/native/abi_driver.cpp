@@ -64,6 +64,45 @@ int main() {
     adam.step = 0;
     EXPECT(cpdp_local_step_opt(pa, mo, m2, gr, W, P, ld, 4, &adam, 0, nullptr), CPDP_ERR_INVALID_ARG, false);
 
+    {
+        // a 3-tensor plan over fake, far-apart addresses (never dereferenced)
+        const int n = 3;
+        const int64_t numel[n] = {100, 0, 1027};
+        void* tp[W * n];
+        void* tm[W * n];
+        void* tv[W * n];
+        void* tg[W * n];
+        float* ts[n];
+        float* ta[n];
+        int k = 0;
+        auto far = [&](void) { return reinterpret_cast<void*>((uintptr_t)(1ull << 44) + ((uintptr_t)(k++) << 24)); };
+        for (int j = 0; j < W * n; ++j) { tp[j] = far(); tm[j] = far(); tv[j] = far(); tg[j] = far(); }
+        for (int t = 0; t < n; ++t) { ts[t] = static_cast<float*>(far()); ta[t] = static_cast<float*>(far()); }
+        cpdp_plan plan = {};
+        plan.table = at(7);
+        const int64_t bytes = cpdp_plan_bytes(W, n);
+        EXPECT(cpdp_plan_build(&plan, bytes, W, n, numel, tp, tm, tv, tg, ts, ta, 0), CPDP_OK, false);
+        if (plan.total_chunks != 3 || plan.total_numel != 1127) { std::printf("FAIL plan totals\n"); ++failures; }
+        EXPECT(cpdp_plan_build(&plan, bytes - 8, W, n, numel, tp, tm, tv, tg, ts, ta, 0), CPDP_ERR_INVALID_ARG, false);
+        void* keep = tg[0];
+        tg[0] = tm[0];  // tensor 0 is non-empty: its grads would alias its momentum
+        EXPECT(cpdp_plan_build(&plan, bytes, W, n, numel, tp, tm, tv, tg, ts, ta, 0), CPDP_ERR_OVERLAP, false);
+        tg[0] = keep;
+        tg[1] = tm[0];  // tensor 1 is empty: its pointers are not ranges
+        EXPECT(cpdp_plan_build(&plan, bytes, W, n, numel, tp, tm, tv, tg, ts, ta, 0), CPDP_OK, false);
+        tg[1] = far();
+        EXPECT(cpdp_plan_build(&plan, bytes, W, n, numel, tp, tm, tv, tg, ts, ta, 0), CPDP_OK, false);
+        EXPECT(cpdp_state_init_plan(&plan, nullptr), CPDP_OK, true);
+        EXPECT(cpdp_local_step_plan(&plan, 4, &sgd, nullptr), CPDP_OK, true);
+        EXPECT(cpdp_sync_step_plan(0, &plan, 4, &sgd, 0.5f, 1.0f, 3u, nullptr), CPDP_OK, true);
+        EXPECT(cpdp_sync_step_plan(0, &plan, 4, &sgd, 1.5f, 1.0f, 0u, nullptr), CPDP_ERR_INVALID_ARG, false);
+        EXPECT(cpdp_plan_build(&plan, bytes, W, n, numel, tp, tm, nullptr, tg, nullptr, nullptr, 0), CPDP_OK, false);
+        EXPECT(cpdp_sync_step_plan(0, &plan, 4, &sgd, 0.5f, 1.0f, 0u, nullptr), CPDP_ERR_NULL, false);
+        EXPECT(cpdp_sync_step_plan(2, &plan, 4, &sgd, 0.5f, 1.0f, 0u, nullptr), CPDP_OK, true);
+        adam.step = 1;
+        EXPECT(cpdp_local_step_plan(&plan, 4, &adam, nullptr), CPDP_ERR_NULL, false);
+    }
+
     EXPECT(cpdp_is_sync_step(4, 4, 0), 1, false);
     EXPECT(cpdp_is_sync_step(3, 4, 0), 0, false);
     EXPECT(cpdp_is_sync_step(0, 4, 0), -CPDP_ERR_INVALID_ARG, false);

@@ -18,6 +18,20 @@ int launch_sync(Sync, Opt, const OptParams&, Param, void*, float*, float*, const
                 float*, int, int64_t, int64_t, float, float, unsigned, void*) {
     return ++g_launches, 0;
 }
+int launch_state_init_plan(Param, const int64_t*, int, int, int64_t, void*) {
+    return ++g_launches, 0;
+}
+int launch_local_step_plan(Opt, const OptParams&, Param, const int64_t*, int, int, int64_t,
+                           void*) {
+    return ++g_launches, 0;
+}
+int launch_sync_plan(Sync, Opt, const OptParams&, Param, const int64_t*, int, int, int64_t, float,
+                     float, unsigned, void*) {
+    return ++g_launches, 0;
+}
+int64_t coords_per_block() { return 1024; }
+int g_uploaded_words = 0;
+int upload_plan(void*, const int64_t*, int64_t words) { return g_uploaded_words = (int)words, 0; }
 bool grid_fits(int rows, int64_t P) { return rows >= 1 && (P + 1023) / 1024 <= 0x7FFFFFFF / rows; }
 const char* hip_error_string(int) { return "stub"; }
 }  // namespace cpdp

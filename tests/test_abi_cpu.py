@@ -296,3 +296,63 @@ def test_lr_at_matches_oracle():
                 (0, 10, 0, 0.0, 0.0), (0, 10, 0, 0.1, 0.2), (0, 10, 0, 0.1, -1.0)]:
         with pytest.raises(ValueError):
             cpdp.cpdp_lr_at(*bad)
+
+
+def test_plan_bytes():
+    assert cpdp.cpdp_plan_bytes(8, 161) == 8 * (4 + 162 + 161 + 4 * 8 * 161 + 2 * 161)
+    assert cpdp.cpdp_plan_bytes(0, 5) == 0
+
+
+def _plan_args(W=2, n=3, numel=(100, 4, 8), **kw):
+    base = A
+    step = 1 << 30
+    k = [0]
+
+    def nxt():
+        k[0] += 1
+        return base + k[0] * step
+    a = dict(params=[nxt() for _ in range(W * n)], mom=[nxt() for _ in range(W * n)],
+             grads=[nxt() for _ in range(W * n)], mom2=None,
+             slow=[nxt() for _ in range(n)], anchor=[nxt() for _ in range(n)], pdt=0,
+             table=T0, bytes=cpdp.cpdp_plan_bytes(W, n))
+    a.update(kw)
+    plan = cpdp.cpdp_plan()
+    plan.table = a["table"]
+    return cpdp.cpdp_plan_build(plan, a["bytes"], W, n, list(numel), a["params"], a["mom"],
+                                a["mom2"], a["grads"], a["slow"], a["anchor"], a["pdt"],
+                                check=False)
+
+
+def test_plan_build_validation():
+    assert _plan_args(W=0) == E.CPDP_ERR_INVALID_ARG
+    assert _plan_args(n=0, numel=()) == E.CPDP_ERR_INVALID_ARG
+    assert _plan_args(bytes=64) == E.CPDP_ERR_INVALID_ARG
+    assert _plan_args(numel=(100, -1, 8)) == E.CPDP_ERR_INVALID_ARG
+    assert _plan_args(pdt=4) == E.CPDP_ERR_DTYPE
+    assert _plan_args(table=None) == E.CPDP_ERR_NULL
+    assert _plan_args(table=T0 + 4) == E.CPDP_ERR_MISALIGNED
+    p = [A + (1 << 30) * (j + 1) for j in range(6)]
+    assert _plan_args(params=[p[0] + 8] + p[1:]) == E.CPDP_ERR_MISALIGNED
+    assert _plan_args(params=[None] + p[1:]) == E.CPDP_ERR_NULL
+    q = list(p)
+    q[1] = q[0] + 256          # second tensor starts inside the first (100 floats)
+    assert _plan_args(params=q) == E.CPDP_ERR_OVERLAP
+    far = A + (1 << 44)
+    assert _plan_args(anchor=[A + (1 << 30), far, far + (1 << 30)]) == E.CPDP_ERR_OVERLAP
+
+
+def test_plan_step_validation():
+    plan = cpdp.cpdp_plan()
+    sgd = opt_struct(kind=0)
+    assert cpdp.cpdp_local_step_plan(plan, 2, sgd, check=False) == E.CPDP_ERR_NULL
+    plan.table = T0
+    plan.W, plan.n_tensors, plan.param_dt = 2, 3, 0
+    plan.total_chunks = 3
+    assert cpdp.cpdp_local_step_plan(plan, 0, sgd, check=False) == E.CPDP_ERR_INVALID_ARG
+    assert cpdp.cpdp_local_step_plan(plan, 2, opt_struct(kind=1), check=False) == E.CPDP_ERR_NULL
+    assert cpdp.cpdp_sync_step_plan(0, plan, 2, sgd, check=False) == E.CPDP_ERR_NULL
+    assert cpdp.cpdp_sync_step_plan(5, plan, 2, sgd, check=False) == E.CPDP_ERR_INVALID_ARG
+    assert cpdp.cpdp_sync_step_plan(2, plan, 2, sgd, flags=8, check=False) == E.CPDP_ERR_INVALID_ARG
+    assert cpdp.cpdp_state_init_plan(plan, check=False) == E.CPDP_ERR_NULL
+    plan.param_dt = 7
+    assert cpdp.cpdp_sync_step_plan(2, plan, 2, sgd, check=False) == E.CPDP_ERR_DTYPE
