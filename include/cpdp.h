@@ -227,7 +227,8 @@ int cpdp_sync_step_opt(int strategy, void* params, void* mom, void* mom2,
  * The table lives in device memory the caller allocates (cpdp_plan_bytes
  * bytes, 8-byte aligned) and keeps alive while the plan is used;
  * cpdp_plan_build fills it once with a synchronous copy.  The cpdp_plan
- * struct is the host handle the step calls take.
+ * struct is the host handle the step calls take; its fields are read-only
+ * for the caller (they are sealed, see cpdp_plan.seal).
  * ------------------------------------------------------------------------ */
 typedef struct cpdp_plan {
     void* table;          /* device memory, >= cpdp_plan_bytes(W, n_tensors)  */
@@ -239,6 +240,11 @@ typedef struct cpdp_plan {
     int has_anchor;       /* reference-model tensors given (CPDP, LocalSGD)     */
     int64_t total_chunks; /* filled by cpdp_plan_build                          */
     int64_t total_numel;  /* filled by cpdp_plan_build: sum of numel            */
+    uint64_t seal;        /* filled by cpdp_plan_build: a hash of every field
+                             above; a step call on a handle whose fields no
+                             longer match it returns CPDP_ERR_INVALID_ARG, so
+                             an edited handle can never make a kernel read the
+                             table with the wrong layout                        */
 } cpdp_plan;
 
 /* Device bytes of a plan table for W replicas of n_tensors tensors. */

@@ -55,7 +55,8 @@ class cpdp_plan(ctypes.Structure):
     _fields_ = [("table", ctypes.c_void_p), ("W", ctypes.c_int), ("n_tensors", ctypes.c_int),
                 ("param_dt", ctypes.c_int), ("has_mom2", ctypes.c_int),
                 ("has_slow_mom", ctypes.c_int), ("has_anchor", ctypes.c_int),
-                ("total_chunks", ctypes.c_int64), ("total_numel", ctypes.c_int64)]
+                ("total_chunks", ctypes.c_int64), ("total_numel", ctypes.c_int64),
+                ("seal", ctypes.c_uint64)]
 
 
 class cpdp_optimizer(ctypes.Structure):

@@ -123,6 +123,30 @@ int make_opt(const cpdp_optimizer* opt, cpdp::Opt* kind, cpdp::OptParams* o) {
     return CPDP_OK;
 }
 
+// Hash of every field of a plan handle except the seal itself (splitmix64
+// finaliser steps over the fields in declaration order).
+uint64_t plan_seal(const cpdp_plan* p) {
+    uint64_t h = 0x243F6A8885A308D3ull;
+    auto mix = [&h](uint64_t x) {
+        h ^= x;
+        h ^= h >> 30;
+        h *= 0xBF58476D1CE4E5B9ull;
+        h ^= h >> 27;
+        h *= 0x94D049BB133111EBull;
+        h ^= h >> 31;
+    };
+    mix(reinterpret_cast<uintptr_t>(p->table));
+    mix((uint64_t)(uint32_t)p->W);
+    mix((uint64_t)(uint32_t)p->n_tensors);
+    mix((uint64_t)(uint32_t)p->param_dt);
+    mix((uint64_t)(uint32_t)p->has_mom2);
+    mix((uint64_t)(uint32_t)p->has_slow_mom);
+    mix((uint64_t)(uint32_t)p->has_anchor);
+    mix((uint64_t)p->total_chunks);
+    mix((uint64_t)p->total_numel);
+    return h;
+}
+
 }  // namespace
 
 extern "C" {
@@ -403,6 +427,7 @@ int cpdp_plan_build(cpdp_plan* plan, int64_t plan_bytes, int W, int n, const int
     plan->has_anchor = anchor != nullptr;
     plan->total_chunks = chunks;
     plan->total_numel = total;
+    plan->seal = plan_seal(plan);
     return CPDP_OK;
 }
 
@@ -413,9 +438,16 @@ static int check_plan(const cpdp_plan* plan) {
     return CPDP_OK;
 }
 
+// The launch shape and the table layout the kernels assume come from the
+// handle, so a step call runs only on the exact fields cpdp_plan_build wrote.
+static int check_seal(const cpdp_plan* plan) {
+    return plan->seal == plan_seal(plan) ? CPDP_OK : CPDP_ERR_INVALID_ARG;
+}
+
 int cpdp_state_init_plan(const cpdp_plan* plan, void* stream) {
     if (int s = check_plan(plan)) return s;
     if (!plan->has_anchor) return CPDP_ERR_NULL;
+    if (int s = check_seal(plan)) return s;
     if (plan->total_chunks == 0) return CPDP_OK;
     return hip_status(cpdp::launch_state_init_plan(param_kind(plan->param_dt),
                                                    static_cast<const int64_t*>(plan->table),
@@ -430,6 +462,7 @@ int cpdp_local_step_plan(const cpdp_plan* plan, int K, const cpdp_optimizer* opt
     cpdp::OptParams o;
     if (int s = make_opt(opt, &kind, &o)) return s;
     if (kind == cpdp::Opt::ADAMW && !plan->has_mom2) return CPDP_ERR_NULL;
+    if (int s = check_seal(plan)) return s;
     if (plan->total_chunks == 0) return CPDP_OK;
     return hip_status(cpdp::launch_local_step_plan(kind, o, param_kind(plan->param_dt),
                                                    static_cast<const int64_t*>(plan->table),
@@ -455,6 +488,7 @@ int cpdp_sync_step_plan(int strategy, const cpdp_plan* plan, int K, const cpdp_o
         if (!plan->has_slow_mom || !plan->has_anchor) return CPDP_ERR_NULL;
     }
     if (kind == cpdp::Opt::ADAMW && !plan->has_mom2) return CPDP_ERR_NULL;
+    if (int s = check_seal(plan)) return s;
     if (plan->total_chunks == 0) return CPDP_OK;
     const cpdp::Sync mode = strategy == CPDP_SYNC_CPDP       ? cpdp::Sync::CPDP
                             : strategy == CPDP_SYNC_LOCALSGD ? cpdp::Sync::LocalSGD

@@ -21,6 +21,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "cpdp_launch.h"
 
 namespace cpdp {
@@ -550,15 +552,21 @@ __device__ __forceinline__ void sync_chunk(const OptParams& o, const Rows& r, fl
     for (int i = 0; i < nw; ++i) PS::template store<FULL, kNTS>(r.prm(i) + p0, n, z.a);
 }
 
+// The gradient rows are written only by the variants (the gradient-mean
+// write-back), so only those instantiations take them as mutable.
+template <bool EXTRA>
+using GradPtr = typename std::conditional<EXTRA, float*, const float*>::type;
+
 template <Sync M, Opt O, int WT, class PS, bool EXTRA>
 __global__ __launch_bounds__(kBlock) void sync_kernel(
     OptParams o, typename PS::T* __restrict__ params, float* __restrict__ mom,
-    float* __restrict__ mom2, const float* __restrict__ grads, float* __restrict__ slow,
+    float* __restrict__ mom2, GradPtr<EXTRA> __restrict__ grads, float* __restrict__ slow,
     float* __restrict__ anchor, int W, int64_t ld, int64_t P, float beta, float alpha_lr,
     float inv_w, unsigned flags) {
     const int64_t p0 = ((int64_t)blockIdx.x * kBlock + threadIdx.x) * kVec;
     if (p0 >= P) return;
-    // grads are written only by the write-back variant
+    // Strided holds mutable row pointers; without EXTRA no store to the
+    // gradient rows is instantiated
     const Strided<PS> r{params, mom, mom2, const_cast<float*>(grads), ld};
     if (p0 + kVec <= P)
         sync_chunk<M, O, WT, PS, true, EXTRA>(o, r, slow, anchor, W, p0, kVec, beta, alpha_lr,
@@ -657,8 +665,11 @@ int sync_w(const OptParams& o, const SyncArgs& a) {
     using T = typename PS::T;
     const float alpha_lr = a.alpha * o.lr;
     const float inv_w = 1.0f / (float)a.W;
+    // the variants run only from the entry points whose gradient argument is
+    // mutable (flags != 0), so dropping const here restores the caller's type
+    const GradPtr<EXTRA> grads = const_cast<float*>(a.grads);
     return launch(sync_kernel<M, O, WT, PS, EXTRA>, blocks_for(a.P), a.stream, o,
-                  static_cast<T*>(a.params), a.mom, a.mom2, a.grads, a.slow, a.anchor, a.W,
+                  static_cast<T*>(a.params), a.mom, a.mom2, grads, a.slow, a.anchor, a.W,
                   a.ld, a.P, a.beta, alpha_lr, inv_w, a.flags);
 }
 

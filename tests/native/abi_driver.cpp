@@ -96,6 +96,18 @@ int main() {
         EXPECT(cpdp_local_step_plan(&plan, 4, &sgd, nullptr), CPDP_OK, true);
         EXPECT(cpdp_sync_step_plan(0, &plan, 4, &sgd, 0.5f, 1.0f, 3u, nullptr), CPDP_OK, true);
         EXPECT(cpdp_sync_step_plan(0, &plan, 4, &sgd, 1.5f, 1.0f, 0u, nullptr), CPDP_ERR_INVALID_ARG, false);
+        // an edited handle no longer matches its seal and never reaches a launch
+        plan.W += 1;
+        EXPECT(cpdp_local_step_plan(&plan, 4, &sgd, nullptr), CPDP_ERR_INVALID_ARG, false);
+        plan.W -= 1;
+        plan.total_chunks += 1;
+        EXPECT(cpdp_sync_step_plan(0, &plan, 4, &sgd, 0.5f, 1.0f, 0u, nullptr), CPDP_ERR_INVALID_ARG, false);
+        EXPECT(cpdp_state_init_plan(&plan, nullptr), CPDP_ERR_INVALID_ARG, false);
+        plan.total_chunks -= 1;
+        plan.table = at(8);
+        EXPECT(cpdp_local_step_plan(&plan, 4, &sgd, nullptr), CPDP_ERR_INVALID_ARG, false);
+        plan.table = at(7);
+        EXPECT(cpdp_local_step_plan(&plan, 4, &sgd, nullptr), CPDP_OK, true);
         EXPECT(cpdp_plan_build(&plan, bytes, W, n, numel, tp, tm, nullptr, tg, nullptr, nullptr, 0), CPDP_OK, false);
         EXPECT(cpdp_sync_step_plan(0, &plan, 4, &sgd, 0.5f, 1.0f, 0u, nullptr), CPDP_ERR_NULL, false);
         EXPECT(cpdp_sync_step_plan(2, &plan, 4, &sgd, 0.5f, 1.0f, 0u, nullptr), CPDP_OK, true);

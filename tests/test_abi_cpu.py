@@ -356,3 +356,7 @@ def test_plan_step_validation():
     assert cpdp.cpdp_state_init_plan(plan, check=False) == E.CPDP_ERR_NULL
     plan.param_dt = 7
     assert cpdp.cpdp_sync_step_plan(2, plan, 2, sgd, check=False) == E.CPDP_ERR_DTYPE
+    # a handle cpdp_plan_build did not seal never reaches a launch
+    plan.param_dt = 0
+    assert cpdp.cpdp_local_step_plan(plan, 2, sgd, check=False) == E.CPDP_ERR_INVALID_ARG
+    assert cpdp.cpdp_sync_step_plan(2, plan, 2, sgd, check=False) == E.CPDP_ERR_INVALID_ARG
