@@ -43,9 +43,23 @@ def build_synth(out: str = LIB_SYNTH) -> str:
     return out
 
 
+CONSUMER = os.path.join(ROOT, "tests", "consumer", "abi_consumer")
+
+
+def build_consumer(out: str = CONSUMER) -> str:
+    """The torch-free host program of the ABI tests, linked to libcpdp.so."""
+    tmp = out + ".tmp"
+    _run([HIPCC, "-O2", "-std=c++17", "-Wall", "-I", os.path.join(ROOT, "include"),
+          "-o", tmp, out + ".cpp", "-L", PKG, "-lcpdp",
+          "-Wl,-rpath,$ORIGIN/../../paper_2607_21224_amd"])
+    os.replace(tmp, out)
+    return out
+
+
 def build_all() -> None:
     build_cpdp()
     build_synth()
+    build_consumer()
 
 
 if __name__ == "__main__":
