@@ -67,17 +67,20 @@ class cpdp_optimizer(ctypes.Structure):
                 ("step", ctypes.c_int64)]
 
 
-def _load() -> ctypes.CDLL:
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load a build of the C ABI and declare its signatures.  The module-level
+    ``lib`` is the default build; tests load differently configured builds of
+    the same sources (e.g. another block size) through this too."""
     # PyTorch ships its own HIP runtime.  Import it first so that libcpdp.so's
     # libamdhip64.so.7 dependency resolves to that already-loaded runtime: the
     # device memory and stream handles torch hands us belong to it, and a
     # second runtime instance in the process would not see the device.
     import torch  # noqa: F401
-    if not os.path.exists(LIB_PATH):
+    if not os.path.exists(path):
         raise ImportError(
-            f"{LIB_PATH} is not built; run `python -m paper_2607_21224_amd.build` "
+            f"{path} is not built; run `python -m paper_2607_21224_amd.build` "
             "(the CPDP path has no CPU fallback)")
-    lib = ctypes.CDLL(LIB_PATH)
+    lib = ctypes.CDLL(path)
     vp, i, i64, f = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_float
     lib.cpdp_state_init.argtypes = [vp, vp, vp, vp, vp, i, i64, i64, i, i, i, vp]
     lib.cpdp_local_step.argtypes = [vp, vp, vp, i, i64, i64, i, f, f, i, i, i, vp]
@@ -117,7 +120,7 @@ def _load() -> ctypes.CDLL:
     return lib
 
 
-lib = _load()
+lib = load_library()
 
 
 class CpdpError(RuntimeError):

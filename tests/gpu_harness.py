@@ -175,6 +175,7 @@ def compare(gpu: dict, ref: "oracle.OracleState", param_dt: str, tag: str,
     if velocity_lr is not None:
         gpu = dict(gpu, slow_mom=-velocity_lr * slow_got)
         slow_want = -velocity_lr * slow_want
+    margins = {}
     pairs = [("params", ref.params), ("mom", ref.mom), ("slow_mom", slow_want),
              ("anchor", ref.anchor)]
     if mom2 is not None:
@@ -221,6 +222,7 @@ def compare(gpu: dict, ref: "oracle.OracleState", param_dt: str, tag: str,
         err = np.abs(got[fin] - want[fin])
         atol_f = atol[fin] if isinstance(atol, np.ndarray) else atol
         lim = atol_f + rtol * np.abs(want[fin])
+        margins[name] = float(np.max(err / lim)) if err.size else 0.0
         bad = err > lim
         if bad.any():
             k = np.argmax(err - lim)
@@ -228,6 +230,7 @@ def compare(gpu: dict, ref: "oracle.OracleState", param_dt: str, tag: str,
                 f"{tag} {name}: {int(bad.sum())}/{bad.size} out of tolerance; worst "
                 f"got {got[fin][k]!r} want {want[fin][k]!r} (rtol {rtol}, "
                 f"atol {atol_f[k] if isinstance(atol_f, np.ndarray) else atol_f})")
+    return margins
 
 
 def check_replicas_reconciled(gpu: dict, param_dt: str, tag: str):
@@ -252,16 +255,21 @@ def run_parity(c: Case, idx: np.ndarray | None = None, stream=None):
     refs = {}
     run_oracle(c, sel, lambda s, kind, st, m2: refs.__setitem__(s, (kind, st.copy(), m2)))
     g = GpuRun(c, stream)
+    worst = {}
     for s in range(1, c.steps + 1):
         kind = g.step(s)
         snap = g.snapshot(idx)
         rk, ref, m2 = refs[s]
         assert kind == rk, (s, kind, rk)
         vlr = c.opt32()["lr"] if c.opt is not None and c.opt["kind"] == "adamw" else None
-        compare(snap, ref, c.param_dt, f"step {s} ({kind})", mom2=m2,
-                scaled=c.opt is not None, velocity_lr=vlr,
-                lr=c.opt32()["lr"] if c.opt is not None else c.hyper32()[0])
+        m = compare(snap, ref, c.param_dt, f"step {s} ({kind})", mom2=m2,
+                    scaled=c.opt is not None, velocity_lr=vlr,
+                    lr=c.opt32()["lr"] if c.opt is not None else c.hyper32()[0])
+        for k, v in m.items():
+            worst[k] = max(worst.get(k, 0.0), v)
         if kind == "reconcile" and c.method != "ddp":
             check_replicas_reconciled(snap, c.param_dt, f"step {s}")
-    log(f"[parity] ok: {c.steps} steps")
+    # largest |gpu - ref| / (atol + rtol |ref|) seen per family: 1.0 is the gate
+    log(f"[parity] ok: {c.steps} steps; worst error / tolerance: " +
+        ", ".join(f"{k} {v:.3g}" for k, v in worst.items()))
     return g

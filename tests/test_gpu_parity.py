@@ -22,14 +22,16 @@ def test_tiny_every_coordinate(seed):
     run_parity(case_of("tiny", seed))
 
 
+@pytest.mark.parametrize("seed", [42, 123, 777])
 @pytest.mark.parametrize("name", ["r50_100", "vit_s", "r50_200", "stress"])
-def test_full_size_sampled(name):
+def test_full_size_sampled(name, seed):
     """Full-size workloads in the benchmark's launch configuration, compared
     on both ends (ragged tail included), every tensor boundary and a random
-    sample of coordinates (coordinates are independent)."""
+    sample of coordinates (coordinates are independent), for the three seeds
+    of the paper's runs (Sec. 5.1)."""
     w = WORKLOADS[name]
-    idx = sample_indices(w.P, w.boundaries()[1:], n_random=1 << 15, seed=1)
-    run_parity(case_of(name), idx)
+    idx = sample_indices(w.P, w.boundaries()[1:], n_random=1 << 15, seed=seed)
+    run_parity(case_of(name, seed), idx)
 
 
 SMALL = [
