@@ -130,10 +130,18 @@ class CpdpError(RuntimeError):
 
 
 def _addr(x) -> int | None:
+    """Device address of a buffer argument: None, an integer address, or a
+    tensor.  A tensor must live on the GPU (a host tensor's address would be
+    dereferenced by a kernel) and be contiguous (the ABI's layouts are dense
+    rows of stride ld)."""
     if x is None:
         return None
     if isinstance(x, int):
         return x
+    if not x.is_cuda:
+        raise ValueError(f"CPDP buffers must be device tensors, got one on {x.device}")
+    if not x.is_contiguous():
+        raise ValueError("CPDP buffers must be contiguous tensors")
     return int(x.data_ptr())
 
 

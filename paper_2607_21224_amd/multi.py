@@ -38,8 +38,12 @@ class CpdpMultiState:
 
     def init(self, theta0_list, stream=None) -> None:
         """Algorithm 1 initialisation from per-tensor initial values."""
-        for a, th in zip(self.anchor, theta0_list):
-            a[: th.numel()].copy_(th.float())
+        if len(theta0_list) != self.n:
+            raise ValueError(f"expected {self.n} initial tensors, got {len(theta0_list)}")
+        for t, (a, th) in enumerate(zip(self.anchor, theta0_list)):
+            if th.numel() != self.numels[t]:
+                raise ValueError(f"tensor {t}: {th.numel()} elements, expected {self.numels[t]}")
+            a[: th.numel()].copy_(th.reshape(-1).float())
         torch.cuda.synchronize()
         cpdp.cpdp_state_init_plan(self.plan, stream)
         self.opt_step = 0

@@ -81,7 +81,7 @@ class CpdpState:
 
     def init(self, theta0: torch.Tensor, stream=None) -> None:
         """Algorithm 1 initialisation; theta0 is (P,) in the parameter dtype."""
-        assert theta0.dtype == self.params.dtype and theta0.numel() >= self.P
+        self._check_theta0(theta0)
         cpdp.cpdp_state_init(theta0, self.params, self.mom, self.slow_mom,
                              self.anchor, self.W, self.P, self.ld, self.K,
                              self.param_dt, "f32", stream)
@@ -123,7 +123,7 @@ class CpdpState:
     def init_opt(self, theta0: torch.Tensor, opt: Optimizer, stream=None) -> None:
         """Initialisation for a general optimizer (second-moment buffers for
         AdamW are allocated and zeroed too)."""
-        assert theta0.dtype == self.params.dtype and theta0.numel() >= self.P
+        self._check_theta0(theta0)
         if opt.kind == "adamw" and self.mom2 is None:
             self.mom2 = torch.empty_like(self.mom)
         cpdp.cpdp_state_init_opt(theta0, self.params, self.mom,
@@ -204,7 +204,10 @@ class CpdpState:
 
     def state_dict(self) -> dict:
         """Host copy of the whole CPDP state (replicas, optimizer state, SlowMo
-        state, reference model, step counter), enough to resume bitwise."""
+        state, reference model, step counter), enough to resume bitwise.
+        Waits for all work on the device first, so steps launched on any
+        stream are included."""
+        torch.cuda.synchronize(self.params.device)
         d = {"W": self.W, "P": self.P, "ld": self.ld, "K": self.K,
              "param_dt": self.param_dt, "opt_step": self.opt_step,
              "params": self.params.cpu(), "mom": self.mom.cpu(),
@@ -225,6 +228,20 @@ class CpdpState:
         st.opt_step = int(d["opt_step"])
         return st
 
+    # The ABI takes raw addresses, so these shape checks are what keeps a
+    # kernel inside the caller's buffers: they raise, they are not asserts.
     def _check_grads(self, g: torch.Tensor) -> None:
-        assert g.dtype == torch.float32 and g.is_contiguous()
-        assert g.shape == (self.W, self.ld), (tuple(g.shape), self.W, self.ld)
+        if g.dtype != torch.float32 or not g.is_contiguous():
+            raise ValueError("grads must be a contiguous float32 tensor")
+        if tuple(g.shape) != (self.W, self.ld):
+            raise ValueError(f"grads must have shape {(self.W, self.ld)}, got {tuple(g.shape)}")
+        if g.device != self.params.device:
+            raise ValueError(f"grads are on {g.device}, the state on {self.params.device}")
+
+    def _check_theta0(self, theta0: torch.Tensor) -> None:
+        if theta0.dtype != self.params.dtype or not theta0.is_contiguous():
+            raise ValueError(f"theta0 must be a contiguous {self.params.dtype} tensor")
+        if theta0.numel() < self.P:
+            raise ValueError(f"theta0 has {theta0.numel()} elements, P = {self.P}")
+        if theta0.device != self.params.device:
+            raise ValueError(f"theta0 is on {theta0.device}, the state on {self.params.device}")

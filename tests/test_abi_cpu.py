@@ -360,3 +360,32 @@ def test_plan_step_validation():
     plan.param_dt = 0
     assert cpdp.cpdp_local_step_plan(plan, 2, sgd, check=False) == E.CPDP_ERR_INVALID_ARG
     assert cpdp.cpdp_sync_step_plan(2, plan, 2, sgd, check=False) == E.CPDP_ERR_INVALID_ARG
+
+
+def test_binding_rejects_host_and_strided_tensors():
+    """The binding never hands a kernel a host address or a strided view: a
+    host tensor or a non-contiguous tensor raises before the library is called."""
+    import torch
+    host = torch.zeros(64)
+    with pytest.raises(ValueError, match="device tensors"):
+        cpdp.cpdp_local_step(host, host, host, 1, 64, 64, 1, 0.1, 0.9)
+    with pytest.raises(ValueError, match="device tensors"):
+        cpdp.cpdp_plan_build(cpdp.cpdp_plan(), 1 << 12, 1, 1, [64], [host], [host], None,
+                             [host], None, None)
+
+
+def test_state_checks_shapes_before_the_library():
+    """CpdpState validates buffer shapes, dtypes and devices itself: the ABI
+    takes raw addresses and cannot see a too-small gradient buffer."""
+    import torch
+    from paper_2607_21224_amd.state import CpdpState, Hyper
+    st = CpdpState(2, 8, ld=16, K=2, device="cpu")
+    h = Hyper.fp32(0.1, 0.9, 0.5, 1.0)
+    with pytest.raises(ValueError, match="shape"):
+        st.local_step(torch.zeros(2, 8), h)
+    with pytest.raises(ValueError, match="float32"):
+        st.reconcile(torch.zeros(2, 16, dtype=torch.float64), h)
+    with pytest.raises(ValueError, match="elements"):
+        st.init(torch.zeros(4))
+    with pytest.raises(ValueError, match="device tensors"):  # shapes fine, but host memory
+        st.init(torch.zeros(8))
