@@ -33,9 +33,11 @@ MALL_EVICT_BYTES = 512 << 20  # twice the 256 MB MALL
 
 
 def kernel_source_hash() -> str:
+    """Hash of the sources that decide what the kernels read and write: the
+    kernels with their launch shapes and dispatch, and the launch interface.
+    (Host validation in cpdp_api.cpp does not change a kernel's traffic.)"""
     h = hashlib.sha256()
     for f in ("paper_2607_21224_amd/csrc/cpdp_kernels.hip",
-              "paper_2607_21224_amd/csrc/cpdp_api.cpp",
               "paper_2607_21224_amd/csrc/cpdp_launch.h"):
         h.update(open(os.path.join(ROOT, f), "rb").read())
     return h.hexdigest()[:16]
@@ -153,9 +155,9 @@ def main() -> int:
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: this build runs on exactly one GPU; the multi-GPU "
-              "sharding of the reconcile is described in DESIGN.md but not "
-              f"implemented (asked for --gpus {args.gpus})", file=sys.stderr)
+        print("bench.py: the CPDP path runs on exactly one GPU; sharding the "
+              "reconcile over several GPUs is not implemented "
+              f"(asked for --gpus {args.gpus})", file=sys.stderr)
         return 2
 
     import torch

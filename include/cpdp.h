@@ -313,12 +313,22 @@ int cpdp_period_for_epoch(int64_t epoch, int64_t warmup_epochs, int K);
  * lr = min_lr + (base_lr - min_lr) * (1 + cos(pi * s / S)) / 2 with
  * s = step - warmup_steps, S = max(1, total_steps - warmup_steps)
  * (Sec. 4.3 names cosine annealing with linear warmup; the exact curve is
- * this build's reading).  Host only.  Returns NaN if step < 0,
+ * a reading of that passage).  Host only.  Returns NaN if step < 0,
  * step >= total_steps, warmup_steps < 0, warmup_steps > total_steps,
  * base_lr <= 0, min_lr < 0 or min_lr > base_lr.
  */
 float cpdp_lr_at(int64_t step, int64_t total_steps, int64_t warmup_steps,
                  float base_lr, float min_lr);
+
+/*
+ * Linear learning-rate scaling with the global batch (Sec. 4.3, Sec. 5.3 and
+ * Table 4): lr = base_lr * global_batch / base_batch, computed in double and
+ * rounded to fp32 (Table 4: base 0.1 at a global batch of 256 gives 0.15,
+ * 0.20, 0.30, 0.40 at 384, 512, 768, 1024).  The result is the base_lr a
+ * schedule (cpdp_lr_at) starts from.  Host only.  Returns NaN if base_lr is
+ * not finite and > 0, or either batch is < 1.
+ */
+float cpdp_linear_scaled_lr(float base_lr, int64_t base_batch, int64_t global_batch);
 
 /* Static, human-readable name of a status code (never NULL). */
 const char* cpdp_status_str(int status);

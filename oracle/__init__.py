@@ -296,6 +296,14 @@ def lr_at(step: int, total_steps: int, warmup_steps: int, base_lr: float,
     return min_lr + (base_lr - min_lr) * (1 + math.cos(math.pi * (step - warmup_steps) / S)) / 2
 
 
+def linear_scaled_lr(base_lr: float, base_batch: int, global_batch: int) -> float:
+    """Sec. 4.3 / Sec. 5.3 linear scaling rule: the learning rate grows in
+    proportion to the global batch, base_lr at base_batch.  Returned in double."""
+    if not (base_lr > 0 and base_batch >= 1 and global_batch >= 1):
+        raise ValueError("invalid scaling arguments")
+    return base_lr * global_batch / base_batch
+
+
 def run(theta0, grad_fn, W: int, K: int, n_steps: int, lr, mu: float,
         beta: float, alpha: float, T: int = 0, param_dt="f32", mom_dt="f32",
         aux_dt="f32", callback=None, use=None, method: str = "cpdp") -> OracleState:

@@ -35,7 +35,8 @@ DTYPES = {"f32": CPDP_F32, "bf16": CPDP_BF16}
 EXPORTS = ("cpdp_state_init", "cpdp_local_step", "cpdp_reconcile",
            "cpdp_localsgd_sync", "cpdp_ddp_step", "cpdp_state_init_opt",
            "cpdp_local_step_opt", "cpdp_sync_step_opt", "cpdp_is_sync_step",
-           "cpdp_period_for_epoch", "cpdp_lr_at", "cpdp_plan_bytes", "cpdp_plan_build",
+           "cpdp_period_for_epoch", "cpdp_lr_at", "cpdp_linear_scaled_lr",
+           "cpdp_plan_bytes", "cpdp_plan_build",
            "cpdp_state_init_plan", "cpdp_local_step_plan", "cpdp_sync_step_plan",
            "cpdp_status_str")
 
@@ -111,6 +112,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.cpdp_period_for_epoch.restype = i
     lib.cpdp_lr_at.argtypes = [i64, i64, i64, f, f]
     lib.cpdp_lr_at.restype = f
+    lib.cpdp_linear_scaled_lr.argtypes = [f, i64, i64]
+    lib.cpdp_linear_scaled_lr.restype = f
     lib.cpdp_status_str.argtypes = [i]
     lib.cpdp_status_str.restype = ctypes.c_char_p
     for name in ("cpdp_state_init", "cpdp_local_step", "cpdp_reconcile",
@@ -268,6 +271,16 @@ def cpdp_lr_at(step: int, total_steps: int, warmup_steps: int, base_lr: float,
                        float(min_lr))
     if math.isnan(r):
         raise ValueError("cpdp_lr_at: invalid arguments")
+    return r
+
+
+def cpdp_linear_scaled_lr(base_lr: float, base_batch: int, global_batch: int) -> float:
+    """base_lr scaled linearly with the global batch; raises ValueError on
+    invalid input."""
+    import math
+    r = lib.cpdp_linear_scaled_lr(float(base_lr), int(base_batch), int(global_batch))
+    if math.isnan(r):
+        raise ValueError("cpdp_linear_scaled_lr: invalid arguments")
     return r
 
 

@@ -524,6 +524,12 @@ float cpdp_lr_at(int64_t step, int64_t total_steps, int64_t warmup_steps, float 
     return (float)((double)min_lr + ((double)base_lr - (double)min_lr) * 0.5 * (1.0 + std::cos(pi * frac)));
 }
 
+float cpdp_linear_scaled_lr(float base_lr, int64_t base_batch, int64_t global_batch) {
+    if (!(finite(base_lr) && base_lr > 0.0f) || base_batch < 1 || global_batch < 1)
+        return std::numeric_limits<float>::quiet_NaN();
+    return (float)((double)base_lr * (double)global_batch / (double)base_batch);
+}
+
 const char* cpdp_status_str(int status) {
     switch (status) {
         case CPDP_OK: return "CPDP_OK";

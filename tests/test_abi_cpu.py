@@ -389,3 +389,19 @@ def test_state_checks_shapes_before_the_library():
         st.init(torch.zeros(4))
     with pytest.raises(ValueError, match="device tensors"):  # shapes fine, but host memory
         st.init(torch.zeros(8))
+
+
+def test_linear_scaled_lr_matches_oracle():
+    """cpdp_linear_scaled_lr is the oracle's rule rounded to fp32, for the
+    Table 4 configurations and other batch ratios; invalid input raises."""
+    import numpy as np
+    for base_lr, base, glob in [(0.1, 256, 256), (0.1, 256, 384), (0.1, 256, 512),
+                                (0.1, 256, 768), (0.1, 256, 1024), (5e-4, 64, 1024),
+                                (0.05, 512, 64), (0.1, 3, 7)]:
+        got = cpdp.cpdp_linear_scaled_lr(base_lr, base, glob)
+        want = float(np.float32(oracle.linear_scaled_lr(float(np.float32(base_lr)), base, glob)))
+        assert got == want, (base_lr, base, glob, got, want)
+    for bad in [(0.0, 256, 512), (float("nan"), 256, 512), (0.1, 0, 512), (0.1, 256, 0),
+                (float("inf"), 1, 1), (-0.1, 1, 1)]:
+        with pytest.raises(ValueError):
+            cpdp.cpdp_linear_scaled_lr(*bad)

@@ -66,3 +66,20 @@ def test_lr_schedule_shape():
     assert low < lrs[-1] < low + 1e-3
     with pytest.raises(ValueError):
         oracle.lr_at(total, total, warm, base, low)
+
+
+def test_linear_lr_scaling_reproduces_table4():
+    """The linear scaling rule gives the learning rates Table 4 prints for
+    every intra-site configuration (64 per GPU, 0.1 at a global batch of 256)."""
+    import json
+    import os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden",
+                                    "table4_lr_scaling.json")))
+    for row in g["rows"]:
+        assert row["global_batch"] == 64 * row["gpus"]
+        got = oracle.linear_scaled_lr(g["base_lr"], g["base_batch"], row["global_batch"])
+        assert abs(got - row["lr"]) < 1e-12, row
+    with pytest.raises(ValueError):
+        oracle.linear_scaled_lr(0.0, 256, 512)
+    with pytest.raises(ValueError):
+        oracle.linear_scaled_lr(0.1, 0, 512)
