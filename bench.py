@@ -141,8 +141,10 @@ def main() -> int:
                          "workload; sgd_wd adds weight decay 5e-4; adamw = AdamW "
                          "(lr 5e-4, betas 0.9/0.999, eps 1e-8, weight decay 0.05)")
     ap.add_argument("--graph", action="store_true",
-                    help="also replay the period as one captured HIP graph and time that "
-                         "(SGD only; removes per-launch host overhead, matters for small P)")
+                    help="also replay the period as a captured HIP graph and time that: "
+                         "with the scalars baked in (plain SGD) and with the scalars read "
+                         "from a device step table (any optimizer); removes per-launch "
+                         "host overhead, matters for small P")
     ap.add_argument("--plan", action="store_true",
                     help="hold the model as one allocation per (replica, tensor), as a "
                          "framework does, and drive it through a multi-tensor plan "
@@ -281,11 +283,7 @@ def main() -> int:
     torch.cuda.synchronize()
     copy_gbps = 2 * 4 * n_copy * reps / (c0.elapsed_time(c1) * 1e-3) / 1e9
 
-    graph_ms = None
-    if args.graph:
-        if opt is not None:
-            raise SystemExit("--graph replays fixed-scalar steps: use --optimizer sgd")
-        graph, _ = st.capture_period(grads, h, method=args.method)
+    def time_replays(graph):
         for _ in range(args.warmup):
             graph.replay()
         torch.cuda.synchronize()
@@ -296,7 +294,23 @@ def main() -> int:
             graph.replay()
         g1.record()
         torch.cuda.synchronize()
-        graph_ms = g0.elapsed_time(g1) / args.steps
+        return g0.elapsed_time(g1) / args.steps
+
+    graph_ms = graph_table_ms = None
+    if args.graph:
+        from paper_2607_21224_amd.state import StepTable
+        if opt is None:
+            # scalars baked into the graph (plain momentum SGD)
+            graph, _ = st.capture_period(grads, h, method=args.method)
+            graph_ms = time_replays(graph)
+        # scalars from a device step table: every replay takes the next K entries
+        topt = opt if opt is not None else Optimizer("sgd", h.lr, h.mu)
+        n_entries = w.K * (args.warmup + args.steps)
+        table = StepTable([(topt, st.opt_step + 1 + i, h.beta, h.alpha)
+                           for i in range(n_entries)], device=dev)
+        graph, _ = st.capture_steps(grads, table, method=args.method)
+        graph_table_ms = time_replays(graph)
+        assert table.position() == n_entries
 
     # cold variant for working sets the 256 MB MALL can hold: a 512 MB scratch
     # write (untimed, same stream) before every timed launch evicts the state
@@ -389,6 +403,9 @@ def main() -> int:
         "graph_replay": None if graph_ms is None else {
             "ms_per_step": round(graph_ms, 5),
             "replica_params_per_s": wp * w.K / (graph_ms * 1e-3)},
+        "graph_replay_step_table": None if graph_table_ms is None else {
+            "ms_per_step": round(graph_table_ms, 5),
+            "replica_params_per_s": wp * w.K / (graph_table_ms * 1e-3)},
         "cold": cold,
         "copy_ceiling_GBps": round(copy_gbps, 1),
         "wall_s_timed_region": round(wall, 4),

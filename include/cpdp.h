@@ -288,6 +288,77 @@ int cpdp_sync_step_plan(int strategy, const cpdp_plan* plan, int K,
                         const cpdp_optimizer* opt, float beta, float alpha,
                         unsigned flags, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Step tables.  A training loop changes scalars every step: AdamW's bias
+ * correction uses the step count, and the learning rate follows a schedule
+ * (Sec. 4.3).  The entry points above take those scalars by value, so a HIP
+ * graph captured over them replays the captured values.  A step table holds
+ * the scalars of n_steps consecutive steps in device memory together with a
+ * position word; the *_table entry points read the entry at the position, and
+ * cpdp_step_table_advance moves it on.  A graph that captures a period's
+ * steps and advances therefore runs the next period's scalars on every replay.
+ *
+ * The table's memory is the caller's (cpdp_step_table_bytes bytes, 16-byte
+ * aligned), kept alive while the table is used; cpdp_step_table_fill writes it
+ * once with a synchronous copy and sets the position to 0.  A step whose
+ * position is outside [0, n_steps) (the table is used up) changes nothing;
+ * cpdp_step_table_advance stops at n_steps, where cpdp_step_table_position
+ * reports it.  All steps of a table use one update rule (momentum SGD, SGD
+ * with weight decay, or AdamW), fixed when it is filled.
+ * ------------------------------------------------------------------------ */
+typedef struct cpdp_step_table {
+    void* table;     /* device memory, >= cpdp_step_table_bytes(n_steps)      */
+    int n_steps;     /* filled by cpdp_step_table_fill                        */
+    int update;      /* filled: 0 momentum SGD, 1 SGD with weight decay,
+                        2 AdamW                                               */
+    uint64_t seal;   /* filled: a hash of the fields above; calls on a handle
+                        whose fields changed since return CPDP_ERR_INVALID_ARG */
+} cpdp_step_table;
+
+/* Device bytes of a step table of n_steps entries (0 if n_steps < 1). */
+int64_t cpdp_step_table_bytes(int n_steps);
+
+/*
+ * Fill a step table from host arrays of n_steps entries: opt[s] is the
+ * optimizer of step s (its step field is AdamW's 1-based count for that
+ * step), beta[s] and alpha[s] the SlowMo coefficients of a CPDP sync at that
+ * step (NULL: 0 and 1).  Every entry is validated as cpdp_sync_step_opt
+ * validates its arguments, and all entries must select the same update rule
+ * (CPDP_ERR_INVALID_ARG otherwise).  Scalars are folded exactly as a direct
+ * call folds them, so a table step is bitwise the corresponding direct call.
+ * NULL handle, table or opt: CPDP_ERR_NULL; table not 16-byte aligned:
+ * CPDP_ERR_MISALIGNED; n_steps < 1 or table_bytes too small:
+ * CPDP_ERR_INVALID_ARG.  The copy is synchronous.
+ */
+int cpdp_step_table_fill(cpdp_step_table* t, int64_t table_bytes, int n_steps,
+                         const cpdp_optimizer* opt, const float* beta,
+                         const float* alpha);
+
+/* Set the position (0 <= position <= n_steps) with a one-thread kernel on
+ * `stream` (no memset or copy, so it may be captured in a graph). */
+int cpdp_step_table_set_position(const cpdp_step_table* t, int64_t position,
+                                 void* stream);
+
+/* Advance the position by one (not past n_steps), one-thread kernel. */
+int cpdp_step_table_advance(const cpdp_step_table* t, void* stream);
+
+/* Synchronous read of the position (waits for the device copy; not for use
+ * under graph capture). */
+int cpdp_step_table_position(const cpdp_step_table* t, int64_t* position);
+
+/* cpdp_local_step_opt with the scalars of the table's current entry.  mom2 is
+ * required for an AdamW table.  Does not advance the position. */
+int cpdp_local_step_table(void* params, void* mom, void* mom2, const void* grads,
+                          int W, int64_t P, int64_t ld, int K,
+                          const cpdp_step_table* t, int param_dt, void* stream);
+
+/* cpdp_sync_step_opt with the scalars (and beta, alpha) of the table's
+ * current entry.  Does not advance the position. */
+int cpdp_sync_step_table(int strategy, void* params, void* mom, void* mom2,
+                         void* grads, float* slow_mom, float* anchor, int W,
+                         int64_t P, int64_t ld, int K, const cpdp_step_table* t,
+                         unsigned flags, int param_dt, void* stream);
+
 /*
  * Synchronisation indicator (Sec. 3.2) with the forced synchronisation at the
  * end of an epoch (Sec. 3.1, Sec. 4.2).  Host only, no GPU work.

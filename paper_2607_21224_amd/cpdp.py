@@ -38,7 +38,9 @@ EXPORTS = ("cpdp_state_init", "cpdp_local_step", "cpdp_reconcile",
            "cpdp_period_for_epoch", "cpdp_lr_at", "cpdp_linear_scaled_lr",
            "cpdp_plan_bytes", "cpdp_plan_build",
            "cpdp_state_init_plan", "cpdp_local_step_plan", "cpdp_sync_step_plan",
-           "cpdp_status_str")
+           "cpdp_step_table_bytes", "cpdp_step_table_fill", "cpdp_step_table_set_position",
+           "cpdp_step_table_advance", "cpdp_step_table_position", "cpdp_local_step_table",
+           "cpdp_sync_step_table", "cpdp_status_str")
 
 CPDP_OPT_SGD = 0
 CPDP_OPT_ADAMW = 1
@@ -57,6 +59,12 @@ class cpdp_plan(ctypes.Structure):
                 ("param_dt", ctypes.c_int), ("has_mom2", ctypes.c_int),
                 ("has_slow_mom", ctypes.c_int), ("has_anchor", ctypes.c_int),
                 ("total_chunks", ctypes.c_int64), ("total_numel", ctypes.c_int64),
+                ("seal", ctypes.c_uint64)]
+
+
+class cpdp_step_table(ctypes.Structure):
+    """Mirror of the C struct cpdp_step_table (include/cpdp.h)."""
+    _fields_ = [("table", ctypes.c_void_p), ("n_steps", ctypes.c_int), ("update", ctypes.c_int),
                 ("seal", ctypes.c_uint64)]
 
 
@@ -107,6 +115,20 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.cpdp_local_step_plan.restype = i
     lib.cpdp_sync_step_plan.argtypes = [i, pp, i, op, f, f, ctypes.c_uint, vp]
     lib.cpdp_sync_step_plan.restype = i
+    tp = ctypes.POINTER(cpdp_step_table)
+    lib.cpdp_step_table_bytes.argtypes = [i]
+    lib.cpdp_step_table_bytes.restype = i64
+    lib.cpdp_step_table_fill.argtypes = [tp, i64, i, op, ctypes.POINTER(f), ctypes.POINTER(f)]
+    lib.cpdp_step_table_set_position.argtypes = [tp, i64, vp]
+    lib.cpdp_step_table_advance.argtypes = [tp, vp]
+    lib.cpdp_step_table_position.argtypes = [tp, ctypes.POINTER(i64)]
+    lib.cpdp_local_step_table.argtypes = [vp, vp, vp, vp, i, i64, i64, i, tp, i, vp]
+    lib.cpdp_sync_step_table.argtypes = [i, vp, vp, vp, vp, vp, vp, i, i64, i64, i, tp,
+                                         ctypes.c_uint, i, vp]
+    for name in ("cpdp_step_table_fill", "cpdp_step_table_set_position",
+                 "cpdp_step_table_advance", "cpdp_step_table_position",
+                 "cpdp_local_step_table", "cpdp_sync_step_table"):
+        getattr(lib, name).restype = i
     lib.cpdp_is_sync_step.argtypes = [i64, i, i64]
     lib.cpdp_period_for_epoch.argtypes = [i64, i64, i]
     lib.cpdp_period_for_epoch.restype = i
@@ -330,3 +352,55 @@ def cpdp_sync_step_plan(strategy, plan: cpdp_plan, K, opt, beta=0.0, alpha=1.0, 
     s = lib.cpdp_sync_step_plan(int(strategy), ctypes.byref(plan), int(K), _opt(opt),
                                 float(beta), float(alpha), int(flags), _stream(stream))
     return _done(s, "cpdp_sync_step_plan", check)
+
+
+def cpdp_step_table_bytes(n_steps: int) -> int:
+    return int(lib.cpdp_step_table_bytes(int(n_steps)))
+
+
+def cpdp_step_table_fill(t: cpdp_step_table, table_bytes, opts, betas=None, alphas=None,
+                         check=True):
+    """opts: a sequence of cpdp_optimizer (one per step); betas / alphas:
+    sequences of floats or None."""
+    n = len(opts)
+    arr = (cpdp_optimizer * n)(*opts)
+    fb = (ctypes.c_float * n)(*[float(x) for x in betas]) if betas is not None else None
+    fa = (ctypes.c_float * n)(*[float(x) for x in alphas]) if alphas is not None else None
+    s = lib.cpdp_step_table_fill(ctypes.byref(t), int(table_bytes), n, arr, fb, fa)
+    return _done(s, "cpdp_step_table_fill", check)
+
+
+def cpdp_step_table_set_position(t: cpdp_step_table, position: int, stream=None, check=True):
+    return _done(lib.cpdp_step_table_set_position(ctypes.byref(t), int(position), _stream(stream)),
+                 "cpdp_step_table_set_position", check)
+
+
+def cpdp_step_table_advance(t: cpdp_step_table, stream=None, check=True):
+    return _done(lib.cpdp_step_table_advance(ctypes.byref(t), _stream(stream)),
+                 "cpdp_step_table_advance", check)
+
+
+def cpdp_step_table_position(t: cpdp_step_table) -> int:
+    pos = ctypes.c_int64(-1)
+    _done(lib.cpdp_step_table_position(ctypes.byref(t), ctypes.byref(pos)),
+          "cpdp_step_table_position", True)
+    return int(pos.value)
+
+
+def cpdp_local_step_table(params, mom, mom2, grads, W, P, ld, K, t: cpdp_step_table,
+                          param_dt=CPDP_F32, stream=None, check=True):
+    s = lib.cpdp_local_step_table(_addr(params), _addr(mom), _addr(mom2), _addr(grads), int(W),
+                                  int(P), int(ld), int(K), ctypes.byref(t), _dt(param_dt),
+                                  _stream(stream))
+    return _done(s, "cpdp_local_step_table", check)
+
+
+def cpdp_sync_step_table(strategy, params, mom, mom2, grads, slow_mom, anchor, W, P, ld, K,
+                         t: cpdp_step_table, flags=0, param_dt=CPDP_F32, stream=None,
+                         check=True):
+    strategy = SYNC_KINDS[strategy] if isinstance(strategy, str) else int(strategy)
+    s = lib.cpdp_sync_step_table(strategy, _addr(params), _addr(mom), _addr(mom2),
+                                 _addr(grads), _addr(slow_mom), _addr(anchor), int(W), int(P),
+                                 int(ld), int(K), ctypes.byref(t), int(flags), _dt(param_dt),
+                                 _stream(stream))
+    return _done(s, "cpdp_sync_step_table", check)

@@ -147,6 +147,79 @@ uint64_t plan_seal(const cpdp_plan* p) {
     return h;
 }
 
+// Pointer checks of a local step with a general optimizer (mom2 only for AdamW).
+int check_local_ptrs(void* params, void* mom, void* mom2, const void* grads, int W, int64_t P,
+                     int64_t ld, size_t sp, bool adam) {
+    const void* ptrs[] = {params, mom, grads, mom2};
+    const Range ranges[] = {rows(params, W, P, ld, sp), rows(mom, W, P, ld, 4),
+                            rows(grads, W, P, ld, 4), rows(mom2, W, P, ld, 4)};
+    const size_t row_es[] = {sp, 4, 4, 4};
+    return check_pointers(ptrs, ranges, row_es, adam ? 4 : 3, ld);
+}
+
+// The buffers a synchronisation step of `strategy` reads or writes, checked;
+// on success *slow, *anc and *m2 are the ones the kernels get (NULL when the
+// strategy or update does not use them).
+int check_sync_ptrs(int strategy, bool adam, void* params, void* mom, void* mom2, void* grads,
+                    float* slow_mom, float* anchor, int W, int64_t P, int64_t ld, size_t sp,
+                    float** slow, float** anc, void** m2) {
+    const bool cpdp_sync = strategy == CPDP_SYNC_CPDP;
+    *slow = cpdp_sync ? slow_mom : nullptr;
+    *anc = strategy == CPDP_SYNC_DDP ? nullptr : anchor;
+    *m2 = adam ? mom2 : nullptr;
+    if (cpdp_sync && (slow_mom == nullptr || anchor == nullptr)) return CPDP_ERR_NULL;
+    if (adam && mom2 == nullptr) return CPDP_ERR_NULL;
+    const void* ptrs[6] = {params, mom, grads};
+    Range ranges[6] = {rows(params, W, P, ld, sp), rows(mom, W, P, ld, 4),
+                       rows(grads, W, P, ld, 4)};
+    size_t row_es[6] = {sp, 4, 4};
+    int n = 3;
+    if (*m2) { ptrs[n] = *m2; ranges[n] = rows(*m2, W, P, ld, 4); row_es[n++] = 4; }
+    if (*slow) { ptrs[n] = *slow; ranges[n] = vec(*slow, P, 4); row_es[n++] = 0; }
+    if (*anc) { ptrs[n] = *anc; ranges[n] = vec(*anc, P, 4); row_es[n++] = 0; }
+    return check_pointers(ptrs, ranges, row_es, n, ld);
+}
+
+bool valid_strategy(int strategy) {
+    return strategy == CPDP_SYNC_CPDP || strategy == CPDP_SYNC_LOCALSGD ||
+           strategy == CPDP_SYNC_DDP;
+}
+
+cpdp::Sync sync_mode(int strategy) {
+    return strategy == CPDP_SYNC_CPDP       ? cpdp::Sync::CPDP
+           : strategy == CPDP_SYNC_LOCALSGD ? cpdp::Sync::LocalSGD
+                                            : cpdp::Sync::DDP;
+}
+
+constexpr unsigned kKnownFlags = CPDP_SYNC_WRITE_GRAD_MEAN | CPDP_SYNC_AVERAGE_OPT_STATE;
+
+// Hash of a step-table handle's fields except the seal (same construction as
+// the plan seal).
+uint64_t step_table_seal(const cpdp_step_table* t) {
+    uint64_t h = 0x13198A2E03707344ull;
+    auto mix = [&h](uint64_t x) {
+        h ^= x;
+        h ^= h >> 30;
+        h *= 0xBF58476D1CE4E5B9ull;
+        h ^= h >> 27;
+        h *= 0x94D049BB133111EBull;
+        h ^= h >> 31;
+    };
+    mix(reinterpret_cast<uintptr_t>(t->table));
+    mix((uint64_t)(uint32_t)t->n_steps);
+    mix((uint64_t)(uint32_t)t->update);
+    return h;
+}
+
+// A usable step-table handle: filled by cpdp_step_table_fill and unchanged.
+int check_step_table(const cpdp_step_table* t, cpdp::Opt* kind) {
+    if (t == nullptr || t->table == nullptr) return CPDP_ERR_NULL;
+    if (t->n_steps < 1 || t->update < 0 || t->update > 2) return CPDP_ERR_INVALID_ARG;
+    if (t->seal != step_table_seal(t)) return CPDP_ERR_INVALID_ARG;
+    *kind = t->update == 2 ? cpdp::Opt::ADAMW : t->update == 1 ? cpdp::Opt::SGD_WD : cpdp::Opt::SGD;
+    return CPDP_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -285,11 +358,7 @@ int cpdp_local_step_opt(void* params, void* mom, void* mom2, const void* grads, 
     if (!cpdp::grid_fits(W, P)) return CPDP_ERR_INVALID_ARG;
     const bool adam = kind == cpdp::Opt::ADAMW;
     const size_t sp = esize(param_dt);
-    const void* ptrs[] = {params, mom, grads, mom2};
-    const Range ranges[] = {rows(params, W, P, ld, sp), rows(mom, W, P, ld, 4),
-                            rows(grads, W, P, ld, 4), rows(mom2, W, P, ld, 4)};
-    const size_t row_es[] = {sp, 4, 4, 4};
-    if (int s = check_pointers(ptrs, ranges, row_es, adam ? 4 : 3, ld)) return s;
+    if (int s = check_local_ptrs(params, mom, mom2, grads, W, P, ld, sp, adam)) return s;
     return hip_status(cpdp::launch_local_step(kind, o, param_kind(param_dt), params,
                                               static_cast<float*>(mom),
                                               adam ? static_cast<float*>(mom2) : nullptr,
@@ -301,42 +370,25 @@ int cpdp_sync_step_opt(int strategy, void* params, void* mom, void* mom2, void* 
                        const cpdp_optimizer* opt, float beta, float alpha, unsigned flags,
                        int param_dt, void* stream) {
     if (int s = check_shape(W, P, ld, K)) return s;
-    if (flags & ~(unsigned)(CPDP_SYNC_WRITE_GRAD_MEAN | CPDP_SYNC_AVERAGE_OPT_STATE))
-        return CPDP_ERR_INVALID_ARG;
-    if (strategy != CPDP_SYNC_CPDP && strategy != CPDP_SYNC_LOCALSGD &&
-        strategy != CPDP_SYNC_DDP)
-        return CPDP_ERR_INVALID_ARG;
+    if (flags & ~kKnownFlags) return CPDP_ERR_INVALID_ARG;
+    if (!valid_strategy(strategy)) return CPDP_ERR_INVALID_ARG;
     cpdp::Opt kind;
     cpdp::OptParams o;
     if (int s = make_opt(opt, &kind, &o)) return s;
-    const bool cpdp_sync = strategy == CPDP_SYNC_CPDP;
-    if (cpdp_sync) {
+    if (strategy == CPDP_SYNC_CPDP) {
         if (!(beta >= 0.0f && beta < 1.0f)) return CPDP_ERR_INVALID_ARG;
         if (!(finite(alpha) && alpha > 0.0f)) return CPDP_ERR_INVALID_ARG;
     }
     if (!is_dtype(param_dt)) return CPDP_ERR_DTYPE;
     if (P == 0) return CPDP_OK;
     if (!cpdp::grid_fits(1, P)) return CPDP_ERR_INVALID_ARG;
-    const bool adam = kind == cpdp::Opt::ADAMW;
-    // which optional arguments this strategy / optimizer reads or writes
-    float* slow = cpdp_sync ? slow_mom : nullptr;
-    float* anc = strategy == CPDP_SYNC_DDP ? nullptr : anchor;
-    void* m2 = adam ? mom2 : nullptr;
-    if (cpdp_sync && (slow_mom == nullptr || anchor == nullptr)) return CPDP_ERR_NULL;
-    if (adam && mom2 == nullptr) return CPDP_ERR_NULL;
-    const size_t sp = esize(param_dt);
-    const void* ptrs[6] = {params, mom, grads};
-    Range ranges[6] = {rows(params, W, P, ld, sp), rows(mom, W, P, ld, 4),
-                       rows(grads, W, P, ld, 4)};
-    size_t row_es[6] = {sp, 4, 4};
-    int n = 3;
-    if (m2) { ptrs[n] = m2; ranges[n] = rows(m2, W, P, ld, 4); row_es[n++] = 4; }
-    if (slow) { ptrs[n] = slow; ranges[n] = vec(slow, P, 4); row_es[n++] = 0; }
-    if (anc) { ptrs[n] = anc; ranges[n] = vec(anc, P, 4); row_es[n++] = 0; }
-    if (int s = check_pointers(ptrs, ranges, row_es, n, ld)) return s;
-    const cpdp::Sync mode = cpdp_sync ? cpdp::Sync::CPDP
-                            : strategy == CPDP_SYNC_LOCALSGD ? cpdp::Sync::LocalSGD
-                                                             : cpdp::Sync::DDP;
+    float* slow;
+    float* anc;
+    void* m2;
+    if (int s = check_sync_ptrs(strategy, kind == cpdp::Opt::ADAMW, params, mom, mom2, grads,
+                                slow_mom, anchor, W, P, ld, esize(param_dt), &slow, &anc, &m2))
+        return s;
+    const cpdp::Sync mode = sync_mode(strategy);
     return hip_status(cpdp::launch_sync(mode, kind, o, param_kind(param_dt), params,
                                         static_cast<float*>(mom), static_cast<float*>(m2),
                                         static_cast<const float*>(grads), slow, anc, W, P, ld,
@@ -474,11 +526,8 @@ int cpdp_sync_step_plan(int strategy, const cpdp_plan* plan, int K, const cpdp_o
                         float beta, float alpha, unsigned flags, void* stream) {
     if (int s = check_plan(plan)) return s;
     if (K < 1) return CPDP_ERR_INVALID_ARG;
-    if (strategy != CPDP_SYNC_CPDP && strategy != CPDP_SYNC_LOCALSGD &&
-        strategy != CPDP_SYNC_DDP)
-        return CPDP_ERR_INVALID_ARG;
-    if (flags & ~(unsigned)(CPDP_SYNC_WRITE_GRAD_MEAN | CPDP_SYNC_AVERAGE_OPT_STATE))
-        return CPDP_ERR_INVALID_ARG;
+    if (!valid_strategy(strategy)) return CPDP_ERR_INVALID_ARG;
+    if (flags & ~kKnownFlags) return CPDP_ERR_INVALID_ARG;
     cpdp::Opt kind;
     cpdp::OptParams o;
     if (int s = make_opt(opt, &kind, &o)) return s;
@@ -490,13 +539,112 @@ int cpdp_sync_step_plan(int strategy, const cpdp_plan* plan, int K, const cpdp_o
     if (kind == cpdp::Opt::ADAMW && !plan->has_mom2) return CPDP_ERR_NULL;
     if (int s = check_seal(plan)) return s;
     if (plan->total_chunks == 0) return CPDP_OK;
-    const cpdp::Sync mode = strategy == CPDP_SYNC_CPDP       ? cpdp::Sync::CPDP
-                            : strategy == CPDP_SYNC_LOCALSGD ? cpdp::Sync::LocalSGD
-                                                             : cpdp::Sync::DDP;
-    return hip_status(cpdp::launch_sync_plan(mode, kind, o, param_kind(plan->param_dt),
+    return hip_status(cpdp::launch_sync_plan(sync_mode(strategy), kind, o, param_kind(plan->param_dt),
                                              static_cast<const int64_t*>(plan->table), plan->W,
                                              plan->n_tensors, plan->total_chunks, beta, alpha,
                                              flags, stream));
+}
+
+int64_t cpdp_step_table_bytes(int n_steps) {
+    if (n_steps < 1) return 0;
+    return cpdp::step_table_bytes(n_steps);
+}
+
+int cpdp_step_table_fill(cpdp_step_table* t, int64_t table_bytes, int n_steps,
+                         const cpdp_optimizer* opt, const float* beta, const float* alpha) {
+    if (t == nullptr || t->table == nullptr || opt == nullptr) return CPDP_ERR_NULL;
+    if ((reinterpret_cast<uintptr_t>(t->table) & 15u) != 0) return CPDP_ERR_MISALIGNED;
+    if (n_steps < 1 || n_steps > (1 << 24)) return CPDP_ERR_INVALID_ARG;
+    const int64_t bytes = cpdp::step_table_bytes(n_steps);
+    if (table_bytes < bytes) return CPDP_ERR_INVALID_ARG;
+    std::vector<unsigned char> host((size_t)bytes, 0);
+    int64_t* header = reinterpret_cast<int64_t*>(host.data());
+    header[0] = 0;
+    header[1] = n_steps;
+    auto* entries = reinterpret_cast<cpdp::StepEntry*>(header + cpdp::kStepTableHeaderWords);
+    cpdp::Opt first = cpdp::Opt::SGD;
+    for (int s = 0; s < n_steps; ++s) {
+        cpdp::Opt kind;
+        cpdp::OptParams o;
+        if (int st = make_opt(&opt[s], &kind, &o)) return st;
+        if (s == 0) first = kind;
+        else if (kind != first) return CPDP_ERR_INVALID_ARG;
+        const float b = beta != nullptr ? beta[s] : 0.0f;
+        const float a = alpha != nullptr ? alpha[s] : 1.0f;
+        if (!(b >= 0.0f && b < 1.0f)) return CPDP_ERR_INVALID_ARG;
+        if (!(finite(a) && a > 0.0f)) return CPDP_ERR_INVALID_ARG;
+        entries[s].o = o;
+        entries[s].beta = b;
+        entries[s].alpha_lr = a * o.lr;  // as the direct launch computes it
+    }
+    if (cpdp::upload_bytes(t->table, host.data(), bytes) != 0) return CPDP_ERR_HIP;
+    t->n_steps = n_steps;
+    t->update = first == cpdp::Opt::ADAMW ? 2 : first == cpdp::Opt::SGD_WD ? 1 : 0;
+    t->seal = step_table_seal(t);
+    return CPDP_OK;
+}
+
+int cpdp_step_table_set_position(const cpdp_step_table* t, int64_t position, void* stream) {
+    cpdp::Opt kind;
+    if (int s = check_step_table(t, &kind)) return s;
+    if (position < 0 || position > t->n_steps) return CPDP_ERR_INVALID_ARG;
+    return hip_status(
+        cpdp::launch_step_table_set(static_cast<int64_t*>(t->table), position, stream));
+}
+
+int cpdp_step_table_advance(const cpdp_step_table* t, void* stream) {
+    cpdp::Opt kind;
+    if (int s = check_step_table(t, &kind)) return s;
+    return hip_status(cpdp::launch_step_table_advance(static_cast<int64_t*>(t->table), stream));
+}
+
+int cpdp_step_table_position(const cpdp_step_table* t, int64_t* position) {
+    cpdp::Opt kind;
+    if (int s = check_step_table(t, &kind)) return s;
+    if (position == nullptr) return CPDP_ERR_NULL;
+    return hip_status(
+        cpdp::read_step_table_position(static_cast<const int64_t*>(t->table), position));
+}
+
+int cpdp_local_step_table(void* params, void* mom, void* mom2, const void* grads, int W,
+                          int64_t P, int64_t ld, int K, const cpdp_step_table* t, int param_dt,
+                          void* stream) {
+    if (int s = check_shape(W, P, ld, K)) return s;
+    cpdp::Opt kind;
+    if (int s = check_step_table(t, &kind)) return s;
+    if (!is_dtype(param_dt)) return CPDP_ERR_DTYPE;
+    if (P == 0) return CPDP_OK;
+    if (!cpdp::grid_fits(W, P)) return CPDP_ERR_INVALID_ARG;
+    const bool adam = kind == cpdp::Opt::ADAMW;
+    if (int s = check_local_ptrs(params, mom, mom2, grads, W, P, ld, esize(param_dt), adam))
+        return s;
+    return hip_status(cpdp::launch_local_step_table(
+        kind, param_kind(param_dt), static_cast<const int64_t*>(t->table), params,
+        static_cast<float*>(mom), adam ? static_cast<float*>(mom2) : nullptr,
+        static_cast<const float*>(grads), W, P, ld, stream));
+}
+
+int cpdp_sync_step_table(int strategy, void* params, void* mom, void* mom2, void* grads,
+                         float* slow_mom, float* anchor, int W, int64_t P, int64_t ld, int K,
+                         const cpdp_step_table* t, unsigned flags, int param_dt, void* stream) {
+    if (int s = check_shape(W, P, ld, K)) return s;
+    if (flags & ~kKnownFlags) return CPDP_ERR_INVALID_ARG;
+    if (!valid_strategy(strategy)) return CPDP_ERR_INVALID_ARG;
+    cpdp::Opt kind;
+    if (int s = check_step_table(t, &kind)) return s;
+    if (!is_dtype(param_dt)) return CPDP_ERR_DTYPE;
+    if (P == 0) return CPDP_OK;
+    if (!cpdp::grid_fits(1, P)) return CPDP_ERR_INVALID_ARG;
+    float* slow;
+    float* anc;
+    void* m2;
+    if (int s = check_sync_ptrs(strategy, kind == cpdp::Opt::ADAMW, params, mom, mom2, grads,
+                                slow_mom, anchor, W, P, ld, esize(param_dt), &slow, &anc, &m2))
+        return s;
+    return hip_status(cpdp::launch_sync_table(
+        sync_mode(strategy), kind, param_kind(param_dt), static_cast<const int64_t*>(t->table),
+        params, static_cast<float*>(mom), static_cast<float*>(m2),
+        static_cast<const float*>(grads), slow, anc, W, P, ld, flags, stream));
 }
 
 int cpdp_is_sync_step(int64_t t, int K, int64_t T) {

@@ -75,6 +75,45 @@ int launch_sync_plan(Sync mode, Opt opt, const OptParams& o, Param pt,
                      const int64_t* plan, int W, int n, int64_t total_chunks,
                      float beta, float alpha, unsigned flags, void* stream);
 
+// Step table in device memory: per-step scalars the table kernels read at
+// run time, so a captured graph can replay steps whose scalars differ (AdamW
+// bias correction, a learning-rate schedule).
+//   words [0] position (index of the entry the next step uses)  [1] n_steps
+//   then n_steps StepEntry records
+// A table kernel whose position is outside [0, n_steps) returns without
+// touching anything; the advance kernel stops at n_steps.
+struct StepEntry {
+    OptParams o;         // the update's scalars, folded as for a direct call
+    float beta;          // SlowMo beta (CPDP steps)
+    float alpha_lr;      // alpha * lr, the SlowMo step length
+    float reserved[4];
+};
+static_assert(sizeof(StepEntry) == 64, "step table entries are 64 bytes");
+constexpr int64_t kStepTableHeaderWords = 2;
+inline int64_t step_table_bytes(int n_steps) {
+    return kStepTableHeaderWords * (int64_t)sizeof(int64_t) +
+           (int64_t)n_steps * (int64_t)sizeof(StepEntry);
+}
+
+int launch_local_step_table(Opt opt, Param pt, const int64_t* table, void* params, float* mom,
+                            float* mom2, const float* grads, int W, int64_t P, int64_t ld,
+                            void* stream);
+
+int launch_sync_table(Sync mode, Opt opt, Param pt, const int64_t* table, void* params,
+                      float* mom, float* mom2, const float* grads, float* slow, float* anchor,
+                      int W, int64_t P, int64_t ld, unsigned flags, void* stream);
+
+// One-thread kernels on the table's position word (graph-capturable: no
+// memset, no copy).
+int launch_step_table_set(int64_t* table, int64_t position, void* stream);
+int launch_step_table_advance(int64_t* table, void* stream);
+
+// Synchronous device-to-host read of a table's position word.
+int read_step_table_position(const int64_t* table, int64_t* position);
+
+// Synchronous host-to-device copy of a filled step table.
+int upload_bytes(void* dev, const void* host, int64_t bytes);
+
 // Coordinates one block of the flat and plan kernels covers.
 int64_t coords_per_block();
 

@@ -50,6 +50,32 @@ class Optimizer:
                                    self.weight_decay, int(step))
 
 
+class StepTable:
+    """Per-step scalars of n consecutive steps in device memory (the C ABI's
+    step table).  ``entries`` is a sequence of (Optimizer, step, beta, alpha):
+    the optimizer of that step (its lr from any schedule), AdamW's 1-based
+    step count, and the SlowMo coefficients of a CPDP sync at that step."""
+
+    def __init__(self, entries, device="cuda"):
+        entries = list(entries)
+        self.n = len(entries)
+        nbytes = cpdp.cpdp_step_table_bytes(self.n)
+        if nbytes <= 0:
+            raise ValueError("a step table needs at least one entry")
+        self.buf = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        self.handle = cpdp.cpdp_step_table()
+        self.handle.table = self.buf.data_ptr()
+        cpdp.cpdp_step_table_fill(self.handle, nbytes, [o.c_struct(st) for o, st, _, _ in entries],
+                                  [b for _, _, b, _ in entries], [a for _, _, _, a in entries])
+
+    def set_position(self, position: int = 0, stream=None) -> None:
+        cpdp.cpdp_step_table_set_position(self.handle, position, stream)
+
+    def position(self) -> int:
+        """The entry the next table step uses (synchronous read)."""
+        return cpdp.cpdp_step_table_position(self.handle)
+
+
 class CpdpState:
     """W replicas of a P-coordinate model with per-replica momentum, SlowMo
     velocity u and the reference (anchor) model, all in HBM."""
@@ -174,6 +200,53 @@ class CpdpState:
             return "reconcile"
         self.local_step(grads, h, stream)
         return "local"
+
+    def step_table(self, t: int, grads: torch.Tensor, table: StepTable, T: int = 0,
+                   stream=None, method: str = "cpdp", flags: int = 0) -> str:
+        """Step t of ``method`` with the scalars of the table's current entry,
+        then advance the table (both on ``stream``).  Same cadence and
+        semantics as step_opt; the optimizer state must match the table's
+        update rule (init_opt with an AdamW optimizer for an AdamW table)."""
+        self._check_grads(grads)
+        if method not in self.METHODS:
+            raise ValueError(method)
+        h = table.handle
+        if h.update == 2 and self.mom2 is None:
+            raise ValueError("an AdamW step table needs the state initialised by init_opt(adamw)")
+        mom2 = self.mom2 if h.update == 2 else None
+        if method == "ddp" or cpdp.cpdp_is_sync_step(t, self.K, T):
+            cpdp.cpdp_sync_step_table(method, self.params, self.mom, mom2, grads, self.slow_mom,
+                                      self.anchor, self.W, self.P, self.ld, self.K, h, flags,
+                                      self.param_dt, stream)
+            kind = "reconcile"
+        else:
+            cpdp.cpdp_local_step_table(self.params, self.mom, mom2, grads, self.W, self.P,
+                                       self.ld, self.K, h, self.param_dt, stream)
+            kind = "local"
+        cpdp.cpdp_step_table_advance(h, stream)
+        return kind
+
+    def capture_steps(self, grads: list, table: StepTable, T: int = 0, t0: int = 1,
+                      method: str = "cpdp", flags: int = 0):
+        """Capture steps t0 .. t0+len(grads)-1 (cadence decided now) as table
+        steps into a HIP graph.  Every replay runs them with the table's next
+        len(grads) entries, so a graph of one period replays successive
+        periods of a schedule.  Returns (graph, kinds)."""
+        for g in grads:
+            self._check_grads(g)
+        graph = torch.cuda.CUDAGraph()
+        kinds = []
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            torch.cuda.synchronize()
+            with torch.cuda.graph(graph, stream=side):
+                cs = torch.cuda.current_stream()
+                for j, g in enumerate(grads):
+                    kinds.append(self.step_table(t0 + j, g, table, T, stream=cs, method=method,
+                                                 flags=flags))
+        torch.cuda.current_stream().wait_stream(side)
+        return graph, kinds
 
     # ---- HIP graph capture of a period --------------------------------------------
 

@@ -115,6 +115,58 @@ int main() {
         EXPECT(cpdp_local_step_plan(&plan, 4, &adam, nullptr), CPDP_ERR_NULL, false);
     }
 
+    {
+        // step tables over a fake aligned table address (never dereferenced)
+        const int n = 4;
+        cpdp_optimizer steps[n];
+        for (int s = 0; s < n; ++s) {
+            steps[s] = adam;
+            steps[s].step = s + 1;
+            steps[s].lr = 1e-3f * (float)(s + 1);
+        }
+        const float betas[n] = {0.5f, 0.5f, 0.5f, 0.5f};
+        cpdp_step_table tab = {};
+        const int64_t tb = cpdp_step_table_bytes(n);
+        if (tb != 16 + 64 * n) { std::printf("FAIL step table bytes\n"); ++failures; }
+        EXPECT(cpdp_step_table_fill(&tab, tb, n, steps, betas, nullptr), CPDP_ERR_NULL, false);
+        tab.table = at(9);
+        EXPECT(cpdp_step_table_fill(&tab, tb - 1, n, steps, betas, nullptr), CPDP_ERR_INVALID_ARG, false);
+        EXPECT(cpdp_step_table_fill(&tab, tb, 0, steps, betas, nullptr), CPDP_ERR_INVALID_ARG, false);
+        steps[2].kind = CPDP_OPT_SGD;  // mixed update rules
+        EXPECT(cpdp_step_table_fill(&tab, tb, n, steps, betas, nullptr), CPDP_ERR_INVALID_ARG, false);
+        steps[2].kind = CPDP_OPT_ADAMW;
+        steps[3].step = 0;  // an entry that a direct call would reject
+        EXPECT(cpdp_step_table_fill(&tab, tb, n, steps, betas, nullptr), CPDP_ERR_INVALID_ARG, false);
+        steps[3].step = 4;
+        const float bad_beta[n] = {0.5f, 1.0f, 0.5f, 0.5f};
+        EXPECT(cpdp_step_table_fill(&tab, tb, n, steps, bad_beta, nullptr), CPDP_ERR_INVALID_ARG, false);
+        EXPECT(cpdp_step_table_fill(&tab, tb, n, steps, betas, nullptr), CPDP_OK, false);
+        if (tab.n_steps != n || tab.update != 2) { std::printf("FAIL step table handle\n"); ++failures; }
+        EXPECT(cpdp_local_step_table(pa, mo, m2, gr, W, P, ld, 4, &tab, 0, nullptr), CPDP_OK, true);
+        EXPECT(cpdp_local_step_table(pa, mo, nullptr, gr, W, P, ld, 4, &tab, 0, nullptr), CPDP_ERR_NULL, false);
+        EXPECT(cpdp_sync_step_table(0, pa, mo, m2, gr, u, an, W, P, ld, 4, &tab, 3u, 0, nullptr), CPDP_OK, true);
+        EXPECT(cpdp_sync_step_table(0, pa, mo, m2, gr, nullptr, an, W, P, ld, 4, &tab, 0u, 0, nullptr), CPDP_ERR_NULL, false);
+        EXPECT(cpdp_sync_step_table(1, pa, mo, m2, gr, nullptr, nullptr, W, P, ld, 4, &tab, 0u, 0, nullptr), CPDP_OK, true);
+        EXPECT(cpdp_sync_step_table(5, pa, mo, m2, gr, u, an, W, P, ld, 4, &tab, 0u, 0, nullptr), CPDP_ERR_INVALID_ARG, false);
+        EXPECT(cpdp_sync_step_table(0, pa, mo, m2, gr, u, an, W, P, ld, 4, &tab, 16u, 0, nullptr), CPDP_ERR_INVALID_ARG, false);
+        EXPECT(cpdp_step_table_advance(&tab, nullptr), CPDP_OK, true);
+        EXPECT(cpdp_step_table_set_position(&tab, 0, nullptr), CPDP_OK, true);
+        EXPECT(cpdp_step_table_set_position(&tab, n, nullptr), CPDP_OK, true);
+        EXPECT(cpdp_step_table_set_position(&tab, n + 1, nullptr), CPDP_ERR_INVALID_ARG, false);
+        EXPECT(cpdp_step_table_set_position(&tab, -1, nullptr), CPDP_ERR_INVALID_ARG, false);
+        int64_t pos = -1;
+        EXPECT(cpdp_step_table_position(&tab, &pos), CPDP_OK, false);
+        EXPECT(cpdp_step_table_position(&tab, nullptr), CPDP_ERR_NULL, false);
+        tab.n_steps += 1;  // an edited handle is rejected everywhere
+        EXPECT(cpdp_local_step_table(pa, mo, m2, gr, W, P, ld, 4, &tab, 0, nullptr), CPDP_ERR_INVALID_ARG, false);
+        EXPECT(cpdp_step_table_advance(&tab, nullptr), CPDP_ERR_INVALID_ARG, false);
+        tab.n_steps -= 1;
+        tab.update = 0;
+        EXPECT(cpdp_sync_step_table(0, pa, mo, m2, gr, u, an, W, P, ld, 4, &tab, 0u, 0, nullptr), CPDP_ERR_INVALID_ARG, false);
+        tab.update = 2;
+        EXPECT(cpdp_local_step_table(pa, mo, m2, gr, W, P, ld, 4, &tab, 0, nullptr), CPDP_OK, true);
+    }
+
     EXPECT(cpdp_is_sync_step(4, 4, 0), 1, false);
     EXPECT(cpdp_is_sync_step(3, 4, 0), 0, false);
     EXPECT(cpdp_is_sync_step(0, 4, 0), -CPDP_ERR_INVALID_ARG, false);

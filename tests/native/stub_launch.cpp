@@ -29,6 +29,19 @@ int launch_sync_plan(Sync, Opt, const OptParams&, Param, const int64_t*, int, in
                      float, unsigned, void*) {
     return ++g_launches, 0;
 }
+int launch_local_step_table(Opt, Param, const int64_t*, void*, float*, float*, const float*, int,
+                            int64_t, int64_t, void*) {
+    return ++g_launches, 0;
+}
+int launch_sync_table(Sync, Opt, Param, const int64_t*, void*, float*, float*, const float*,
+                      float*, float*, int, int64_t, int64_t, unsigned, void*) {
+    return ++g_launches, 0;
+}
+int launch_step_table_set(int64_t*, int64_t, void*) { return ++g_launches, 0; }
+int launch_step_table_advance(int64_t*, void*) { return ++g_launches, 0; }
+int read_step_table_position(const int64_t*, int64_t* position) { return *position = 0, 0; }
+int64_t g_uploaded_bytes = 0;
+int upload_bytes(void*, const void*, int64_t bytes) { return g_uploaded_bytes = bytes, 0; }
 int64_t coords_per_block() { return 1024; }
 int g_uploaded_words = 0;
 int upload_plan(void*, const int64_t*, int64_t words) { return g_uploaded_words = (int)words, 0; }
