@@ -171,6 +171,9 @@ def compare(gpu: dict, ref: "oracle.OracleState", param_dt: str, tag: str,
     v = -lr*u (Sec. 3.3) instead of u: with a small lr (AdamW's 5e-4) a
     single one-ulp difference of one fp32 replica moves u by ulp/(W*lr), above
     a 1e-6 relative gate on u, while v is unaffected by the amplification."""
+    if param_dt == "bf16" and velocity_lr is None and not lr:
+        # u = (anchor - avg) / lr: its bf16 flip allowance is divided by lr
+        raise ValueError("compare() of a bf16 run needs lr (or velocity_lr)")
     slow_got, slow_want = gpu["slow_mom"], ref.slow
     if velocity_lr is not None:
         gpu = dict(gpu, slow_mom=-velocity_lr * slow_got)

@@ -11,7 +11,8 @@ from paper_2607_21224_amd.state import CpdpState, Hyper
 
 pytestmark = pytest.mark.gpu
 
-RAGGED = [(W, P) for W in (1, 2, 3, 8, 32) for P in (1, 3, 4, 5, 7, 8, 9, 1023, 1025, 4097)]
+RAGGED = [(W, P) for W in (1, 2, 3, 5, 8, 32)
+          for P in (1, 3, 4, 5, 7, 8, 9, 1023, 1025, 4097, (1 << 20) + 3)]
 
 
 @pytest.mark.parametrize("W,P", RAGGED)
@@ -34,7 +35,7 @@ def test_ragged_sizes_and_pad_canaries(W, P, dt):
     g.grads[:, P:] = canary
     for s in range(1, c.steps + 1):
         g.step(s)
-        compare(g.snapshot(), refs[s], dt, f"W={W} P={P} step {s}")
+        compare(g.snapshot(), refs[s], dt, f"W={W} P={P} step {s}", lr=c.hyper32()[0])
     torch.cuda.synchronize()
     assert (g.st.params[:, P:].float() == -1280.0).all()
     assert (g.st.mom[:, P:] == -1280.0).all()
