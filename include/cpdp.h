@@ -360,6 +360,24 @@ int cpdp_sync_step_table(int strategy, void* params, void* mom, void* mom2,
                          unsigned flags, int param_dt, void* stream);
 
 /*
+ * Failure detection.  Right after a CPDP reconcile or a LocalSGD sync every
+ * replica holds the reference model in the parameter storage type (the
+ * broadcast of Algorithm 1, Sec. 3.3), and the paper relies on exactly that
+ * consistency at every synchronisation and at the epoch end (Sec. 3.1).  This
+ * call counts the coordinates p < P at which at least one replica's stored
+ * parameter differs bitwise from R(anchor) (a NaN matches a NaN); a nonzero
+ * count after a synchronisation means a missed or partial one.
+ *   params [W x ld] param_dt, anchor [P] fp32: read only
+ *   count  device pointer to one uint64, 8-byte aligned: overwritten (a
+ *          one-thread kernel zeroes it first, so the call may be captured in
+ *          a graph); read it after synchronising the stream.
+ * Validation as cpdp_reconcile for the arguments it shares.
+ */
+int cpdp_count_unsynced(const void* params, const float* anchor, int W,
+                        int64_t P, int64_t ld, int param_dt, uint64_t* count,
+                        void* stream);
+
+/*
  * Synchronisation indicator (Sec. 3.2) with the forced synchronisation at the
  * end of an epoch (Sec. 3.1, Sec. 4.2).  Host only, no GPU work.
  *   t: 1-based step counter inside the epoch; K: period (>= 1);

@@ -40,7 +40,7 @@ EXPORTS = ("cpdp_state_init", "cpdp_local_step", "cpdp_reconcile",
            "cpdp_state_init_plan", "cpdp_local_step_plan", "cpdp_sync_step_plan",
            "cpdp_step_table_bytes", "cpdp_step_table_fill", "cpdp_step_table_set_position",
            "cpdp_step_table_advance", "cpdp_step_table_position", "cpdp_local_step_table",
-           "cpdp_sync_step_table", "cpdp_status_str")
+           "cpdp_sync_step_table", "cpdp_count_unsynced", "cpdp_status_str")
 
 CPDP_OPT_SGD = 0
 CPDP_OPT_ADAMW = 1
@@ -129,6 +129,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                  "cpdp_step_table_advance", "cpdp_step_table_position",
                  "cpdp_local_step_table", "cpdp_sync_step_table"):
         getattr(lib, name).restype = i
+    lib.cpdp_count_unsynced.argtypes = [vp, vp, i, i64, i64, i, vp, vp]
+    lib.cpdp_count_unsynced.restype = i
     lib.cpdp_is_sync_step.argtypes = [i64, i, i64]
     lib.cpdp_period_for_epoch.argtypes = [i64, i64, i]
     lib.cpdp_period_for_epoch.restype = i
@@ -404,3 +406,13 @@ def cpdp_sync_step_table(strategy, params, mom, mom2, grads, slow_mom, anchor, W
                                  int(ld), int(K), ctypes.byref(t), int(flags), _dt(param_dt),
                                  _stream(stream))
     return _done(s, "cpdp_sync_step_table", check)
+
+
+def cpdp_count_unsynced(params, anchor, W, P, ld, count, param_dt=CPDP_F32, stream=None,
+                        check=True):
+    """Enqueue the count of coordinates where some replica differs from the
+    reference model (stored type, bitwise) into ``count`` (a device uint64 /
+    int64 tensor of one element)."""
+    s = lib.cpdp_count_unsynced(_addr(params), _addr(anchor), int(W), int(P), int(ld),
+                                _dt(param_dt), _addr(count), _stream(stream))
+    return _done(s, "cpdp_count_unsynced", check)

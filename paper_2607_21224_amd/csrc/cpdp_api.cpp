@@ -647,6 +647,26 @@ int cpdp_sync_step_table(int strategy, void* params, void* mom, void* mom2, void
         static_cast<const float*>(grads), slow, anc, W, P, ld, flags, stream));
 }
 
+int cpdp_count_unsynced(const void* params, const float* anchor, int W, int64_t P, int64_t ld,
+                        int param_dt, uint64_t* count, void* stream) {
+    if (int s = check_shape(W, P, ld, 1)) return s;
+    if (!is_dtype(param_dt)) return CPDP_ERR_DTYPE;
+    if (count == nullptr) return CPDP_ERR_NULL;
+    if ((reinterpret_cast<uintptr_t>(count) & 7u) != 0) return CPDP_ERR_MISALIGNED;
+    if (!cpdp::grid_fits(1, P)) return CPDP_ERR_INVALID_ARG;
+    if (P > 0) {
+        const size_t sp = esize(param_dt);
+        const void* ptrs[] = {params, anchor, count};
+        const Range ranges[] = {rows(params, W, P, ld, sp), vec(anchor, P, 4), vec(count, 1, 8)};
+        const size_t row_es[] = {sp, 0, 0};
+        if (int s = check_pointers(ptrs, ranges, row_es, 2, ld)) return s;
+        // the count may not lie inside either input
+        if (overlap(ranges[2], ranges[0]) || overlap(ranges[2], ranges[1])) return CPDP_ERR_OVERLAP;
+    }
+    return hip_status(cpdp::launch_count_unsynced(param_kind(param_dt), params, anchor, W, P, ld,
+                                                  count, stream));
+}
+
 int cpdp_is_sync_step(int64_t t, int K, int64_t T) {
     if (t < 1 || K < 1 || T < 0 || (T > 0 && t > T)) return -CPDP_ERR_INVALID_ARG;
     return (t % K == 0 || (T > 0 && t == T)) ? 1 : 0;

@@ -114,6 +114,12 @@ int read_step_table_position(const int64_t* table, int64_t* position);
 // Synchronous host-to-device copy of a filled step table.
 int upload_bytes(void* dev, const void* host, int64_t bytes);
 
+// Zero *count, then add the number of coordinates p < P at which some
+// replica's stored parameter differs bitwise from the anchor rounded to the
+// parameter storage type.
+int launch_count_unsynced(Param pt, const void* params, const float* anchor, int W, int64_t P,
+                          int64_t ld, uint64_t* count, void* stream);
+
 // Coordinates one block of the flat and plan kernels covers.
 int64_t coords_per_block();
 

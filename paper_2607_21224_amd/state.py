@@ -100,6 +100,7 @@ class CpdpState:
         self.anchor = torch.empty(max(self.P, 1), dtype=torch.float32, device=device)
         self.mom2 = None          # AdamW second moments, allocated by init_opt
         self.opt_step = 0         # optimizer updates applied (AdamW bias correction)
+        self._count = None        # device word of count_unsynced
 
     @property
     def torch_param_dtype(self):
@@ -247,6 +248,21 @@ class CpdpState:
                                                  flags=flags))
         torch.cuda.current_stream().wait_stream(side)
         return graph, kinds
+
+    def count_unsynced(self, stream=None) -> int:
+        """Coordinates at which some replica does not hold the reference model
+        (bitwise, in the parameter storage type).  0 right after every CPDP or
+        LocalSGD synchronisation; anything else is a missed or partial sync.
+        Synchronises the stream to read the result."""
+        if self._count is None:
+            self._count = torch.zeros(1, dtype=torch.int64, device=self.params.device)
+        cpdp.cpdp_count_unsynced(self.params, self.anchor, self.W, self.P, self.ld, self._count,
+                                 self.param_dt, stream)
+        if stream is not None:
+            stream.synchronize()
+        else:
+            torch.cuda.synchronize(self.params.device)
+        return int(self._count.item())
 
     # ---- HIP graph capture of a period --------------------------------------------
 

@@ -167,6 +167,18 @@ int main() {
         EXPECT(cpdp_local_step_table(pa, mo, m2, gr, W, P, ld, 4, &tab, 0, nullptr), CPDP_OK, true);
     }
 
+    {
+        uint64_t* cnt = static_cast<uint64_t*>(at(10));
+        EXPECT(cpdp_count_unsynced(pa, an, W, P, ld, 0, cnt, nullptr), CPDP_OK, true);
+        EXPECT(cpdp_count_unsynced(pa, an, W, 0, ld, 0, cnt, nullptr), CPDP_OK, true);  // zeroes the count
+        EXPECT(cpdp_count_unsynced(pa, an, W, P, ld, 0, nullptr, nullptr), CPDP_ERR_NULL, false);
+        EXPECT(cpdp_count_unsynced(pa, nullptr, W, P, ld, 0, cnt, nullptr), CPDP_ERR_NULL, false);
+        EXPECT(cpdp_count_unsynced(pa, an, W, P, ld, 0, reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(cnt) + 4), nullptr), CPDP_ERR_MISALIGNED, false);
+        EXPECT(cpdp_count_unsynced(pa, an, W, P, ld, 0, reinterpret_cast<uint64_t*>(an), nullptr), CPDP_ERR_OVERLAP, false);
+        EXPECT(cpdp_count_unsynced(pa, an, W, P, P - 1, 0, cnt, nullptr), CPDP_ERR_INVALID_ARG, false);
+        EXPECT(cpdp_count_unsynced(pa, an, W, P, ld, 3, cnt, nullptr), CPDP_ERR_DTYPE, false);
+    }
+
     EXPECT(cpdp_is_sync_step(4, 4, 0), 1, false);
     EXPECT(cpdp_is_sync_step(3, 4, 0), 0, false);
     EXPECT(cpdp_is_sync_step(0, 4, 0), -CPDP_ERR_INVALID_ARG, false);

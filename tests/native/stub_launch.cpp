@@ -42,6 +42,10 @@ int launch_step_table_advance(int64_t*, void*) { return ++g_launches, 0; }
 int read_step_table_position(const int64_t*, int64_t* position) { return *position = 0, 0; }
 int64_t g_uploaded_bytes = 0;
 int upload_bytes(void*, const void*, int64_t bytes) { return g_uploaded_bytes = bytes, 0; }
+int launch_count_unsynced(Param, const void*, const float*, int, int64_t, int64_t, uint64_t*,
+                          void*) {
+    return ++g_launches, 0;
+}
 int64_t coords_per_block() { return 1024; }
 int g_uploaded_words = 0;
 int upload_plan(void*, const int64_t*, int64_t words) { return g_uploaded_words = (int)words, 0; }
