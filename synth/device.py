@@ -35,6 +35,13 @@ def lib():
     return _lib
 
 
+def _check_f32_device(x, name: str) -> None:
+    """The kernels write through the raw address: only a contiguous fp32
+    tensor on the GPU may reach them."""
+    if x.dtype != torch.float32 or not x.is_contiguous() or not x.is_cuda:
+        raise ValueError(f"{name} must be a contiguous float32 GPU tensor")
+
+
 def _stream(s):
     if s is None:
         return None
@@ -46,9 +53,12 @@ def fill_normal(out, P: int, seed: int, kind: int, t: int, sigma: float,
                 stream=None) -> None:
     """Fill out[:, :P] (a contiguous (rows, ld) fp32 CUDA tensor) with stream
     key(seed, kind, t, row) draws."""
-    assert out.dtype == torch.float32 and out.is_contiguous()
+    _check_f32_device(out, "out")
+    if out.dim() not in (1, 2):
+        raise ValueError("out must be a (ld,) or (rows, ld) tensor")
     rows, ld = (out.shape[0], out.shape[1]) if out.dim() == 2 else (1, out.shape[0])
-    assert P <= ld
+    if not 0 <= P <= ld:
+        raise ValueError(f"P = {P} does not fit rows of {ld}")
     r = lib().synth_fill_normal(out.data_ptr(), rows, P, ld, seed, kind, t, sigma,
                                 gen.outlier_threshold(outlier_rate), outlier_scale,
                                 _stream(stream))
@@ -68,6 +78,11 @@ def fill_grads(out, P: int, seed: int, step: int, sigma: float = 1e-3,
 
 
 def copy_f32(dst, src, n: int, stream=None) -> None:
+    _check_f32_device(dst, "dst")
+    _check_f32_device(src, "src")
+    if not 0 <= n <= min(dst.numel(), src.numel()):
+        raise ValueError(f"copy of {n} elements between tensors of {src.numel()} and "
+                         f"{dst.numel()}")
     r = lib().synth_copy_f32(dst.data_ptr(), src.data_ptr(), n, _stream(stream))
     if r != 0:
         raise RuntimeError(f"synth_copy_f32 failed ({r})")

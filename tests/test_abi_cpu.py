@@ -405,3 +405,14 @@ def test_linear_scaled_lr_matches_oracle():
                 (float("inf"), 1, 1), (-0.1, 1, 1)]:
         with pytest.raises(ValueError):
             cpdp.cpdp_linear_scaled_lr(*bad)
+
+
+def test_synth_device_wrappers_reject_host_and_small_tensors():
+    """The device input generator and copy kernel never receive a host
+    address or a size beyond the tensors (checked before the library)."""
+    import torch
+    from synth import device as sdev
+    with pytest.raises(ValueError, match="GPU tensor"):
+        sdev.fill_grads(torch.zeros(2, 16), 16, 1, 1)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        sdev.copy_f32(torch.zeros(4), torch.zeros(4), 4)
