@@ -34,12 +34,14 @@ MALL_EVICT_BYTES = 512 << 20  # twice the 256 MB MALL
 
 def kernel_source_hash() -> str:
     """Hash of the sources that decide what the kernels read and write: the
-    kernels with their launch shapes and dispatch, and the launch interface.
-    (Host validation in cpdp_api.cpp does not change a kernel's traffic.)"""
+    kernel translation units with their launch shapes and dispatch, the
+    shared device code and the launch interface.  (Host validation in
+    cpdp_api.cpp does not change a kernel's traffic.)"""
+    from paper_2607_21224_amd.build import KERNEL_HEADERS, KERNEL_SOURCES
     h = hashlib.sha256()
-    for f in ("paper_2607_21224_amd/csrc/cpdp_kernels.hip",
-              "paper_2607_21224_amd/csrc/cpdp_launch.h"):
-        h.update(open(os.path.join(ROOT, f), "rb").read())
+    csrc = os.path.join(ROOT, "paper_2607_21224_amd", "csrc")
+    for f in (*KERNEL_SOURCES, *KERNEL_HEADERS):
+        h.update(open(os.path.join(csrc, f), "rb").read())
     return h.hexdigest()[:16]
 
 

@@ -18,9 +18,20 @@ LIB_SYNTH = os.path.join(ROOT, "synth", "libsynth.so")
 
 # -ffp-contract=off: only the explicit fmaf calls fuse, so the arithmetic is
 # exactly what the source says.  Packed fp32 instructions are disabled.
-HIP_FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
-             "-ffp-contract=off", "-Xclang", "-target-feature", "-Xclang",
-             "-packed-fp32-ops", "-Wall", "-Wno-unused-command-line-argument"]
+COMPILE_FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
+                 "-ffp-contract=off", "-Xclang", "-target-feature", "-Xclang",
+                 "-packed-fp32-ops", "-Wall", "-Wno-unused-command-line-argument"]
+HIP_FLAGS = COMPILE_FLAGS + ["-shared"]
+
+# the kernel translation units of libcpdp.so (compiled in parallel) and the
+# host validation layer
+KERNEL_SOURCES = ("kernels_flat.hip", "kernels_sync_cpdp.hip", "kernels_sync_localsgd.hip",
+                  "kernels_sync_ddp.hip", "kernels_plan.hip", "kernels_table.hip",
+                  "kernels_check.hip")
+# headers the kernel sources include (part of what the recorded traffic is for)
+KERNEL_HEADERS = ("cpdp_device.h", "cpdp_sync_impl.h", "cpdp_launch.h")
+HOST_SOURCES = ("cpdp_api.cpp",)
+OBJ_ROOT = os.path.join(ROOT, "_build")
 
 
 def _run(cmd):
@@ -30,11 +41,22 @@ def _run(cmd):
 
 
 def build_cpdp(out: str = LIB_CPDP, extra=()) -> str:
+    from concurrent.futures import ThreadPoolExecutor
     csrc = os.path.join(PKG, "csrc")
+    objdir = os.path.join(OBJ_ROOT, os.path.basename(out) + ".objs")
+    os.makedirs(objdir, exist_ok=True)
+    sources = KERNEL_SOURCES + HOST_SOURCES
+
+    def compile_one(name):
+        obj = os.path.join(objdir, name + ".o")
+        _run([HIPCC, *COMPILE_FLAGS, *extra, "-I", os.path.join(ROOT, "include"), "-I", csrc,
+              "-c", "-o", obj, os.path.join(csrc, name)])
+        return obj
+
+    with ThreadPoolExecutor(len(sources)) as ex:
+        objs = list(ex.map(compile_one, sources))
     tmp = out + ".tmp"
-    _run([HIPCC, *HIP_FLAGS, *extra, "-I", os.path.join(ROOT, "include"), "-I", csrc,
-          "-o", tmp, os.path.join(csrc, "cpdp_kernels.hip"),
-          os.path.join(csrc, "cpdp_api.cpp")])
+    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs])
     os.replace(tmp, out)
     return out
 

@@ -1,5 +1,5 @@
 // Internal interface between the C ABI (cpdp_api.cpp: validation, dispatch)
-// and the gfx950 kernels (cpdp_kernels.hip).  Plain C++ types only, so the
+// and the gfx950 kernels (kernels_*.hip).  Plain C++ types only, so the
 // validation layer builds with any host compiler.  Every launcher assumes its
 // arguments were validated (P > 0, aligned, non-overlapping) and returns 0 on
 // success or the HIP error code of a failed launch.
@@ -53,6 +53,14 @@ int launch_sync(Sync mode, Opt opt, const OptParams& o, Param pt, void* params,
                 float* mom, float* mom2, const float* grads, float* slow,
                 float* anchor, int W, int64_t P, int64_t ld, float beta,
                 float alpha, unsigned flags, void* stream);
+
+// launch_sync for one strategy; each is instantiated in its own translation
+// unit (kernels_sync_<strategy>.hip).
+template <Sync M>
+int launch_sync_mode(Opt opt, const OptParams& o, Param pt, void* params, float* mom,
+                     float* mom2, const float* grads, float* slow, float* anchor, int W,
+                     int64_t P, int64_t ld, float beta, float alpha, unsigned flags,
+                     void* stream);
 
 // Multi-tensor plan table in device memory, as 64-bit words:
 //   [0] W  [1] n  [2] total chunks  [3] reserved

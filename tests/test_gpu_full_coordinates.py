@@ -1,6 +1,7 @@
 """Every coordinate of the ResNet-50/CIFAR-100-sized workload (W=8,
-P=23,712,932 in 161 tensors, K=4) for one whole period (three local steps and
-the reconcile) against the oracle, in the benchmark's launch configuration.
+P=23,712,932 in 161 tensors, K=4) and of the ViT-S-sized one (W=8,
+P=21,332,068, K=4) for one whole period (three local steps and the reconcile)
+against the oracle, in the benchmark's launch configuration.
 
 Inputs come from the seeded generator: on the device for the HIP path, copied
 to the host for the oracle (the generator is the one module both sides share;
@@ -18,8 +19,9 @@ from synth import device as sdev
 pytestmark = pytest.mark.gpu
 
 
-def test_r50_100_one_period_every_coordinate():
-    w = WORKLOADS["r50_100"]
+@pytest.mark.parametrize("name", ["r50_100", "vit_s"])
+def test_one_period_every_coordinate(name):
+    w = WORKLOADS[name]
     c = Case(W=w.W, P=w.P, K=w.K, lr=w.lr, mu=w.mu, beta=w.beta, alpha=w.alpha, steps=w.K,
              ld=w.ld, seed=42)
     P, W = c.P, c.W
@@ -52,8 +54,8 @@ def test_r50_100_one_period_every_coordinate():
             oracle.local_step(ref, g64, lr, mu)
         del g64
         snap = g.snapshot()
-        m = compare(snap, ref, "f32", f"r50_100 every coordinate, step {s} ({kind})", lr=lr)
+        m = compare(snap, ref, "f32", f"{name} every coordinate, step {s} ({kind})", lr=lr)
         del snap
-        log(f"[full-coords] step {s} {kind}: {W}x{P} coordinates match; worst error / "
+        log(f"[full-coords] {name} step {s} {kind}: {W}x{P} coordinates match; worst error / "
             f"tolerance " + ", ".join(f"{k} {v:.3g}" for k, v in m.items()))
     assert kind == "reconcile"
