@@ -359,6 +359,15 @@ int cpdp_sync_step_table(int strategy, void* params, void* mom, void* mom2,
                          int64_t P, int64_t ld, int K, const cpdp_step_table* t,
                          unsigned flags, int param_dt, void* stream);
 
+/* cpdp_local_step_plan / cpdp_sync_step_plan with the scalars (and beta,
+ * alpha) of a step table's current entry; the update rule is the table's.
+ * An AdamW table needs a plan with mom2.  Do not advance the position. */
+int cpdp_local_step_plan_table(const cpdp_plan* plan, int K,
+                               const cpdp_step_table* t, void* stream);
+int cpdp_sync_step_plan_table(int strategy, const cpdp_plan* plan, int K,
+                              const cpdp_step_table* t, unsigned flags,
+                              void* stream);
+
 /*
  * Failure detection.  Right after a CPDP reconcile or a LocalSGD sync every
  * replica holds the reference model in the parameter storage type (the

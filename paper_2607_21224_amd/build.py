@@ -26,10 +26,10 @@ HIP_FLAGS = COMPILE_FLAGS + ["-shared"]
 # the kernel translation units of libcpdp.so (compiled in parallel) and the
 # host validation layer
 KERNEL_SOURCES = ("kernels_flat.hip", "kernels_sync_cpdp.hip", "kernels_sync_localsgd.hip",
-                  "kernels_sync_ddp.hip", "kernels_plan.hip", "kernels_table.hip",
-                  "kernels_check.hip")
+                  "kernels_sync_ddp.hip", "kernels_plan.hip", "kernels_plan_table.hip",
+                  "kernels_table.hip", "kernels_check.hip")
 # headers the kernel sources include (part of what the recorded traffic is for)
-KERNEL_HEADERS = ("cpdp_device.h", "cpdp_sync_impl.h", "cpdp_launch.h")
+KERNEL_HEADERS = ("cpdp_device.h", "cpdp_sync_impl.h", "cpdp_plan_impl.h", "cpdp_launch.h")
 HOST_SOURCES = ("cpdp_api.cpp",)
 OBJ_ROOT = os.path.join(ROOT, "_build")
 

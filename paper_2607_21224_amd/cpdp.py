@@ -40,7 +40,8 @@ EXPORTS = ("cpdp_state_init", "cpdp_local_step", "cpdp_reconcile",
            "cpdp_state_init_plan", "cpdp_local_step_plan", "cpdp_sync_step_plan",
            "cpdp_step_table_bytes", "cpdp_step_table_fill", "cpdp_step_table_set_position",
            "cpdp_step_table_advance", "cpdp_step_table_position", "cpdp_local_step_table",
-           "cpdp_sync_step_table", "cpdp_count_unsynced", "cpdp_status_str")
+           "cpdp_sync_step_table", "cpdp_local_step_plan_table", "cpdp_sync_step_plan_table",
+           "cpdp_count_unsynced", "cpdp_status_str")
 
 CPDP_OPT_SGD = 0
 CPDP_OPT_ADAMW = 1
@@ -129,6 +130,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                  "cpdp_step_table_advance", "cpdp_step_table_position",
                  "cpdp_local_step_table", "cpdp_sync_step_table"):
         getattr(lib, name).restype = i
+    lib.cpdp_local_step_plan_table.argtypes = [pp, i, tp, vp]
+    lib.cpdp_local_step_plan_table.restype = i
+    lib.cpdp_sync_step_plan_table.argtypes = [i, pp, i, tp, ctypes.c_uint, vp]
+    lib.cpdp_sync_step_plan_table.restype = i
     lib.cpdp_count_unsynced.argtypes = [vp, vp, i, i64, i64, i, vp, vp]
     lib.cpdp_count_unsynced.restype = i
     lib.cpdp_is_sync_step.argtypes = [i64, i, i64]
@@ -416,3 +421,17 @@ def cpdp_count_unsynced(params, anchor, W, P, ld, count, param_dt=CPDP_F32, stre
     s = lib.cpdp_count_unsynced(_addr(params), _addr(anchor), int(W), int(P), int(ld),
                                 _dt(param_dt), _addr(count), _stream(stream))
     return _done(s, "cpdp_count_unsynced", check)
+
+
+def cpdp_local_step_plan_table(plan: cpdp_plan, K, t: cpdp_step_table, stream=None, check=True):
+    s = lib.cpdp_local_step_plan_table(ctypes.byref(plan), int(K), ctypes.byref(t),
+                                       _stream(stream))
+    return _done(s, "cpdp_local_step_plan_table", check)
+
+
+def cpdp_sync_step_plan_table(strategy, plan: cpdp_plan, K, t: cpdp_step_table, flags=0,
+                              stream=None, check=True):
+    strategy = SYNC_KINDS[strategy] if isinstance(strategy, str) else int(strategy)
+    s = lib.cpdp_sync_step_plan_table(int(strategy), ctypes.byref(plan), int(K),
+                                      ctypes.byref(t), int(flags), _stream(stream))
+    return _done(s, "cpdp_sync_step_plan_table", check)

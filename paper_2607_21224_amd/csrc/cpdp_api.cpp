@@ -647,6 +647,39 @@ int cpdp_sync_step_table(int strategy, void* params, void* mom, void* mom2, void
         static_cast<const float*>(grads), slow, anc, W, P, ld, flags, stream));
 }
 
+int cpdp_local_step_plan_table(const cpdp_plan* plan, int K, const cpdp_step_table* t,
+                               void* stream) {
+    if (int s = check_plan(plan)) return s;
+    if (K < 1) return CPDP_ERR_INVALID_ARG;
+    cpdp::Opt kind;
+    if (int s = check_step_table(t, &kind)) return s;
+    if (kind == cpdp::Opt::ADAMW && !plan->has_mom2) return CPDP_ERR_NULL;
+    if (int s = check_seal(plan)) return s;
+    if (plan->total_chunks == 0) return CPDP_OK;
+    return hip_status(cpdp::launch_local_step_plan_table(
+        kind, param_kind(plan->param_dt), static_cast<const int64_t*>(plan->table), plan->W,
+        plan->n_tensors, plan->total_chunks, static_cast<const int64_t*>(t->table), stream));
+}
+
+int cpdp_sync_step_plan_table(int strategy, const cpdp_plan* plan, int K,
+                              const cpdp_step_table* t, unsigned flags, void* stream) {
+    if (int s = check_plan(plan)) return s;
+    if (K < 1) return CPDP_ERR_INVALID_ARG;
+    if (!valid_strategy(strategy)) return CPDP_ERR_INVALID_ARG;
+    if (flags & ~kKnownFlags) return CPDP_ERR_INVALID_ARG;
+    cpdp::Opt kind;
+    if (int s = check_step_table(t, &kind)) return s;
+    if (strategy == CPDP_SYNC_CPDP && (!plan->has_slow_mom || !plan->has_anchor))
+        return CPDP_ERR_NULL;
+    if (kind == cpdp::Opt::ADAMW && !plan->has_mom2) return CPDP_ERR_NULL;
+    if (int s = check_seal(plan)) return s;
+    if (plan->total_chunks == 0) return CPDP_OK;
+    return hip_status(cpdp::launch_sync_plan_table(
+        sync_mode(strategy), kind, param_kind(plan->param_dt),
+        static_cast<const int64_t*>(plan->table), plan->W, plan->n_tensors, plan->total_chunks,
+        static_cast<const int64_t*>(t->table), flags, stream));
+}
+
 int cpdp_count_unsynced(const void* params, const float* anchor, int W, int64_t P, int64_t ld,
                         int param_dt, uint64_t* count, void* stream) {
     if (int s = check_shape(W, P, ld, 1)) return s;

@@ -477,6 +477,25 @@ __device__ __forceinline__ bool step_entry(const int64_t* table, StepEntry& e) {
     return true;
 }
 
+// Where a step's scalars come from: the launch arguments, or the entry at the
+// position of a device step table (no entry when the table is used up).
+struct DirectScalars {
+    OptParams o;
+    float beta;
+    float alpha_lr;
+    __device__ __forceinline__ bool get(StepEntry& e) const {
+        e.o = o;
+        e.beta = beta;
+        e.alpha_lr = alpha_lr;
+        return true;
+    }
+};
+
+struct TableScalars {
+    const int64_t* table;
+    __device__ __forceinline__ bool get(StepEntry& e) const { return step_entry(table, e); }
+};
+
 // ---- launch helpers -------------------------------------------------------------
 
 inline int64_t blocks_for(int64_t P) { return (P + (int64_t)kBlock * kVec - 1) / ((int64_t)kBlock * kVec); }

@@ -111,6 +111,13 @@ int launch_sync_table(Sync mode, Opt opt, Param pt, const int64_t* table, void* 
                       float* mom, float* mom2, const float* grads, float* slow, float* anchor,
                       int W, int64_t P, int64_t ld, unsigned flags, void* stream);
 
+// Plan steps with the scalars of a step table's current entry.
+int launch_local_step_plan_table(Opt opt, Param pt, const int64_t* plan, int W, int n,
+                                 int64_t total_chunks, const int64_t* table, void* stream);
+int launch_sync_plan_table(Sync mode, Opt opt, Param pt, const int64_t* plan, int W, int n,
+                           int64_t total_chunks, const int64_t* table, unsigned flags,
+                           void* stream);
+
 // One-thread kernels on the table's position word (graph-capturable: no
 // memset, no copy).
 int launch_step_table_set(int64_t* table, int64_t position, void* stream);

@@ -60,6 +60,39 @@ class CpdpMultiState:
         cpdp.cpdp_local_step_plan(self.plan, self.K, c, stream)
         return "local"
 
+    def step_table(self, t: int, table, T: int = 0, stream=None, method: str = "cpdp",
+                   flags: int = 0) -> str:
+        """Step t on self.grads with the scalars of the step table's current
+        entry, then advance the table (see CpdpState.step_table)."""
+        h = table.handle
+        if method == "ddp" or cpdp.cpdp_is_sync_step(t, self.K, T):
+            cpdp.cpdp_sync_step_plan_table(method, self.plan, self.K, h, flags, stream)
+            kind = "reconcile"
+        else:
+            cpdp.cpdp_local_step_plan_table(self.plan, self.K, h, stream)
+            kind = "local"
+        cpdp.cpdp_step_table_advance(h, stream)
+        return kind
+
+    def capture_steps(self, n_steps: int, table, T: int = 0, t0: int = 1,
+                      method: str = "cpdp", flags: int = 0):
+        """Capture steps t0 .. t0+n_steps-1 (cadence decided now) as table
+        steps on self.grads into a HIP graph; every replay runs them with the
+        table's next n_steps entries.  Returns (graph, kinds)."""
+        graph = torch.cuda.CUDAGraph()
+        kinds = []
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            torch.cuda.synchronize()
+            with torch.cuda.graph(graph, stream=side):
+                cs = torch.cuda.current_stream()
+                for j in range(n_steps):
+                    kinds.append(self.step_table(t0 + j, table, T, stream=cs, method=method,
+                                                 flags=flags))
+        torch.cuda.current_stream().wait_stream(side)
+        return graph, kinds
+
     def sgd(self, h: Hyper) -> Optimizer:
         return Optimizer("sgd", h.lr, h.mu)
 

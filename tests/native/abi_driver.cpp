@@ -165,6 +165,40 @@ int main() {
         EXPECT(cpdp_sync_step_table(0, pa, mo, m2, gr, u, an, W, P, ld, 4, &tab, 0u, 0, nullptr), CPDP_ERR_INVALID_ARG, false);
         tab.update = 2;
         EXPECT(cpdp_local_step_table(pa, mo, m2, gr, W, P, ld, 4, &tab, 0, nullptr), CPDP_OK, true);
+
+        // plans driven by the step table
+        const int nt = 2;
+        const int64_t numel[nt] = {100, 7};
+        void* tp[W * nt];
+        void* tm[W * nt];
+        void* tv[W * nt];
+        void* tg[W * nt];
+        float* ts[nt];
+        float* ta[nt];
+        int k = 64;
+        auto far = [&](void) { return reinterpret_cast<void*>((uintptr_t)(1ull << 44) + ((uintptr_t)(k++) << 24)); };
+        for (int j = 0; j < W * nt; ++j) { tp[j] = far(); tm[j] = far(); tv[j] = far(); tg[j] = far(); }
+        for (int j = 0; j < nt; ++j) { ts[j] = static_cast<float*>(far()); ta[j] = static_cast<float*>(far()); }
+        cpdp_plan plan = {};
+        plan.table = at(11);
+        EXPECT(cpdp_plan_build(&plan, cpdp_plan_bytes(W, nt), W, nt, numel, tp, tm, tv, tg, ts, ta, 0), CPDP_OK, false);
+        EXPECT(cpdp_local_step_plan_table(&plan, 4, &tab, nullptr), CPDP_OK, true);
+        EXPECT(cpdp_sync_step_plan_table(0, &plan, 4, &tab, 3u, nullptr), CPDP_OK, true);
+        EXPECT(cpdp_sync_step_plan_table(2, &plan, 4, &tab, 0u, nullptr), CPDP_OK, true);
+        EXPECT(cpdp_sync_step_plan_table(4, &plan, 4, &tab, 0u, nullptr), CPDP_ERR_INVALID_ARG, false);
+        EXPECT(cpdp_sync_step_plan_table(0, &plan, 4, &tab, 64u, nullptr), CPDP_ERR_INVALID_ARG, false);
+        EXPECT(cpdp_local_step_plan_table(&plan, 0, &tab, nullptr), CPDP_ERR_INVALID_ARG, false);
+        EXPECT(cpdp_local_step_plan_table(&plan, 4, nullptr, nullptr), CPDP_ERR_NULL, false);
+        tab.n_steps += 1;
+        EXPECT(cpdp_local_step_plan_table(&plan, 4, &tab, nullptr), CPDP_ERR_INVALID_ARG, false);
+        tab.n_steps -= 1;
+        plan.W += 1;
+        EXPECT(cpdp_sync_step_plan_table(1, &plan, 4, &tab, 0u, nullptr), CPDP_ERR_INVALID_ARG, false);
+        plan.W -= 1;
+        // an AdamW table needs the plan's second moments; CPDP needs u and anchor
+        EXPECT(cpdp_plan_build(&plan, cpdp_plan_bytes(W, nt), W, nt, numel, tp, tm, nullptr, tg, nullptr, nullptr, 0), CPDP_OK, false);
+        EXPECT(cpdp_local_step_plan_table(&plan, 4, &tab, nullptr), CPDP_ERR_NULL, false);
+        EXPECT(cpdp_sync_step_plan_table(0, &plan, 4, &tab, 0u, nullptr), CPDP_ERR_NULL, false);
     }
 
     {

@@ -37,6 +37,14 @@ int launch_sync_table(Sync, Opt, Param, const int64_t*, void*, float*, float*, c
                       float*, float*, int, int64_t, int64_t, unsigned, void*) {
     return ++g_launches, 0;
 }
+int launch_local_step_plan_table(Opt, Param, const int64_t*, int, int, int64_t, const int64_t*,
+                                 void*) {
+    return ++g_launches, 0;
+}
+int launch_sync_plan_table(Sync, Opt, Param, const int64_t*, int, int, int64_t, const int64_t*,
+                           unsigned, void*) {
+    return ++g_launches, 0;
+}
 int launch_step_table_set(int64_t*, int64_t, void*) { return ++g_launches, 0; }
 int launch_step_table_advance(int64_t*, void*) { return ++g_launches, 0; }
 int read_step_table_position(const int64_t*, int64_t* position) { return *position = 0, 0; }

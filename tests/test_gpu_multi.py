@@ -106,3 +106,63 @@ def test_plan_ragged_matches_oracle(method, kind, dt, flags):
                                      for i in range(W)]).astype(np.float64)
         compare(snap, ref, dt, f"{method} {kind} step {s}", mom2=m2 if kind == "adamw" else None,
                 scaled=True, velocity_lr=opt.lr if kind == "adamw" else None, lr=opt.lr)
+
+
+@pytest.mark.parametrize("method,flags", [("cpdp", 0), ("cpdp", 3), ("localsgd", 0), ("ddp", 1)])
+def test_plan_with_step_table(method, flags):
+    """Plan steps driven by a step table (AdamW, warmup + cosine lr) are
+    bitwise the plan steps with the scalars passed directly; a HIP graph of one
+    period of table steps, replayed for successive periods, is bitwise the
+    eager loop."""
+    from paper_2607_21224_amd import cpdp
+    from paper_2607_21224_amd.state import StepTable
+    from synth import device as sdev
+    W, K, periods = 5, 3, 3
+    n = K * periods
+    beta, alpha = 0.5, 0.75
+    opts = [Optimizer("adamw", cpdp.cpdp_lr_at(s, n, K, 5e-4, 5e-5), 0.9, 0.999, 1e-8, 0.05)
+            for s in range(n)]
+    log(f"[plan-table] {method} flags={flags} W={W} K={K} periods={periods}")
+    states = [CpdpMultiState(W, NUMELS, K, adamw=True) for _ in range(3)]
+    offs = np.cumsum([0] + NUMELS)
+    th = torch.from_numpy(gen.theta0(13, np.arange(sum(NUMELS)))).cuda()
+    for st in states:
+        st.init([th[offs[t]:offs[t + 1]] for t in range(len(NUMELS))])
+    direct, tabled, graphed = states
+    t_eager = StepTable([(opts[s], s + 1, beta, alpha) for s in range(n)])
+    t_graph = StepTable([(opts[s], s + 1, beta, alpha) for s in range(n)])
+    graph, kinds = graphed.capture_steps(K, t_graph, method=method, flags=flags)
+    g = torch.empty((W, max(sum(NUMELS), 1)), device="cuda")
+
+    def load_grads(st):
+        for i in range(W):
+            for t in range(len(NUMELS)):
+                if NUMELS[t]:
+                    st.grads[i][t][:NUMELS[t]].copy_(g[i, offs[t]:offs[t + 1]])
+
+    def same(a, b, tag):
+        for fam in ("params", "mom", "mom2"):
+            for i in range(W):
+                x, y = a.gather(fam, i), b.gather(fam, i)
+                assert torch.equal(x.view(torch.int32), y.view(torch.int32)), (tag, fam, i)
+        for fam in ("slow_mom", "anchor"):
+            assert torch.equal(a.gather(fam).view(torch.int32), b.gather(fam).view(torch.int32)), \
+                (tag, fam)
+
+    for r in range(periods):
+        # one gradient set per period: the graph reads the same buffers at every step
+        sdev.fill_grads(g, sum(NUMELS), 13, r + 1, 1e-3, 0.0)
+        for st in states:
+            load_grads(st)
+        graph.replay()
+        for j in range(K):
+            s = r * K + j + 1
+            ka = direct.step(s, opts[s - 1], beta, alpha, 0, method=method, flags=flags)
+            kb = tabled.step_table(s, t_eager, method=method, flags=flags)
+            assert ka == kb == kinds[j]
+            torch.cuda.synchronize()
+            same(direct, tabled, f"step {s}")
+        # every state steps on its own copy of the period's gradients, which the
+        # write-back variant overwrites with their mean at each sync, identically
+        same(direct, graphed, f"period {r + 1}")
+    assert t_eager.position() == n and t_graph.position() == n
