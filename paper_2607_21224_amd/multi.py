@@ -93,6 +93,47 @@ class CpdpMultiState:
         torch.cuda.current_stream().wait_stream(side)
         return graph, kinds
 
+    # ---- checkpoint / resume ---------------------------------------------------
+
+    FAMILIES = ("params", "mom", "mom2", "grads", "slow_mom", "anchor")
+
+    def state_dict(self) -> dict:
+        """Host copy of every tensor of the state (and the optimizer step
+        count), enough to resume bitwise.  Waits for all device work first."""
+        torch.cuda.synchronize()
+        d = {"W": self.W, "numels": list(self.numels), "K": self.K, "param_dt": self.param_dt,
+             "opt_step": self.opt_step}
+        for fam in self.FAMILIES:
+            src = getattr(self, fam)
+            if src is None:
+                continue
+            if fam in ("slow_mom", "anchor"):
+                d[fam] = [x.cpu() for x in src]
+            else:
+                d[fam] = [[x.cpu() for x in row] for row in src]
+        return d
+
+    def load_state_dict(self, d: dict) -> None:
+        """Copy a state_dict into this state's tensors in place (the plan keeps
+        pointing at them).  Shapes, replica count and types must match."""
+        if (d["W"], list(d["numels"]), d["param_dt"]) != (self.W, self.numels, self.param_dt):
+            raise ValueError("state_dict is for a different model layout")
+        if ("mom2" in d) != (self.mom2 is not None):
+            raise ValueError("state_dict and state differ in AdamW second moments")
+        for fam in self.FAMILIES:
+            dst = getattr(self, fam)
+            if dst is None:
+                continue
+            if fam in ("slow_mom", "anchor"):
+                for x, y in zip(dst, d[fam]):
+                    x.copy_(y)
+            else:
+                for row_x, row_y in zip(dst, d[fam]):
+                    for x, y in zip(row_x, row_y):
+                        x.copy_(y)
+        self.opt_step = int(d["opt_step"])
+        torch.cuda.synchronize()
+
     def sgd(self, h: Hyper) -> Optimizer:
         return Optimizer("sgd", h.lr, h.mu)
 

@@ -166,3 +166,39 @@ def test_plan_with_step_table(method, flags):
         # write-back variant overwrites with their mean at each sync, identically
         same(direct, graphed, f"period {r + 1}")
     assert t_eager.position() == n and t_graph.position() == n
+
+
+def test_plan_checkpoint_resume_bitwise():
+    """Two periods, save, load into a fresh state, two more periods: bitwise
+    the four periods run straight (AdamW, so the step count is resumed too)."""
+    W, K = 4, 3
+    opt = Optimizer("adamw", 5e-4, 0.9, 0.999, 1e-8, 0.05)
+    offs = np.cumsum([0] + NUMELS)
+    th = torch.from_numpy(gen.theta0(21, np.arange(sum(NUMELS)))).cuda()
+    a = CpdpMultiState(W, NUMELS, K, adamw=True)
+    b = CpdpMultiState(W, NUMELS, K, adamw=True)
+    for st in (a, b):
+        st.init([th[offs[t]:offs[t + 1]] for t in range(len(NUMELS))])
+
+    def run(st, steps):
+        for s in steps:
+            g = torch.from_numpy(gen.grads(21, s, W, np.arange(sum(NUMELS)))).cuda()
+            for i in range(W):
+                for t in range(len(NUMELS)):
+                    if NUMELS[t]:
+                        st.grads[i][t][:NUMELS[t]].copy_(g[i, offs[t]:offs[t + 1]])
+            st.step(s, opt, 0.5, 1.0)
+        torch.cuda.synchronize()
+
+    run(a, range(1, 2 * K + 1))
+    saved = a.state_dict()
+    c = CpdpMultiState(W, NUMELS, K, adamw=True)
+    c.load_state_dict(saved)
+    run(c, range(2 * K + 1, 4 * K + 1))
+    run(b, range(1, 4 * K + 1))
+    for fam in ("params", "mom", "mom2"):
+        for i in range(W):
+            assert torch.equal(b.gather(fam, i).view(torch.int32), c.gather(fam, i).view(torch.int32)), (fam, i)
+    for fam in ("slow_mom", "anchor"):
+        assert torch.equal(b.gather(fam).view(torch.int32), c.gather(fam).view(torch.int32)), fam
+    assert c.opt_step == b.opt_step == 4 * K
