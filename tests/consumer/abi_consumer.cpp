@@ -3,15 +3,19 @@
 // (initialisation, then local steps and reconciles on the host cadence of
 // cpdp_is_sync_step) on inputs read from files and writes the final state.
 //
-// usage: abi_consumer W P K steps T lr mu beta alpha param_dt dir
+// usage: abi_consumer W P K steps T lr mu beta alpha param_dt dir [periods]
 //   dir/theta0.bin        P parameters (fp32, or raw bf16 bits when param_dt = 1)
 //   dir/grads_<s>.bin     W x P fp32 gradients of step s = 1..steps, replica-major
 // writes dir/params.bin (W x P, parameter storage), dir/mom.bin (W x P fp32),
 // dir/slow.bin and dir/anchor.bin (P fp32) and dir/kinds.txt (one line per step).
 // Rows are padded to ld = P rounded up to 64 elements; the padding is filled
 // with a byte pattern before the run and checked untouched afterwards.
+// With a trailing `periods` argument it then times that many further periods
+// on the last gradients and prints the host time per C-ABI call (validation
+// and enqueue, no synchronisation) and the device time per period.
 #include <hip/hip_runtime.h>
 
+#include <chrono>
 #include <cstdint>
 #include <cstdio>
 #include <cstdlib>
@@ -58,10 +62,12 @@ static bool write_file(const std::string& path, const void* src, size_t bytes) {
 static constexpr unsigned char kPad = 0x5A;
 
 int main(int argc, char** argv) {
-    if (argc != 12) {
-        std::fprintf(stderr, "usage: %s W P K steps T lr mu beta alpha param_dt dir\n", argv[0]);
+    if (argc != 12 && argc != 13) {
+        std::fprintf(stderr, "usage: %s W P K steps T lr mu beta alpha param_dt dir [periods]\n",
+                     argv[0]);
         return 2;
     }
+    const int time_periods = argc == 13 ? std::atoi(argv[12]) : 0;
     const int W = std::atoi(argv[1]);
     const int64_t P = std::atoll(argv[2]);
     const int K = std::atoi(argv[3]);
@@ -124,6 +130,41 @@ int main(int argc, char** argv) {
                                      CPDP_F32, CPDP_F32, stream));
         HIP_OK(hipStreamSynchronize(stream));
         kinds += sync ? "reconcile\n" : "local\n";
+    }
+
+    if (time_periods > 0) {
+        hipEvent_t e0, e1;
+        HIP_OK(hipEventCreate(&e0));
+        HIP_OK(hipEventCreate(&e1));
+        double host_s = 0.0;
+        int64_t calls = 0;
+        HIP_OK(hipEventRecord(e0, stream));
+        for (int r = 0; r < time_periods; ++r) {
+            for (int t = 1; t <= K; ++t) {
+                const auto h0 = std::chrono::steady_clock::now();
+                const int sync = cpdp_is_sync_step(t, K, 0);
+                const int st = sync ? cpdp_reconcile(d_params, d_mom, d_grads, d_slow, d_anchor, W,
+                                                     P, ld, K, lr, mu, beta, alpha, pdt, CPDP_F32,
+                                                     CPDP_F32, stream)
+                                    : cpdp_local_step(d_params, d_mom, d_grads, W, P, ld, K, lr,
+                                                      mu, pdt, CPDP_F32, CPDP_F32, stream);
+                host_s += std::chrono::duration<double>(std::chrono::steady_clock::now() - h0).count();
+                ++calls;
+                if (st != CPDP_OK) {
+                    std::fprintf(stderr, "timed call failed: %s\n", cpdp_status_str(st));
+                    return 1;
+                }
+            }
+        }
+        HIP_OK(hipEventRecord(e1, stream));
+        HIP_OK(hipEventSynchronize(e1));
+        float ms = 0.0f;
+        HIP_OK(hipEventElapsedTime(&ms, e0, e1));
+        std::printf("timing: %d periods of K=%d, host %.2f us per call (cadence, validation, "
+                    "enqueue), device %.2f us per period\n",
+                    time_periods, K, 1e6 * host_s / (double)calls, 1e3 * ms / time_periods);
+        HIP_OK(hipEventDestroy(e0));
+        HIP_OK(hipEventDestroy(e1));
     }
 
     std::vector<unsigned char> params(W * ld * ps);
