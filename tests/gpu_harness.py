@@ -221,7 +221,9 @@ def compare(gpu: dict, ref: "oracle.OracleState", param_dt: str, tag: str,
                 atol = atol + flip
         nan_g, nan_w = np.isnan(got), np.isnan(want)
         assert np.array_equal(nan_g, nan_w), f"{tag} {name}: NaN positions differ"
-        fin = ~nan_w
+        inf_w = np.isinf(want)
+        assert np.array_equal(got[inf_w], want[inf_w]), f"{tag} {name}: infinities differ"
+        fin = ~(nan_w | inf_w)
         err = np.abs(got[fin] - want[fin])
         atol_f = atol[fin] if isinstance(atol, np.ndarray) else atol
         lim = atol_f + rtol * np.abs(want[fin])
