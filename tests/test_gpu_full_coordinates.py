@@ -1,7 +1,9 @@
 """Every coordinate of the ResNet-50/CIFAR-100-sized workload (W=8,
-P=23,712,932 in 161 tensors, K=4) and of the ViT-S-sized one (W=8,
-P=21,332,068, K=4) for one whole period (three local steps and the reconcile)
-against the oracle, in the benchmark's launch configuration.
+P=23,712,932 in 161 tensors, K=4), of the ViT-S-sized one (W=8,
+P=21,332,068, K=4) and of the ResNet-50/TinyImageNet-sized one (W=16,
+P=23,917,832, K=8, gradients with 1 % outliers x100) for one whole period
+(K-1 local steps and the reconcile) against the oracle, in the benchmark's
+launch configuration.
 
 Inputs come from the seeded generator: on the device for the HIP path, copied
 to the host for the oracle (the generator is the one module both sides share;
@@ -19,11 +21,11 @@ from synth import device as sdev
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("name", ["r50_100", "vit_s"])
+@pytest.mark.parametrize("name", ["r50_100", "vit_s", "r50_200"])
 def test_one_period_every_coordinate(name):
     w = WORKLOADS[name]
     c = Case(W=w.W, P=w.P, K=w.K, lr=w.lr, mu=w.mu, beta=w.beta, alpha=w.alpha, steps=w.K,
-             ld=w.ld, seed=42)
+             ld=w.ld, seed=42, outlier_rate=w.outlier_rate)
     P, W = c.P, c.W
     lr, mu, beta, alpha = c.hyper32()
     rng = np.random.default_rng(0)
