@@ -60,9 +60,17 @@ def recorded_traffic(kernel: str, workload: str, variant: str = ""):
     return rec.get("bytes_per_launch")
 
 
-def _oracle_slice(w, start: int, n: int, budget_s: float) -> dict:
+# optimizer descriptors of --optimizer, as bench.py passes them to the GPU path
+OPTIMIZERS = {"sgd_wd": dict(kind="sgd", weight_decay=5e-4),
+              "adamw": dict(kind="adamw", lr=5e-4, momentum=0.9, beta2=0.999, eps=1e-8,
+                            weight_decay=0.05)}
+
+
+def _oracle_slice(w, start: int, n: int, budget_s: float, method: str = "cpdp",
+                  optimizer: str = "sgd") -> dict:
     """Whole periods of the oracle on coordinates [start, start + n) (mod P)
-    until budget_s has elapsed; returns counts and per-kind times."""
+    until budget_s has elapsed, for the strategy and optimizer being
+    benchmarked; returns counts and per-kind times."""
     import numpy as np
     import oracle
     from synth import gen
@@ -74,19 +82,41 @@ def _oracle_slice(w, start: int, n: int, budget_s: float) -> dict:
     grads = [gen.grads(42, s, w.W, idx, w.grad_sigma, w.outlier_rate).astype(np.float64)
              for s in range(1, w.K + 1)]
     st = oracle.state_init(th0, w.W, w.param_dt)
+    mom2 = np.zeros((w.W, n))
+    o = OPTIMIZERS.get(optimizer)
+    if o is None:
+        make = None
+    elif o["kind"] == "sgd":
+        make = lambda t: oracle.sgd(lr, mu, f(o["weight_decay"]))  # noqa: E731
+    else:
+        make = lambda t: oracle.adamw(f(o["lr"]), f(o["momentum"]), f(o["beta2"]),  # noqa: E731
+                                      f(o["eps"]), f(o["weight_decay"]), t)
     out = {"periods": 0, "rec_s": 0.0, "rec_n": 0, "loc_s": 0.0, "loc_n": 0}
+    t_global = 0
     t0 = time.perf_counter()
     while True:
         for s in range(1, w.K + 1):
+            t_global += 1
+            g = grads[s - 1]
+            sync = method == "ddp" or oracle.is_sync_step(s, w.K)
             c0 = time.perf_counter()
-            if oracle.is_sync_step(s, w.K):
-                oracle.reconcile(st, grads[s - 1], lr, mu, beta, alpha)
-                out["rec_s"] += time.perf_counter() - c0
-                out["rec_n"] += 1
+            if make is not None:
+                if sync:
+                    oracle.sync_opt(st, method, g, make(t_global), beta, alpha, mom2)
+                else:
+                    oracle.local_step_opt(st, g, make(t_global), mom2)
+            elif not sync:
+                oracle.local_step(st, g, lr, mu)
+            elif method == "cpdp":
+                oracle.reconcile(st, g, lr, mu, beta, alpha)
+            elif method == "localsgd":
+                oracle.localsgd_sync(st, g, lr, mu)
             else:
-                oracle.local_step(st, grads[s - 1], lr, mu)
-                out["loc_s"] += time.perf_counter() - c0
-                out["loc_n"] += 1
+                oracle.ddp_step(st, g, lr, mu)
+            dt = time.perf_counter() - c0
+            key = "rec" if sync else "loc"
+            out[key + "_s"] += dt
+            out[key + "_n"] += 1
         out["periods"] += 1
         out["elapsed"] = time.perf_counter() - t0
         if out["elapsed"] >= budget_s:
@@ -94,7 +124,8 @@ def _oracle_slice(w, start: int, n: int, budget_s: float) -> dict:
 
 
 def cpu_baseline(w, budget_s: float = 10.0, n_coords: int = 1 << 18,
-                 parallel_budget_s: float = 5.0) -> dict:
+                 parallel_budget_s: float = 5.0, method: str = "cpdp",
+                 optimizer: str = "sgd") -> dict:
     """The oracle as it stands on the first n_coords coordinates of the
     workload (coordinates are independent), repeating whole periods until
     budget_s has elapsed, on one thread.  A second leg runs the same oracle
@@ -103,13 +134,14 @@ def cpu_baseline(w, budget_s: float = 10.0, n_coords: int = 1 << 18,
     from concurrent.futures import ThreadPoolExecutor
 
     n = min(n_coords, w.P)
-    r = _oracle_slice(w, 0, n, budget_s)
+    r = _oracle_slice(w, 0, n, budget_s, method, optimizer)
     el = r["elapsed"]
     scale = w.P / n  # per-call seconds extrapolated to the whole workload
     out = {"value": w.W * n * w.K * r["periods"] / el, "unit": "replica-params/s",
            "cores": 1, "kind": "oracle",
            "sample": f"first {n} of {w.P} coordinates of {w.name}, W={w.W}, "
-                     f"{r['periods']} periods of K={w.K} steps, fp64 C oracle, 1 thread, "
+                     f"{r['periods']} periods of K={w.K} steps ({method}, {optimizer}), "
+                     f"fp64 C oracle, 1 thread, "
                      f"{el:.1f} s",
            "s_per_reconcile_full_P": round(r["rec_s"] / max(r["rec_n"], 1) * scale, 4),
            "s_per_local_step_full_P": (round(r["loc_s"] / r["loc_n"] * scale, 4)
@@ -119,7 +151,8 @@ def cpu_baseline(w, budget_s: float = 10.0, n_coords: int = 1 << 18,
         threads = max(1, min(16, len(os.sched_getaffinity(0))))
         with ThreadPoolExecutor(threads) as ex:
             t0 = time.perf_counter()
-            parts = list(ex.map(lambda k: _oracle_slice(w, k * n, n, parallel_budget_s),
+            parts = list(ex.map(lambda k: _oracle_slice(w, k * n, n, parallel_budget_s,
+                                                        method, optimizer),
                                 range(threads)))
             wall = time.perf_counter() - t0
         done = sum(p["periods"] for p in parts)
@@ -194,10 +227,12 @@ def main() -> int:
             sdev.fill_grads(g, w.P, 42, s, w.grad_sigma, w.outlier_rate, stream=stream)
             grads.append(g)
         opt = None
-        if args.optimizer == "sgd_wd":
-            opt = Optimizer("sgd", h.lr, h.mu, weight_decay=5e-4)
-        elif args.optimizer == "adamw":
-            opt = Optimizer("adamw", 5e-4, 0.9, 0.999, 1e-8, 0.05)
+        if args.optimizer != "sgd":
+            o = dict(OPTIMIZERS[args.optimizer])
+            kind = o.pop("kind")
+            if kind == "sgd":  # the workload's learning rate and momentum, plus decay
+                o.update(lr=h.lr, momentum=h.mu)
+            opt = Optimizer(kind, **o)
         multi = None
         if args.plan:
             from paper_2607_21224_amd.multi import CpdpMultiState
@@ -414,7 +449,8 @@ def main() -> int:
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget,
-                                           parallel_budget_s=args.cpu_budget / 2)
+                                           parallel_budget_s=args.cpu_budget / 2,
+                                           method=args.method, optimizer=args.optimizer)
     print(json.dumps(out), flush=True)
     return 0
 
