@@ -6,7 +6,7 @@ from __future__ import annotations
 import torch
 
 from . import cpdp
-from .state import Hyper, Optimizer
+from .state import Hyper, Optimizer, _on
 
 
 class CpdpMultiState:
@@ -45,7 +45,7 @@ class CpdpMultiState:
                 raise ValueError(f"tensor {t}: {th.numel()} elements, expected {self.numels[t]}")
             a[: th.numel()].copy_(th.reshape(-1).float())
         torch.cuda.synchronize()
-        cpdp.cpdp_state_init_plan(self.plan, stream)
+        cpdp.cpdp_state_init_plan(self.plan, _on(stream))
         self.opt_step = 0
 
     def step(self, t: int, opt: Optimizer, beta: float = 0.0, alpha: float = 1.0, T: int = 0,
@@ -55,9 +55,9 @@ class CpdpMultiState:
         self.opt_step += 1
         c = opt.c_struct(self.opt_step)
         if method == "ddp" or cpdp.cpdp_is_sync_step(t, self.K, T):
-            cpdp.cpdp_sync_step_plan(method, self.plan, self.K, c, beta, alpha, flags, stream)
+            cpdp.cpdp_sync_step_plan(method, self.plan, self.K, c, beta, alpha, flags, _on(stream))
             return "reconcile"
-        cpdp.cpdp_local_step_plan(self.plan, self.K, c, stream)
+        cpdp.cpdp_local_step_plan(self.plan, self.K, c, _on(stream))
         return "local"
 
     def step_table(self, t: int, table, T: int = 0, stream=None, method: str = "cpdp",
@@ -66,12 +66,12 @@ class CpdpMultiState:
         entry, then advance the table (see CpdpState.step_table)."""
         h = table.handle
         if method == "ddp" or cpdp.cpdp_is_sync_step(t, self.K, T):
-            cpdp.cpdp_sync_step_plan_table(method, self.plan, self.K, h, flags, stream)
+            cpdp.cpdp_sync_step_plan_table(method, self.plan, self.K, h, flags, _on(stream))
             kind = "reconcile"
         else:
-            cpdp.cpdp_local_step_plan_table(self.plan, self.K, h, stream)
+            cpdp.cpdp_local_step_plan_table(self.plan, self.K, h, _on(stream))
             kind = "local"
-        cpdp.cpdp_step_table_advance(h, stream)
+        cpdp.cpdp_step_table_advance(h, _on(stream))
         return kind
 
     def capture_steps(self, n_steps: int, table, T: int = 0, t0: int = 1,

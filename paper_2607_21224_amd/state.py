@@ -4,6 +4,10 @@ PyTorch only allocates the HBM buffers and supplies the stream; every update
 goes through the C ABI (``cpdp.py``).  Layout: params / mom are (W, ld)
 tensors whose first P columns are the replicas' coordinates (row stride ld);
 slow_mom (u) and anchor (the reference model) are (P,) fp32 tensors.
+
+Every method that launches takes ``stream``: a ``torch.cuda.Stream``, a raw
+``hipStream_t`` integer, or None for torch's current stream, as torch's own
+operations use (the C ABI itself reads a NULL stream as the null stream).
 """
 from __future__ import annotations
 
@@ -16,6 +20,15 @@ from . import cpdp
 
 def round_up(x: int, m: int) -> int:
     return (x + m - 1) // m * m
+
+
+def _on(stream):
+    """The stream a launch goes to: the one given, else torch's current
+    stream, so work inside ``torch.cuda.stream(s)`` (or a graph capture on
+    ``s``) stays ordered with the rest of that stream."""
+    if stream is not None or not torch.cuda.is_available():
+        return stream  # without a GPU the binding rejects the buffers itself
+    return torch.cuda.current_stream()
 
 
 @dataclass(frozen=True)
@@ -69,7 +82,7 @@ class StepTable:
                                   [b for _, _, b, _ in entries], [a for _, _, _, a in entries])
 
     def set_position(self, position: int = 0, stream=None) -> None:
-        cpdp.cpdp_step_table_set_position(self.handle, position, stream)
+        cpdp.cpdp_step_table_set_position(self.handle, position, _on(stream))
 
     def position(self) -> int:
         """The entry the next table step uses (synchronous read)."""
@@ -111,20 +124,20 @@ class CpdpState:
         self._check_theta0(theta0)
         cpdp.cpdp_state_init(theta0, self.params, self.mom, self.slow_mom,
                              self.anchor, self.W, self.P, self.ld, self.K,
-                             self.param_dt, "f32", stream)
+                             self.param_dt, "f32", _on(stream))
 
     def local_step(self, grads: torch.Tensor, h: Hyper, stream=None) -> None:
         self._check_grads(grads)
         cpdp.cpdp_local_step(self.params, self.mom, grads, self.W, self.P,
                              self.ld, self.K, h.lr, h.mu, self.param_dt, "f32",
-                             "f32", stream)
+                             "f32", _on(stream))
 
     def reconcile(self, grads: torch.Tensor, h: Hyper, stream=None) -> None:
         self._check_grads(grads)
         cpdp.cpdp_reconcile(self.params, self.mom, grads, self.slow_mom,
                             self.anchor, self.W, self.P, self.ld, self.K, h.lr,
                             h.mu, h.beta, h.alpha, self.param_dt, "f32", "f32",
-                            stream)
+                            _on(stream))
 
     def localsgd_sync(self, grads: torch.Tensor, h: Hyper, stream=None,
                       write_anchor: bool = True) -> None:
@@ -134,14 +147,14 @@ class CpdpState:
         cpdp.cpdp_localsgd_sync(self.params, self.mom, grads,
                                 self.anchor if write_anchor else None, self.W,
                                 self.P, self.ld, self.K, h.lr, h.mu,
-                                self.param_dt, "f32", "f32", stream)
+                                self.param_dt, "f32", "f32", _on(stream))
 
     def ddp_step(self, grads: torch.Tensor, h: Hyper, stream=None) -> None:
         """Synchronous DDP step (Sec. 3.1, Sec. 5.3)."""
         self._check_grads(grads)
         cpdp.cpdp_ddp_step(self.params, self.mom, grads, self.W, self.P,
                            self.ld, h.lr, h.mu, self.param_dt, "f32", "f32",
-                           stream)
+                           _on(stream))
 
     METHODS = ("cpdp", "localsgd", "ddp")
 
@@ -156,7 +169,7 @@ class CpdpState:
         cpdp.cpdp_state_init_opt(theta0, self.params, self.mom,
                                  self.mom2 if opt.kind == "adamw" else None,
                                  self.slow_mom, self.anchor, self.W, self.P, self.ld,
-                                 self.K, self.param_dt, stream)
+                                 self.K, self.param_dt, _on(stream))
         self.opt_step = 0
 
     def step_opt(self, t: int, grads: torch.Tensor, opt: Optimizer, beta: float = 0.0,
@@ -174,10 +187,10 @@ class CpdpState:
         if method == "ddp" or cpdp.cpdp_is_sync_step(t, self.K, T):
             cpdp.cpdp_sync_step_opt(method, self.params, self.mom, mom2, grads,
                                     self.slow_mom, self.anchor, self.W, self.P, self.ld,
-                                    self.K, c, beta, alpha, flags, self.param_dt, stream)
+                                    self.K, c, beta, alpha, flags, self.param_dt, _on(stream))
             return "reconcile"
         cpdp.cpdp_local_step_opt(self.params, self.mom, mom2, grads, self.W, self.P,
-                                 self.ld, self.K, c, self.param_dt, stream)
+                                 self.ld, self.K, c, self.param_dt, _on(stream))
         return "local"
 
     def step(self, t: int, grads: torch.Tensor, h: Hyper, T: int = 0,
@@ -218,13 +231,13 @@ class CpdpState:
         if method == "ddp" or cpdp.cpdp_is_sync_step(t, self.K, T):
             cpdp.cpdp_sync_step_table(method, self.params, self.mom, mom2, grads, self.slow_mom,
                                       self.anchor, self.W, self.P, self.ld, self.K, h, flags,
-                                      self.param_dt, stream)
+                                      self.param_dt, _on(stream))
             kind = "reconcile"
         else:
             cpdp.cpdp_local_step_table(self.params, self.mom, mom2, grads, self.W, self.P,
-                                       self.ld, self.K, h, self.param_dt, stream)
+                                       self.ld, self.K, h, self.param_dt, _on(stream))
             kind = "local"
-        cpdp.cpdp_step_table_advance(h, stream)
+        cpdp.cpdp_step_table_advance(h, _on(stream))
         return kind
 
     def capture_steps(self, grads: list, table: StepTable, T: int = 0, t0: int = 1,
@@ -257,9 +270,11 @@ class CpdpState:
         if self._count is None:
             self._count = torch.zeros(1, dtype=torch.int64, device=self.params.device)
         cpdp.cpdp_count_unsynced(self.params, self.anchor, self.W, self.P, self.ld, self._count,
-                                 self.param_dt, stream)
-        if stream is not None:
+                                 self.param_dt, _on(stream))
+        if isinstance(stream, torch.cuda.Stream):
             stream.synchronize()
+        elif stream is None:
+            torch.cuda.current_stream().synchronize()
         else:
             torch.cuda.synchronize(self.params.device)
         return int(self._count.item())

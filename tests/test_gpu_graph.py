@@ -33,3 +33,41 @@ def test_period_graph_replays_match_eager(method, dt):
         a, b = eager.snapshot(), graphed.snapshot()
         for k in a:
             assert np.array_equal(a[k], b[k], equal_nan=True), (period, k)
+
+
+def test_state_methods_default_to_torchs_current_stream():
+    """Without a stream argument the state methods launch on torch's current
+    stream: steps called that way inside a graph capture on a side stream are
+    captured, and the replay equals the same steps run eagerly, bitwise."""
+    import torch
+    from paper_2607_21224_amd.state import CpdpState, Hyper
+    from synth import device as sdev
+    W, P, K = 4, 20_011, 2
+    h = Hyper.fp32(0.1, 0.9, 0.5, 1.0)
+    th = torch.empty(P, dtype=torch.float32, device="cuda")
+    sdev.fill_theta0(th, P, 42, 0.02)
+    eager, graphed = CpdpState(W, P, K=K), CpdpState(W, P, K=K)
+    grads = []
+    for s in (1, 2):
+        g = torch.empty((W, eager.ld), dtype=torch.float32, device="cuda")
+        sdev.fill_grads(g, P, 42, s, 1e-3, 0.0)
+        grads.append(g)
+    eager.init(th)
+    graphed.init(th)
+    for s, g in zip((1, 2), grads):
+        eager.step(s, g, h)
+    graph = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(graph, stream=side):
+            kinds = [graphed.step(s, g, h) for s, g in zip((1, 2), grads)]
+    torch.cuda.current_stream().wait_stream(side)
+    assert kinds == ["local", "reconcile"]
+    graph.replay()
+    torch.cuda.synchronize()
+    for name in ("params", "mom", "slow_mom", "anchor"):
+        a, b = getattr(eager, name), getattr(graphed, name)
+        if a.dim() == 2:  # the row padding [P, ld) is never written
+            a, b = a[:, :P], b[:, :P]
+        assert torch.equal(a, b), name
