@@ -6,7 +6,7 @@ from __future__ import annotations
 import torch
 
 from . import cpdp
-from .state import Hyper, Optimizer, _on
+from .state import Hyper, Optimizer, _on, check_exact, load_exact
 
 
 class CpdpMultiState:
@@ -120,17 +120,23 @@ class CpdpMultiState:
             raise ValueError("state_dict is for a different model layout")
         if ("mom2" in d) != (self.mom2 is not None):
             raise ValueError("state_dict and state differ in AdamW second moments")
+        pairs = []
         for fam in self.FAMILIES:
             dst = getattr(self, fam)
             if dst is None:
                 continue
-            if fam in ("slow_mom", "anchor"):
-                for x, y in zip(dst, d[fam]):
-                    x.copy_(y)
-            else:
-                for row_x, row_y in zip(dst, d[fam]):
-                    for x, y in zip(row_x, row_y):
-                        x.copy_(y)
+            rows = [dst] if fam in ("slow_mom", "anchor") else dst
+            src = [d[fam]] if fam in ("slow_mom", "anchor") else d[fam]
+            if len(src) != len(rows) or any(len(a) != len(b) for a, b in zip(rows, src)):
+                raise ValueError(f"{fam}: state_dict has a different number of tensors")
+            for i, (row_x, row_y) in enumerate(zip(rows, src)):
+                for t, (x, y) in enumerate(zip(row_x, row_y)):
+                    pairs.append((x, y, f"{fam}[{i}][{t}]"))
+        # every tensor is checked before any is overwritten
+        for x, y, name in pairs:
+            check_exact(x, y, name)
+        for x, y, name in pairs:
+            load_exact(x, y, name)
         self.opt_step = int(d["opt_step"])
         torch.cuda.synchronize()
 

@@ -22,6 +22,21 @@ def round_up(x: int, m: int) -> int:
     return (x + m - 1) // m * m
 
 
+def check_exact(ref: torch.Tensor, src, name: str) -> None:
+    """A checkpointed tensor must have exactly the shape and dtype of the state
+    buffer it restores: never a broadcast or a conversion."""
+    if not isinstance(src, torch.Tensor):
+        raise ValueError(f"{name}: expected a tensor, got {type(src).__name__}")
+    if tuple(src.shape) != tuple(ref.shape) or src.dtype != ref.dtype:
+        raise ValueError(f"{name}: expected {tuple(ref.shape)} {ref.dtype}, "
+                         f"got {tuple(src.shape)} {src.dtype}")
+
+
+def load_exact(dst: torch.Tensor, src, name: str) -> None:
+    check_exact(dst, src, name)
+    dst.copy_(src)
+
+
 def _on(stream):
     """The stream a launch goes to: the one given, else torch's current
     stream, so work inside ``torch.cuda.stream(s)`` (or a graph capture on
@@ -322,13 +337,15 @@ class CpdpState:
 
     @classmethod
     def from_state_dict(cls, d: dict, device="cuda") -> "CpdpState":
+        """A new state holding a state_dict's values.  Every buffer must have
+        exactly the shape and type the layout (W, P, ld, param_dt) implies:
+        the kernels trust the state's W and ld, so a mismatched buffer is
+        rejected here rather than copied or broadcast."""
         st = cls(d["W"], d["P"], d["ld"], d["K"], d["param_dt"], device=device)
-        st.params.copy_(d["params"])
-        st.mom.copy_(d["mom"])
-        st.slow_mom.copy_(d["slow_mom"])
-        st.anchor.copy_(d["anchor"])
         if "mom2" in d:
-            st.mom2 = d["mom2"].to(device)
+            st.mom2 = torch.empty_like(st.mom)
+        for name in ("params", "mom", "slow_mom", "anchor") + (("mom2",) if "mom2" in d else ()):
+            load_exact(getattr(st, name), d[name], name)
         st.opt_step = int(d["opt_step"])
         return st
 

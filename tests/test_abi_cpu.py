@@ -416,3 +416,28 @@ def test_synth_device_wrappers_reject_host_and_small_tensors():
         sdev.fill_grads(torch.zeros(2, 16), 16, 1, 1)
     with pytest.raises(ValueError, match="GPU tensor"):
         sdev.copy_f32(torch.zeros(4), torch.zeros(4), 4)
+
+
+def test_checkpoint_restore_rejects_mismatched_buffers():
+    """from_state_dict copies only buffers of exactly the layout's shape and
+    type: the kernels trust the state's W and ld, so a checkpoint buffer that
+    is smaller, broadcastable or of another type must not reach them."""
+    import torch
+    from paper_2607_21224_amd.state import CpdpState
+    st = CpdpState(2, 8, ld=16, K=2, device="cpu")
+    for name in ("params", "mom", "slow_mom", "anchor"):
+        getattr(st, name).copy_(torch.arange(getattr(st, name).numel(),
+                                             dtype=torch.float32).view_as(getattr(st, name)))
+    d = {"W": 2, "P": 8, "ld": 16, "K": 2, "param_dt": "f32", "opt_step": 3,
+         "params": st.params.clone(), "mom": st.mom.clone(), "slow_mom": st.slow_mom.clone(),
+         "anchor": st.anchor.clone(), "mom2": st.mom.clone()}
+    back = CpdpState.from_state_dict(d, device="cpu")
+    for name in ("params", "mom", "slow_mom", "anchor"):
+        assert torch.equal(getattr(back, name), getattr(st, name))
+    assert torch.equal(back.mom2, st.mom) and back.opt_step == 3
+    bad = [("mom2", torch.zeros(2, 8)), ("mom2", torch.zeros(16)),
+           ("mom", torch.zeros(2, 16, dtype=torch.float64)), ("anchor", torch.zeros(1)),
+           ("params", [0.0] * 32)]
+    for name, value in bad:
+        with pytest.raises(ValueError, match=name):
+            CpdpState.from_state_dict(dict(d, **{name: value}), device="cpu")

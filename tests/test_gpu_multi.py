@@ -202,3 +202,12 @@ def test_plan_checkpoint_resume_bitwise():
     for fam in ("slow_mom", "anchor"):
         assert torch.equal(b.gather(fam).view(torch.int32), c.gather(fam).view(torch.int32)), fam
     assert c.opt_step == b.opt_step == 4 * K
+
+    # a checkpoint with one tensor of the wrong size is rejected before any
+    # tensor of the state is overwritten
+    bad = dict(saved, mom2=[list(row) for row in saved["mom2"]])
+    bad["mom2"][1][2] = torch.zeros(bad["mom2"][1][2].numel() + 1)
+    before = c.gather("params", 0).clone()
+    with pytest.raises(ValueError, match=r"mom2\[1\]\[2\]"):
+        c.load_state_dict(bad)
+    assert torch.equal(c.gather("params", 0), before)
