@@ -177,6 +177,34 @@ def _addr(x) -> int | None:
     return int(x.data_ptr())
 
 
+def _esize(dt) -> int:
+    return 2 if _dt(dt) == CPDP_BF16 else 4
+
+
+def _span(x, n_elems: int, dt, name: str):
+    """Address of a buffer argument the call touches for n_elems elements of
+    storage type dt.  A tensor must hold at least those bytes: the ABI takes
+    raw addresses and cannot see a buffer's size, so a short tensor would
+    send the kernel past its end."""
+    if hasattr(x, "data_ptr") and n_elems > 0:
+        need = n_elems * _esize(dt)
+        have = x.numel() * x.element_size()
+        if have < need:
+            raise ValueError(f"{name}: the call touches {need} bytes, the tensor holds {have}")
+    return _addr(x)
+
+
+def _rows(x, W, P, ld, dt, name: str):
+    """A W-row family (row stride ld, P coordinates per row)."""
+    W, P, ld = int(W), int(P), int(ld)
+    n = (W - 1) * ld + P if W >= 1 and P > 0 and ld >= P else 0
+    return _span(x, n, dt, name)
+
+
+def _vec(x, P, name: str, dt=CPDP_F32):
+    return _span(x, int(P) if int(P) > 0 else 0, dt, name)
+
+
 def _stream(s) -> int | None:
     if s is None:
         return None
@@ -208,8 +236,10 @@ def cpdp_is_sync_step(t: int, K: int, T: int = 0) -> bool:
 
 def cpdp_state_init(theta0, params, mom, slow_mom, anchor, W, P, ld, K,
                     param_dt=CPDP_F32, mom_dt=CPDP_F32, stream=None, check=True):
-    s = lib.cpdp_state_init(_addr(theta0), _addr(params), _addr(mom),
-                            _addr(slow_mom), _addr(anchor), int(W), int(P),
+    s = lib.cpdp_state_init(_vec(theta0, P, "theta0", param_dt),
+                            _rows(params, W, P, ld, param_dt, "params"),
+                            _rows(mom, W, P, ld, mom_dt, "mom"),
+                            _vec(slow_mom, P, "slow_mom"), _vec(anchor, P, "anchor"), int(W), int(P),
                             int(ld), int(K), _dt(param_dt), _dt(mom_dt),
                             _stream(stream))
     return _done(s, "cpdp_state_init", check)
@@ -218,7 +248,9 @@ def cpdp_state_init(theta0, params, mom, slow_mom, anchor, W, P, ld, K,
 def cpdp_local_step(params, mom, grads, W, P, ld, K, lr, mu,
                     param_dt=CPDP_F32, grad_dt=CPDP_F32, mom_dt=CPDP_F32,
                     stream=None, check=True):
-    s = lib.cpdp_local_step(_addr(params), _addr(mom), _addr(grads), int(W),
+    s = lib.cpdp_local_step(_rows(params, W, P, ld, param_dt, "params"),
+                            _rows(mom, W, P, ld, mom_dt, "mom"),
+                            _rows(grads, W, P, ld, grad_dt, "grads"), int(W),
                             int(P), int(ld), int(K), float(lr), float(mu),
                             _dt(param_dt), _dt(grad_dt), _dt(mom_dt),
                             _stream(stream))
@@ -228,8 +260,10 @@ def cpdp_local_step(params, mom, grads, W, P, ld, K, lr, mu,
 def cpdp_reconcile(params, mom, grads, slow_mom, anchor, W, P, ld, K, lr, mu,
                    beta, alpha, param_dt=CPDP_F32, grad_dt=CPDP_F32,
                    mom_dt=CPDP_F32, stream=None, check=True):
-    s = lib.cpdp_reconcile(_addr(params), _addr(mom), _addr(grads),
-                           _addr(slow_mom), _addr(anchor), int(W), int(P),
+    s = lib.cpdp_reconcile(_rows(params, W, P, ld, param_dt, "params"),
+                           _rows(mom, W, P, ld, mom_dt, "mom"),
+                           _rows(grads, W, P, ld, grad_dt, "grads"),
+                           _vec(slow_mom, P, "slow_mom"), _vec(anchor, P, "anchor"), int(W), int(P),
                            int(ld), int(K), float(lr), float(mu), float(beta),
                            float(alpha), _dt(param_dt), _dt(grad_dt),
                            _dt(mom_dt), _stream(stream))
@@ -239,8 +273,10 @@ def cpdp_reconcile(params, mom, grads, slow_mom, anchor, W, P, ld, K, lr, mu,
 def cpdp_localsgd_sync(params, mom, grads, anchor, W, P, ld, K, lr, mu,
                        param_dt=CPDP_F32, grad_dt=CPDP_F32, mom_dt=CPDP_F32,
                        stream=None, check=True):
-    s = lib.cpdp_localsgd_sync(_addr(params), _addr(mom), _addr(grads),
-                               _addr(anchor), int(W), int(P), int(ld), int(K),
+    s = lib.cpdp_localsgd_sync(_rows(params, W, P, ld, param_dt, "params"),
+                               _rows(mom, W, P, ld, mom_dt, "mom"),
+                               _rows(grads, W, P, ld, grad_dt, "grads"),
+                               _vec(anchor, P, "anchor"), int(W), int(P), int(ld), int(K),
                                float(lr), float(mu), _dt(param_dt), _dt(grad_dt),
                                _dt(mom_dt), _stream(stream))
     return _done(s, "cpdp_localsgd_sync", check)
@@ -248,7 +284,9 @@ def cpdp_localsgd_sync(params, mom, grads, anchor, W, P, ld, K, lr, mu,
 
 def cpdp_ddp_step(params, mom, grads, W, P, ld, lr, mu, param_dt=CPDP_F32,
                   grad_dt=CPDP_F32, mom_dt=CPDP_F32, stream=None, check=True):
-    s = lib.cpdp_ddp_step(_addr(params), _addr(mom), _addr(grads), int(W),
+    s = lib.cpdp_ddp_step(_rows(params, W, P, ld, param_dt, "params"),
+                          _rows(mom, W, P, ld, mom_dt, "mom"),
+                          _rows(grads, W, P, ld, grad_dt, "grads"), int(W),
                           int(P), int(ld), float(lr), float(mu), _dt(param_dt),
                           _dt(grad_dt), _dt(mom_dt), _stream(stream))
     return _done(s, "cpdp_ddp_step", check)
@@ -260,15 +298,22 @@ def _opt(opt):
 
 def cpdp_state_init_opt(theta0, params, mom, mom2, slow_mom, anchor, W, P, ld, K,
                         param_dt=CPDP_F32, stream=None, check=True):
-    s = lib.cpdp_state_init_opt(_addr(theta0), _addr(params), _addr(mom), _addr(mom2),
-                                _addr(slow_mom), _addr(anchor), int(W), int(P), int(ld),
+    s = lib.cpdp_state_init_opt(_vec(theta0, P, "theta0", param_dt),
+                                _rows(params, W, P, ld, param_dt, "params"),
+                                _rows(mom, W, P, ld, CPDP_F32, "mom"),
+                                _rows(mom2, W, P, ld, CPDP_F32, "mom2"),
+                                _vec(slow_mom, P, "slow_mom"), _vec(anchor, P, "anchor"),
+                                int(W), int(P), int(ld),
                                 int(K), _dt(param_dt), _stream(stream))
     return _done(s, "cpdp_state_init_opt", check)
 
 
 def cpdp_local_step_opt(params, mom, mom2, grads, W, P, ld, K, opt, param_dt=CPDP_F32,
                         stream=None, check=True):
-    s = lib.cpdp_local_step_opt(_addr(params), _addr(mom), _addr(mom2), _addr(grads),
+    s = lib.cpdp_local_step_opt(_rows(params, W, P, ld, param_dt, "params"),
+                                _rows(mom, W, P, ld, CPDP_F32, "mom"),
+                                _rows(mom2, W, P, ld, CPDP_F32, "mom2"),
+                                _rows(grads, W, P, ld, CPDP_F32, "grads"),
                                 int(W), int(P), int(ld), int(K), _opt(opt),
                                 _dt(param_dt), _stream(stream))
     return _done(s, "cpdp_local_step_opt", check)
@@ -278,8 +323,11 @@ def cpdp_sync_step_opt(strategy, params, mom, mom2, grads, slow_mom, anchor, W, 
                        opt, beta=0.0, alpha=1.0, flags=0, param_dt=CPDP_F32, stream=None,
                        check=True):
     strategy = SYNC_KINDS[strategy] if isinstance(strategy, str) else int(strategy)
-    s = lib.cpdp_sync_step_opt(strategy, _addr(params), _addr(mom), _addr(mom2),
-                               _addr(grads), _addr(slow_mom), _addr(anchor), int(W),
+    s = lib.cpdp_sync_step_opt(strategy, _rows(params, W, P, ld, param_dt, "params"),
+                               _rows(mom, W, P, ld, CPDP_F32, "mom"),
+                               _rows(mom2, W, P, ld, CPDP_F32, "mom2"),
+                               _rows(grads, W, P, ld, CPDP_F32, "grads"),
+                               _vec(slow_mom, P, "slow_mom"), _vec(anchor, P, "anchor"), int(W),
                                int(P), int(ld), int(K), _opt(opt), float(beta),
                                float(alpha), int(flags), _dt(param_dt), _stream(stream))
     return _done(s, "cpdp_sync_step_opt", check)
@@ -329,17 +377,31 @@ def cpdp_plan_build(plan: cpdp_plan, plan_bytes, W, n_tensors, numel, params, mo
     """numel: n ints; params/mom/grads/mom2: W*n tensors or addresses,
     replica-major ([i*n + t]); slow_mom/anchor: n tensors or None."""
     keep = []
+    numel = [int(x) for x in numel]
 
-    def arr(xs):
-        r = _ptr_array(xs)
-        if r is None:
+    if len(numel) != int(n_tensors):
+        raise ValueError(f"numel has {len(numel)} entries for {n_tensors} tensors")
+
+    def arr(xs, dt, name, count):
+        if xs is None:
             return None
+        # the library reads exactly `count` addresses from the array
+        if len(xs) != count:
+            raise ValueError(f"{name}: {len(xs)} entries, the plan needs {count}")
+        # every tensor must hold its model tensor's numel elements (the table
+        # records raw addresses; the kernels trust numel)
+        for k, x in enumerate(xs):
+            _span(x, numel[k % len(numel)], dt, f"{name}[{k}]")
+        r = _ptr_array(xs)
         keep.append(r[1])
         return r[0]
-    nm = (ctypes.c_int64 * len(numel))(*[int(x) for x in numel])
+    wn = int(W) * len(numel) if int(W) > 0 else 0
+    nm = (ctypes.c_int64 * len(numel))(*numel)
     s = lib.cpdp_plan_build(ctypes.byref(plan), int(plan_bytes), int(W), int(n_tensors), nm,
-                            arr(params), arr(mom), arr(mom2), arr(grads), arr(slow_mom),
-                            arr(anchor), _dt(param_dt))
+                            arr(params, param_dt, "params", wn), arr(mom, CPDP_F32, "mom", wn),
+                            arr(mom2, CPDP_F32, "mom2", wn), arr(grads, CPDP_F32, "grads", wn),
+                            arr(slow_mom, CPDP_F32, "slow_mom", len(numel)),
+                            arr(anchor, CPDP_F32, "anchor", len(numel)), _dt(param_dt))
     return _done(s, "cpdp_plan_build", check)
 
 
@@ -396,7 +458,10 @@ def cpdp_step_table_position(t: cpdp_step_table) -> int:
 
 def cpdp_local_step_table(params, mom, mom2, grads, W, P, ld, K, t: cpdp_step_table,
                           param_dt=CPDP_F32, stream=None, check=True):
-    s = lib.cpdp_local_step_table(_addr(params), _addr(mom), _addr(mom2), _addr(grads), int(W),
+    s = lib.cpdp_local_step_table(_rows(params, W, P, ld, param_dt, "params"),
+                                  _rows(mom, W, P, ld, CPDP_F32, "mom"),
+                                  _rows(mom2, W, P, ld, CPDP_F32, "mom2"),
+                                  _rows(grads, W, P, ld, CPDP_F32, "grads"), int(W),
                                   int(P), int(ld), int(K), ctypes.byref(t), _dt(param_dt),
                                   _stream(stream))
     return _done(s, "cpdp_local_step_table", check)
@@ -406,8 +471,12 @@ def cpdp_sync_step_table(strategy, params, mom, mom2, grads, slow_mom, anchor, W
                          t: cpdp_step_table, flags=0, param_dt=CPDP_F32, stream=None,
                          check=True):
     strategy = SYNC_KINDS[strategy] if isinstance(strategy, str) else int(strategy)
-    s = lib.cpdp_sync_step_table(strategy, _addr(params), _addr(mom), _addr(mom2),
-                                 _addr(grads), _addr(slow_mom), _addr(anchor), int(W), int(P),
+    s = lib.cpdp_sync_step_table(strategy, _rows(params, W, P, ld, param_dt, "params"),
+                                 _rows(mom, W, P, ld, CPDP_F32, "mom"),
+                                 _rows(mom2, W, P, ld, CPDP_F32, "mom2"),
+                                 _rows(grads, W, P, ld, CPDP_F32, "grads"),
+                                 _vec(slow_mom, P, "slow_mom"), _vec(anchor, P, "anchor"),
+                                 int(W), int(P),
                                  int(ld), int(K), ctypes.byref(t), int(flags), _dt(param_dt),
                                  _stream(stream))
     return _done(s, "cpdp_sync_step_table", check)
@@ -418,7 +487,10 @@ def cpdp_count_unsynced(params, anchor, W, P, ld, count, param_dt=CPDP_F32, stre
     """Enqueue the count of coordinates where some replica differs from the
     reference model (stored type, bitwise) into ``count`` (a device uint64 /
     int64 tensor of one element)."""
-    s = lib.cpdp_count_unsynced(_addr(params), _addr(anchor), int(W), int(P), int(ld),
+    if hasattr(count, "data_ptr") and count.numel() * count.element_size() < 8:
+        raise ValueError("count: the call writes 8 bytes, the tensor holds fewer")
+    s = lib.cpdp_count_unsynced(_rows(params, W, P, ld, param_dt, "params"),
+                                _vec(anchor, P, "anchor"), int(W), int(P), int(ld),
                                 _dt(param_dt), _addr(count), _stream(stream))
     return _done(s, "cpdp_count_unsynced", check)
 

@@ -441,3 +441,45 @@ def test_checkpoint_restore_rejects_mismatched_buffers():
     for name, value in bad:
         with pytest.raises(ValueError, match=name):
             CpdpState.from_state_dict(dict(d, **{name: value}), device="cpu")
+
+
+def test_binding_rejects_tensors_smaller_than_the_call_touches():
+    """The ABI takes raw addresses, so the binding checks that every tensor
+    argument holds the bytes the call will touch ((W-1)*ld + P elements of a
+    row family, P of a vector, numel of a plan tensor): a short tensor never
+    reaches a kernel.  (Integer addresses stand for the other buffers; they
+    pass through unchecked, as in C.)"""
+    import torch
+    W, P, ld = 3, 100, 128
+    a = [A + k * (1 << 30) for k in range(8)]
+    full = torch.zeros(W * ld)
+    short = torch.zeros(W * P)                      # rows of stride P, not ld
+    short_vec = torch.zeros(P - 1)
+    with pytest.raises(ValueError, match="grads"):
+        cpdp.cpdp_local_step(a[0], a[1], short, W, P, ld, 1, 0.1, 0.9)
+    with pytest.raises(ValueError, match="anchor"):
+        cpdp.cpdp_reconcile(a[0], a[1], a[2], a[3], short_vec, W, P, ld, 2, 0.1, 0.9, 0.5, 1.0)
+    with pytest.raises(ValueError, match="params"):  # bf16 rows: 2 bytes per element
+        cpdp.cpdp_local_step(torch.zeros((W - 1) * ld + P - 1, dtype=torch.bfloat16), a[1], a[2],
+                             W, P, ld, 1, 0.1, 0.9, param_dt="bf16")
+    with pytest.raises(ValueError, match="theta0"):
+        cpdp.cpdp_state_init(short_vec, a[1], a[2], a[3], a[4], W, P, ld, 1)
+    with pytest.raises(ValueError, match="mom2"):
+        cpdp.cpdp_local_step_opt(a[0], a[1], short, a[2], W, P, ld, 1,
+                                 cpdp.cpdp_optimizer(1, 1e-3, 0.9, 0.999, 1e-8, 0.0, 1))
+    with pytest.raises(ValueError, match="count"):
+        cpdp.cpdp_count_unsynced(a[0], a[1], W, P, ld, torch.zeros(1, dtype=torch.int32))
+    # a right-sized host tensor gets past the size check and stops at the device check
+    with pytest.raises(ValueError, match="device tensors"):
+        cpdp.cpdp_local_step(a[0], a[1], full, W, P, ld, 1, 0.1, 0.9)
+    # plans: the pointer arrays must have W*n (or n) entries, each tensor numel elements
+    t63 = torch.zeros(63)
+    with pytest.raises(ValueError, match="numel"):
+        cpdp.cpdp_plan_build(cpdp.cpdp_plan(), 1 << 12, 1, 2, [64], a[:2], a[2:4], None,
+                             a[4:6], None, None)
+    with pytest.raises(ValueError, match="entries"):
+        cpdp.cpdp_plan_build(cpdp.cpdp_plan(), 1 << 12, 2, 1, [64], a[:1], a[2:4], None,
+                             a[4:6], None, None)
+    with pytest.raises(ValueError, match=r"grads\[1\]"):
+        cpdp.cpdp_plan_build(cpdp.cpdp_plan(), 1 << 12, 2, 1, [64], a[:2], a[2:4], None,
+                             [a[4], t63], None, None)
