@@ -14,15 +14,17 @@ from synth import WORKLOADS, gen
 pytestmark = pytest.mark.gpu
 
 
-def test_plan_equals_flat_resnet50_layout():
-    """161 ResNet-50 tensors x 8 replicas, each its own allocation, against
-    the flat buffer on the same seeded inputs: bitwise equal after every step."""
-    w = WORKLOADS["r50_100"]
+@pytest.mark.parametrize("name", ["r50_100", "vit_s", "r50_200"])
+def test_plan_equals_flat_model_layouts(name):
+    """The model's tensors (ResNet-50: 161, ViT-S: 146) x W replicas, each its
+    own allocation, against the flat buffer on the same seeded inputs over two
+    periods: bitwise equal after every step."""
+    w = WORKLOADS[name]
     numels = [x for _, x in w.tensors]
     offs = np.cumsum([0] + numels)
-    c = Case(W=w.W, P=w.P, K=w.K, lr=w.lr, mu=w.mu, beta=w.beta, alpha=w.alpha, steps=8,
-             ld=w.ld)
-    log(f"[multi] r50_100 layout: {len(numels)} tensors, W={c.W}")
+    c = Case(W=w.W, P=w.P, K=w.K, lr=w.lr, mu=w.mu, beta=w.beta, alpha=w.alpha,
+             steps=2 * w.K, ld=w.ld, outlier_rate=w.outlier_rate)
+    log(f"[multi] {name} layout: {len(numels)} tensors, W={c.W}")
     flat = GpuRun(c)
     multi = CpdpMultiState(c.W, numels, c.K)
     multi.init([flat.st.anchor[offs[t]:offs[t + 1]] for t in range(len(numels))])
