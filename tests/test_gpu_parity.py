@@ -22,6 +22,14 @@ def test_tiny_every_coordinate(seed):
     run_parity(case_of("tiny", seed))
 
 
+def test_tiny_long_horizon_every_coordinate():
+    """200 periods (400 steps) of the tiny workload, every coordinate compared
+    every 20 periods: the anchor accumulates across periods, so this checks
+    that rounding differences between the fp32 kernel and the oracle stay
+    bounded over a long run instead of drifting out of tolerance."""
+    run_parity(case_of("tiny", steps=400), every=40)
+
+
 @pytest.mark.parametrize("seed", [42, 123, 777])
 @pytest.mark.parametrize("name", ["r50_100", "vit_s", "r50_200", "stress"])
 def test_full_size_sampled(name, seed):
