@@ -79,8 +79,11 @@ def _oracle_slice(w, start: int, n: int, budget_s: float, method: str = "cpdp",
     f = lambda x: float(np.float32(x))  # noqa: E731
     lr, mu, beta, alpha = f(w.lr), f(w.mu), f(w.beta), f(w.alpha)
     th0 = gen.theta0(42, idx, w.theta_sigma).astype(np.float64)
-    grads = [gen.grads(42, s, w.W, idx, w.grad_sigma, w.outlier_rate).astype(np.float64)
+    grads = [gen.grads(42, s, w.W, idx, w.grad_sigma, w.outlier_rate)
              for s in range(1, w.K + 1)]
+    if w.grad_dt == "bf16":  # the stored bf16 values are the input
+        grads = [gen.bf16_round(g) for g in grads]
+    grads = [g.astype(np.float64) for g in grads]
     st = oracle.state_init(th0, w.W, w.param_dt)
     mom2 = np.zeros((w.W, n))
     o = OPTIMIZERS.get(optimizer)
@@ -186,6 +189,9 @@ def main() -> int:
                          "(ResNet-50 / ViT-S tensor lists) instead of the flat buffer")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=10.0)
+    ap.add_argument("--grad-dtype", default="f32", choices=["f32", "bf16"],
+                    help="gradient storage of the flat momentum-SGD path (bf16 halves the "
+                         "gradient bytes; parameters keep the workload's type)")
     ap.add_argument("--row-align-bytes", type=int, default=0,
                     help="round each replica row up to a multiple of this many bytes "
                          "(0 = the workload's default of 1 MiB)")
@@ -203,6 +209,12 @@ def main() -> int:
     from synth import device as sdev
 
     w = WORKLOADS[args.workload]
+    if args.grad_dtype != "f32":
+        if args.plan or args.graph or args.optimizer != "sgd":
+            raise SystemExit("--grad-dtype bf16 runs the flat momentum-SGD path only "
+                             "(no --plan, --graph or --optimizer)")
+        import dataclasses
+        w = dataclasses.replace(w, grad_dt=args.grad_dtype)
     if args.row_align_bytes:
         import dataclasses
         assert args.row_align_bytes % 256 == 0
@@ -214,7 +226,8 @@ def main() -> int:
     adamw = args.optimizer == "adamw"
     if args.plan and args.graph:
         raise SystemExit("--graph captures the flat-buffer path; drop --plan")
-    st = None if args.plan else CpdpState(w.W, w.P, w.ld, w.K, w.param_dt, device=dev)
+    st = None if args.plan else CpdpState(w.W, w.P, w.ld, w.K, w.param_dt, device=dev,
+                                          grad_dt=w.grad_dt)
     h = Hyper.fp32(w.lr, w.mu, w.beta, w.alpha)
     with torch.cuda.stream(stream):
         th = torch.empty(w.P, dtype=torch.float32, device=dev)
@@ -225,6 +238,8 @@ def main() -> int:
         for s in range(1, w.K + 1):
             g = torch.empty((w.W, w.ld), dtype=torch.float32, device=dev)
             sdev.fill_grads(g, w.P, 42, s, w.grad_sigma, w.outlier_rate, stream=stream)
+            if w.grad_dt == "bf16":
+                g = g.to(torch.bfloat16)  # round to nearest even
             grads.append(g)
         opt = None
         if args.optimizer != "sgd":
@@ -393,6 +408,8 @@ def main() -> int:
 
     variant = "" if (args.method, args.optimizer) == ("cpdp", "sgd") else \
         f"_{args.method}_{args.optimizer}"
+    if w.grad_dt == "bf16":
+        variant += "_bf16grads"
     if args.plan:
         variant += "_plan"
 
@@ -412,11 +429,13 @@ def main() -> int:
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "f32" if w.param_dt == "f32" else "bf16 params, f32 grads/mom/state",
+        "dtype": ("f32" if (w.param_dt, w.grad_dt) == ("f32", "f32") else
+                  f"{w.param_dt} params, {w.grad_dt} grads, f32 mom/state"),
         "data": "synthetic",
-        "config": {"workload": f"{w.name}: W={w.W} replicas, P={w.P} ({w.param_dt} params), "
+        "config": {"workload": f"{w.name}: W={w.W} replicas, P={w.P} ({w.param_dt} params"
+                               f"{', bf16 grads' if w.grad_dt == 'bf16' else ''}), "
                                f"K={w.K}, lr={w.lr}, mu={w.mu}, beta={w.beta}, alpha={w.alpha}",
-                   "W": w.W, "P": w.P, "ld": w.ld, "K": w.K,
+                   "W": w.W, "P": w.P, "ld": w.ld, "K": w.K, "grad_dt": w.grad_dt,
                    "method": args.method, "optimizer": args.optimizer,
                    "layout": (f"multi-tensor plan: {len(w.tensors)} tensors x {w.W} replicas, "
                               "one allocation each; step 1's gradients every step"

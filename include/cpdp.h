@@ -20,9 +20,13 @@
  *   boundary and ld * sizeof(element) must be a multiple of 16.  The ranges
  *   of different arguments must not overlap.
  *
- * Storage types (param_dt, grad_dt, mom_dt): CPDP_F32 everywhere, or
- *   params in CPDP_BF16 with fp32 grads and momentum.  All arithmetic is fp32;
- *   bf16 parameters are rounded to nearest-even each time they are written.
+ * Storage types (param_dt, grad_dt, mom_dt): params CPDP_F32 or CPDP_BF16;
+ *   momentum CPDP_F32.  Gradients are CPDP_F32, or CPDP_BF16 on the entry
+ *   points that take a grad_dt (cpdp_local_step, cpdp_reconcile,
+ *   cpdp_localsgd_sync, cpdp_ddp_step); every other entry point reads fp32
+ *   gradients.  All arithmetic is fp32: bf16 values are widened exactly on
+ *   load, and bf16 parameters are rounded to nearest-even each time they are
+ *   written.  Any other combination returns CPDP_ERR_DTYPE.
  *
  * Hyperparameters are fp32: lr > 0 and finite (Sec. 3.1), 0 <= mu < 1,
  *   0 <= beta < 1 (Sec. 3.1), alpha > 0 and finite, K >= 1 (Sec. 3.1).

@@ -10,7 +10,8 @@
 // All of them are HBM-streaming kernels: nothing here is a dense contraction, so
 // there is no MFMA and no LDS.  Every thread owns VEC = 4 consecutive
 // coordinates and moves them with 128-bit (fp32) or 64-bit (bf16) vector
-// accesses; a wavefront therefore touches 1 KiB (fp32) of each array row per
+// accesses (parameters, and on the plain momentum-SGD entry points also the
+// gradients, may be stored as bf16); a wavefront therefore touches 1 KiB (fp32) of each array row per
 // access, fully coalesced.  Every output element is written by exactly one
 // thread, there are no atomics and no inter-block dependencies, and the
 // cross-replica sums run in a fixed order (replica 0, 1, ..., W-1) inside one
@@ -186,21 +187,23 @@ __device__ __forceinline__ float opt_update(const OptParams& o, float th, float&
 // per replica and tensor, replica-major).  Both expose the same accessors, so
 // the step code below is written once.
 
-template <class PS>
+template <class PS, class GS_ = ParamF32>
 struct Strided {
+    using GS = GS_;  // gradient storage type
     typename PS::T* params;
     float* mom;
     float* mom2;
-    float* grads;
+    typename GS::T* grads;
     int64_t ld;
     __device__ __forceinline__ typename PS::T* prm(int i) const { return params + (int64_t)i * ld; }
     __device__ __forceinline__ float* m(int i) const { return mom + (int64_t)i * ld; }
     __device__ __forceinline__ float* v(int i) const { return mom2 + (int64_t)i * ld; }
-    __device__ __forceinline__ float* g(int i) const { return grads + (int64_t)i * ld; }
+    __device__ __forceinline__ typename GS::T* g(int i) const { return grads + (int64_t)i * ld; }
 };
 
 template <class PS>
 struct Table {
+    using GS = ParamF32;    // plans hold fp32 gradients
     const int64_t* params;  // 64-bit device addresses, entry i*n + t
     const int64_t* mom;
     const int64_t* mom2;
@@ -253,12 +256,12 @@ __device__ __forceinline__ int64_t plan_tensor(const PlanView& v, int64_t n, int
 
 // ---- local step: one replica row per block, 4 coordinates per thread -------
 
-template <Opt O, class PS, bool FULL>
+template <Opt O, class PS, class GS, bool FULL>
 __device__ __forceinline__ void local_chunk(const OptParams& o, typename PS::T* params,
-                                            float* mom, float* mom2, const float* grads,
-                                            int n) {
+                                            float* mom, float* mom2,
+                                            const typename GS::T* grads, int n) {
     float g[kVec], m[kVec], v[kVec] = {0.0f, 0.0f, 0.0f, 0.0f}, th[kVec];
-    load_f32<FULL, kNTL>(grads, n, g);
+    GS::template load<FULL, kNTL>(grads, n, g);
     load_f32<FULL, kNTL>(mom, n, m);
     if constexpr (O == Opt::ADAMW) load_f32<FULL, kNTL>(mom2, n, v);
     PS::template load<FULL, kNTL>(params, n, th);
@@ -269,15 +272,16 @@ __device__ __forceinline__ void local_chunk(const OptParams& o, typename PS::T* 
     PS::template store<FULL, kNTS>(params, n, th);
 }
 
-template <Opt O, class PS>
+template <Opt O, class PS, class GS = ParamF32>
 __device__ __forceinline__ void local_dispatch(const OptParams& o, typename PS::T* params,
-                                               float* mom, float* mom2, const float* grads,
-                                               int64_t p0, int64_t P) {
+                                               float* mom, float* mom2,
+                                               const typename GS::T* grads, int64_t p0,
+                                               int64_t P) {
     if (p0 + kVec <= P)
-        local_chunk<O, PS, true>(o, params + p0, mom + p0, mom2 + p0, grads + p0, kVec);
+        local_chunk<O, PS, GS, true>(o, params + p0, mom + p0, mom2 + p0, grads + p0, kVec);
     else
-        local_chunk<O, PS, false>(o, params + p0, mom + p0, mom2 + p0, grads + p0,
-                                  (int)(P - p0));
+        local_chunk<O, PS, GS, false>(o, params + p0, mom + p0, mom2 + p0, grads + p0,
+                                      (int)(P - p0));
 }
 
 // ---- fused synchronisation steps ----------------------------------------------
@@ -323,7 +327,8 @@ __device__ __forceinline__ void grad_batch(const Rows& r, int i0, int64_t p0, in
                                            float (&acc)[kVec]) {
     float g[C][kVec];
 #pragma unroll
-    for (int c = 0; c < C; ++c) load_f32<FULL, kNTL>(r.g(i0 + c) + p0, n, g[c]);
+    for (int c = 0; c < C; ++c)
+        Rows::GS::template load<FULL, kNTL>(r.g(i0 + c) + p0, n, g[c]);
 #pragma unroll
     for (int c = 0; c < C; ++c)
 #pragma unroll
@@ -337,7 +342,8 @@ __device__ __forceinline__ void step_batch(const OptParams& o, const Rows& r, in
     float m[C][kVec], v[C][kVec], th[C][kVec], g[C][kVec];
 #pragma unroll
     for (int c = 0; c < C; ++c) {
-        if constexpr (M == Sync::LocalSGD) load_f32<FULL, kNTL>(r.g(i0 + c) + p0, n, g[c]);
+        if constexpr (M == Sync::LocalSGD)
+            Rows::GS::template load<FULL, kNTL>(r.g(i0 + c) + p0, n, g[c]);
         load_f32<FULL, kNTL>(r.m(i0 + c) + p0, n, m[c]);
         if constexpr (kAdam) load_f32<FULL, kNTL>(r.v(i0 + c) + p0, n, v[c]);
         PS::template load<FULL, kNTL>(r.prm(i0 + c) + p0, n, th[c]);
@@ -403,7 +409,8 @@ __device__ __forceinline__ void sync_chunk(const OptParams& o, const Rows& r, fl
 #pragma unroll
         for (int k = 0; k < kVec; ++k) z.gbar[k] = acc[k] * inv_w;
         if (EXTRA && (flags & kSyncWriteGbar))
-            for (int i = 0; i < nw; ++i) store_f32<FULL, kNTS>(r.g(i) + p0, n, z.gbar);
+            for (int i = 0; i < nw; ++i)
+                Rows::GS::template store<FULL, kNTS>(r.g(i) + p0, n, z.gbar);
     }
 
     if constexpr (M == Sync::CPDP) {
@@ -459,8 +466,8 @@ __device__ __forceinline__ void sync_chunk(const OptParams& o, const Rows& r, fl
 
 // The gradient rows are written only by the variants (the gradient-mean
 // write-back), so only those instantiations take them as mutable.
-template <bool EXTRA>
-using GradPtr = typename std::conditional<EXTRA, float*, const float*>::type;
+template <bool EXTRA, class GS = ParamF32>
+using GradPtr = typename std::conditional<EXTRA, typename GS::T*, const typename GS::T*>::type;
 
 // ---- step tables: the scalars of the current step read from device memory -----
 //
@@ -522,7 +529,7 @@ struct SyncArgs {
     void* params;
     float* mom;
     float* mom2;
-    const float* grads;
+    const void* grads;  // fp32 or bf16 rows (Grad)
     float* slow;
     float* anchor;
     int W;

@@ -10,6 +10,10 @@ namespace cpdp {
 
 enum class Param { F32, BF16 };
 
+// Gradient storage of the flat local and synchronisation steps: fp32, or bf16
+// (momentum SGD without variants only; plans and step tables take fp32).
+enum class Grad { F32, BF16 };
+
 // The per-replica optimizer update: momentum SGD, SGD with coupled weight
 // decay, or AdamW.
 enum class Opt { SGD, SGD_WD, ADAMW };
@@ -45,20 +49,20 @@ int launch_state_init(Param pt, const void* theta0, void* params, float* mom,
                       float* mom2, float* slow, float* anchor, int W, int64_t P,
                       int64_t ld, void* stream);
 
-int launch_local_step(Opt opt, const OptParams& o, Param pt, void* params,
-                      float* mom, float* mom2, const float* grads, int W,
+int launch_local_step(Opt opt, const OptParams& o, Param pt, Grad gt, void* params,
+                      float* mom, float* mom2, const void* grads, int W,
                       int64_t P, int64_t ld, void* stream);
 
-int launch_sync(Sync mode, Opt opt, const OptParams& o, Param pt, void* params,
-                float* mom, float* mom2, const float* grads, float* slow,
+int launch_sync(Sync mode, Opt opt, const OptParams& o, Param pt, Grad gt, void* params,
+                float* mom, float* mom2, const void* grads, float* slow,
                 float* anchor, int W, int64_t P, int64_t ld, float beta,
                 float alpha, unsigned flags, void* stream);
 
 // launch_sync for one strategy; each is instantiated in its own translation
 // unit (kernels_sync_<strategy>.hip).
 template <Sync M>
-int launch_sync_mode(Opt opt, const OptParams& o, Param pt, void* params, float* mom,
-                     float* mom2, const float* grads, float* slow, float* anchor, int W,
+int launch_sync_mode(Opt opt, const OptParams& o, Param pt, Grad gt, void* params, float* mom,
+                     float* mom2, const void* grads, float* slow, float* anchor, int W,
                      int64_t P, int64_t ld, float beta, float alpha, unsigned flags,
                      void* stream);
 

@@ -39,17 +39,17 @@ __global__ __launch_bounds__(kBlock) void state_init_kernel(
                               (int)(P - p0));
 }
 
-template <Opt O, class PS>
+template <Opt O, class PS, class GS>
 __global__ __launch_bounds__(kBlock) void local_step_kernel(
     OptParams o, typename PS::T* __restrict__ params, float* __restrict__ mom,
-    float* __restrict__ mom2, const float* __restrict__ grads, int64_t ld, int64_t P,
+    float* __restrict__ mom2, const typename GS::T* __restrict__ grads, int64_t ld, int64_t P,
     int64_t blocks_per_row) {
     const int64_t row = blockIdx.x / blocks_per_row;
     const int64_t col = blockIdx.x - row * blocks_per_row;
     const int64_t p0 = (col * kBlock + threadIdx.x) * kVec;
     if (p0 >= P) return;
     const int64_t off = row * ld;
-    local_dispatch<O, PS>(o, params + off, mom + off, mom2 + off, grads + off, p0, P);
+    local_dispatch<O, PS, GS>(o, params + off, mom + off, mom2 + off, grads + off, p0, P);
 }
 
 template <class PS>
@@ -60,21 +60,33 @@ int state_init_t(const void* theta0, void* params, float* mom, float* mom2, floa
                   static_cast<T*>(params), mom, mom2, slow, anchor, W, ld, P);
 }
 
-template <Opt O, class PS>
-int local_step_t(const OptParams& o, void* params, float* mom, float* mom2, const float* grads,
+template <Opt O, class PS, class GS>
+int local_step_t(const OptParams& o, void* params, float* mom, float* mom2, const void* grads,
                  int W, int64_t P, int64_t ld, void* stream) {
     using T = typename PS::T;
     const int64_t bpr = blocks_for(P);
-    return launch(local_step_kernel<O, PS>, bpr * W, stream, o, static_cast<T*>(params), mom,
-                  mom2, grads, ld, P, bpr);
+    return launch(local_step_kernel<O, PS, GS>, bpr * W, stream, o, static_cast<T*>(params),
+                  mom, mom2, static_cast<const typename GS::T*>(grads), ld, P, bpr);
 }
 
 template <Opt O>
-int local_step_p(const OptParams& o, Param pt, void* params, float* mom, float* mom2,
-                 const float* grads, int W, int64_t P, int64_t ld, void* stream) {
+int local_step_p(const OptParams& o, Param pt, Grad gt, void* params, float* mom, float* mom2,
+                 const void* grads, int W, int64_t P, int64_t ld, void* stream) {
+    if (gt == Grad::BF16) {
+        // bf16 gradients: momentum SGD only (the validation layer enforces it)
+        if constexpr (O == Opt::SGD)
+            return pt == Param::BF16
+                       ? local_step_t<O, ParamBF16, ParamBF16>(o, params, mom, mom2, grads, W, P,
+                                                               ld, stream)
+                       : local_step_t<O, ParamF32, ParamBF16>(o, params, mom, mom2, grads, W, P,
+                                                              ld, stream);
+        return (int)hipErrorInvalidValue;
+    }
     return pt == Param::BF16
-               ? local_step_t<O, ParamBF16>(o, params, mom, mom2, grads, W, P, ld, stream)
-               : local_step_t<O, ParamF32>(o, params, mom, mom2, grads, W, P, ld, stream);
+               ? local_step_t<O, ParamBF16, ParamF32>(o, params, mom, mom2, grads, W, P, ld,
+                                                      stream)
+               : local_step_t<O, ParamF32, ParamF32>(o, params, mom, mom2, grads, W, P, ld,
+                                                     stream);
 }
 
 }  // namespace
@@ -88,32 +100,35 @@ int launch_state_init(Param pt, const void* theta0, void* params, float* mom, fl
                                         stream);
 }
 
-int launch_local_step(Opt opt, const OptParams& o, Param pt, void* params, float* mom,
-                      float* mom2, const float* grads, int W, int64_t P, int64_t ld,
+int launch_local_step(Opt opt, const OptParams& o, Param pt, Grad gt, void* params, float* mom,
+                      float* mom2, const void* grads, int W, int64_t P, int64_t ld,
                       void* stream) {
     switch (opt) {
         case Opt::SGD_WD:
-            return local_step_p<Opt::SGD_WD>(o, pt, params, mom, mom2, grads, W, P, ld, stream);
+            return local_step_p<Opt::SGD_WD>(o, pt, gt, params, mom, mom2, grads, W, P, ld,
+                                             stream);
         case Opt::ADAMW:
-            return local_step_p<Opt::ADAMW>(o, pt, params, mom, mom2, grads, W, P, ld, stream);
+            return local_step_p<Opt::ADAMW>(o, pt, gt, params, mom, mom2, grads, W, P, ld,
+                                            stream);
         default:
-            return local_step_p<Opt::SGD>(o, pt, params, mom, mom2, grads, W, P, ld, stream);
+            return local_step_p<Opt::SGD>(o, pt, gt, params, mom, mom2, grads, W, P, ld, stream);
     }
 }
 
-int launch_sync(Sync mode, Opt opt, const OptParams& o, Param pt, void* params, float* mom,
-                float* mom2, const float* grads, float* slow, float* anchor, int W, int64_t P,
-                int64_t ld, float beta, float alpha, unsigned flags, void* stream) {
+int launch_sync(Sync mode, Opt opt, const OptParams& o, Param pt, Grad gt, void* params,
+                float* mom, float* mom2, const void* grads, float* slow, float* anchor, int W,
+                int64_t P, int64_t ld, float beta, float alpha, unsigned flags, void* stream) {
     switch (mode) {
         case Sync::LocalSGD:
-            return launch_sync_mode<Sync::LocalSGD>(opt, o, pt, params, mom, mom2, grads, slow,
-                                                    anchor, W, P, ld, beta, alpha, flags, stream);
+            return launch_sync_mode<Sync::LocalSGD>(opt, o, pt, gt, params, mom, mom2, grads,
+                                                    slow, anchor, W, P, ld, beta, alpha, flags,
+                                                    stream);
         case Sync::DDP:
-            return launch_sync_mode<Sync::DDP>(opt, o, pt, params, mom, mom2, grads, slow, anchor,
-                                               W, P, ld, beta, alpha, flags, stream);
+            return launch_sync_mode<Sync::DDP>(opt, o, pt, gt, params, mom, mom2, grads, slow,
+                                               anchor, W, P, ld, beta, alpha, flags, stream);
         default:
-            return launch_sync_mode<Sync::CPDP>(opt, o, pt, params, mom, mom2, grads, slow, anchor,
-                                                W, P, ld, beta, alpha, flags, stream);
+            return launch_sync_mode<Sync::CPDP>(opt, o, pt, gt, params, mom, mom2, grads, slow,
+                                                anchor, W, P, ld, beta, alpha, flags, stream);
     }
 }
 

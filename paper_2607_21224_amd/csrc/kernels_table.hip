@@ -68,12 +68,14 @@ template <Sync M, Opt O, class PS>
 int sync_table_t(const int64_t* table, const SyncArgs& a) {
     using T = typename PS::T;
     const float inv_w = 1.0f / (float)a.W;
+    // step tables take fp32 gradients
+    const float* grads = static_cast<const float*>(a.grads);
     if (a.flags != 0)
         return launch(sync_table_kernel<M, O, PS, true>, blocks_for(a.P), a.stream, table,
-                      static_cast<T*>(a.params), a.mom, a.mom2, const_cast<float*>(a.grads),
+                      static_cast<T*>(a.params), a.mom, a.mom2, const_cast<float*>(grads),
                       a.slow, a.anchor, a.W, a.ld, a.P, inv_w, a.flags);
     return launch(sync_table_kernel<M, O, PS, false>, blocks_for(a.P), a.stream, table,
-                  static_cast<T*>(a.params), a.mom, a.mom2, a.grads, a.slow, a.anchor, a.W,
+                  static_cast<T*>(a.params), a.mom, a.mom2, grads, a.slow, a.anchor, a.W,
                   a.ld, a.P, inv_w, a.flags);
 }
 

@@ -115,7 +115,14 @@ class CpdpState:
     ROW_ALIGN_BYTES = 1 << 20
 
     def __init__(self, W: int, P: int, ld: int | None = None, K: int = 1,
-                 param_dt: str = "f32", device="cuda"):
+                 param_dt: str = "f32", device="cuda", grad_dt: str = "f32"):
+        """grad_dt: storage type of the gradient rows the steps take, "f32", or
+        "bf16" for the momentum-SGD steps (local_step, reconcile,
+        localsgd_sync, ddp_step and step()); the general-optimizer and
+        step-table paths take fp32 gradients."""
+        if grad_dt not in ("f32", "bf16"):
+            raise ValueError(f"grad_dt must be 'f32' or 'bf16', got {grad_dt!r}")
+        self.grad_dt = grad_dt
         self.W, self.P, self.K = int(W), int(P), int(K)
         esize = 2 if param_dt == "bf16" else 4
         align = self.ROW_ALIGN_BYTES // esize
@@ -144,14 +151,14 @@ class CpdpState:
     def local_step(self, grads: torch.Tensor, h: Hyper, stream=None) -> None:
         self._check_grads(grads)
         cpdp.cpdp_local_step(self.params, self.mom, grads, self.W, self.P,
-                             self.ld, self.K, h.lr, h.mu, self.param_dt, "f32",
+                             self.ld, self.K, h.lr, h.mu, self.param_dt, self.grad_dt,
                              "f32", _on(stream))
 
     def reconcile(self, grads: torch.Tensor, h: Hyper, stream=None) -> None:
         self._check_grads(grads)
         cpdp.cpdp_reconcile(self.params, self.mom, grads, self.slow_mom,
                             self.anchor, self.W, self.P, self.ld, self.K, h.lr,
-                            h.mu, h.beta, h.alpha, self.param_dt, "f32", "f32",
+                            h.mu, h.beta, h.alpha, self.param_dt, self.grad_dt, "f32",
                             _on(stream))
 
     def localsgd_sync(self, grads: torch.Tensor, h: Hyper, stream=None,
@@ -162,13 +169,13 @@ class CpdpState:
         cpdp.cpdp_localsgd_sync(self.params, self.mom, grads,
                                 self.anchor if write_anchor else None, self.W,
                                 self.P, self.ld, self.K, h.lr, h.mu,
-                                self.param_dt, "f32", "f32", _on(stream))
+                                self.param_dt, self.grad_dt, "f32", _on(stream))
 
     def ddp_step(self, grads: torch.Tensor, h: Hyper, stream=None) -> None:
         """Synchronous DDP step (Sec. 3.1, Sec. 5.3)."""
         self._check_grads(grads)
         cpdp.cpdp_ddp_step(self.params, self.mom, grads, self.W, self.P,
-                           self.ld, h.lr, h.mu, self.param_dt, "f32", "f32",
+                           self.ld, h.lr, h.mu, self.param_dt, self.grad_dt, "f32",
                            _on(stream))
 
     METHODS = ("cpdp", "localsgd", "ddp")
@@ -193,7 +200,7 @@ class CpdpState:
         """One step of ``method`` with a general optimizer (see step()).
         ``flags`` selects sync-step variants (cpdp.CPDP_SYNC_WRITE_GRAD_MEAN,
         cpdp.CPDP_SYNC_AVERAGE_OPT_STATE)."""
-        self._check_grads(grads)
+        self._check_grads(grads, fp32_only=True)
         if method not in self.METHODS:
             raise ValueError(method)
         self.opt_step += 1
@@ -236,7 +243,7 @@ class CpdpState:
         then advance the table (both on ``stream``).  Same cadence and
         semantics as step_opt; the optimizer state must match the table's
         update rule (init_opt with an AdamW optimizer for an AdamW table)."""
-        self._check_grads(grads)
+        self._check_grads(grads, fp32_only=True)
         if method not in self.METHODS:
             raise ValueError(method)
         h = table.handle
@@ -262,7 +269,7 @@ class CpdpState:
         len(grads) entries, so a graph of one period replays successive
         periods of a schedule.  Returns (graph, kinds)."""
         for g in grads:
-            self._check_grads(g)
+            self._check_grads(g, fp32_only=True)
         graph = torch.cuda.CUDAGraph()
         kinds = []
         side = torch.cuda.Stream()
@@ -328,7 +335,7 @@ class CpdpState:
         stream are included."""
         torch.cuda.synchronize(self.params.device)
         d = {"W": self.W, "P": self.P, "ld": self.ld, "K": self.K,
-             "param_dt": self.param_dt, "opt_step": self.opt_step,
+             "param_dt": self.param_dt, "grad_dt": self.grad_dt, "opt_step": self.opt_step,
              "params": self.params.cpu(), "mom": self.mom.cpu(),
              "slow_mom": self.slow_mom.cpu(), "anchor": self.anchor.cpu()}
         if self.mom2 is not None:
@@ -341,7 +348,8 @@ class CpdpState:
         exactly the shape and type the layout (W, P, ld, param_dt) implies:
         the kernels trust the state's W and ld, so a mismatched buffer is
         rejected here rather than copied or broadcast."""
-        st = cls(d["W"], d["P"], d["ld"], d["K"], d["param_dt"], device=device)
+        st = cls(d["W"], d["P"], d["ld"], d["K"], d["param_dt"], device=device,
+                 grad_dt=d.get("grad_dt", "f32"))
         if "mom2" in d:
             st.mom2 = torch.empty_like(st.mom)
         for name in ("params", "mom", "slow_mom", "anchor") + (("mom2",) if "mom2" in d else ()):
@@ -351,9 +359,13 @@ class CpdpState:
 
     # The ABI takes raw addresses, so these shape checks are what keeps a
     # kernel inside the caller's buffers: they raise, they are not asserts.
-    def _check_grads(self, g: torch.Tensor) -> None:
-        if g.dtype != torch.float32 or not g.is_contiguous():
-            raise ValueError("grads must be a contiguous float32 tensor")
+    def _check_grads(self, g: torch.Tensor, fp32_only: bool = False) -> None:
+        if fp32_only and self.grad_dt != "f32":
+            raise ValueError("the general-optimizer and step-table paths take fp32 gradients; "
+                             "this state was made with grad_dt='bf16'")
+        want = torch.bfloat16 if self.grad_dt == "bf16" else torch.float32
+        if g.dtype != want or not g.is_contiguous():
+            raise ValueError(f"grads must be a contiguous {want} tensor")
         if tuple(g.shape) != (self.W, self.ld):
             raise ValueError(f"grads must have shape {(self.W, self.ld)}, got {tuple(g.shape)}")
         if g.device != self.params.device:

@@ -67,7 +67,8 @@ class Workload:
     beta: float
     alpha: float
     periods: int
-    param_dt: str = "f32"          # "f32" or "bf16"; grads and momentum are f32
+    param_dt: str = "f32"          # "f32" or "bf16"; momentum is f32
+    grad_dt: str = "f32"           # gradient storage, "f32" or "bf16"
     theta_sigma: float = 0.02
     grad_sigma: float = 1e-3
     outlier_rate: float = 0.0
@@ -94,16 +95,19 @@ class Workload:
     def param_bytes(self) -> int:
         return 2 if self.param_dt == "bf16" else 4
 
+    def grad_bytes(self) -> int:
+        return 2 if self.grad_dt == "bf16" else 4
+
     def _replica_bytes(self, adamw: bool) -> int:
         """Per replica-coordinate bytes every step moves: the gradient read,
         the optimizer state read and written (momentum, plus AdamW's second
         moment), the parameter read and written."""
-        return 4 + (16 if adamw else 8) + 2 * self.param_bytes()
+        return self.grad_bytes() + (16 if adamw else 8) + 2 * self.param_bytes()
 
     def reconcile_bytes(self, adamw: bool = False) -> int:
         """Algorithmic HBM bytes of one reconcile: every state tensor read
         once, every updated one written once, plus u and anchor read and
-        written (grads, optimizer state, u and anchor are fp32)."""
+        written (optimizer state, u and anchor are fp32)."""
         return self.P * (self.W * self._replica_bytes(adamw) + 16)
 
     def sync_bytes(self, method: str = "cpdp", adamw: bool = False) -> int:

@@ -48,6 +48,7 @@ class Case:
     # with lr / mu above
     opt: dict | None = None
     flags: int = 0            # sync-step variants (general-optimizer path only)
+    grad_dt: str = "f32"      # gradient storage ("bf16": momentum-SGD steps only)
 
     def opt32(self) -> dict:
         f = lambda x: float(np.float32(x))  # noqa: E731
@@ -82,8 +83,10 @@ def oracle_inputs(c: Case, idx: np.ndarray):
     th0 = gen.theta0(c.seed, idx, c.theta_sigma).astype(np.float64)
 
     def grads(step, W, P):
-        return gen.grads(c.seed, step, c.W, idx, c.grad_sigma,
-                         c.outlier_rate).astype(np.float64)
+        g = gen.grads(c.seed, step, c.W, idx, c.grad_sigma, c.outlier_rate)
+        if c.grad_dt == "bf16":  # the input the GPU steps on is the stored bf16 value
+            g = gen.bf16_round(g)
+        return g.astype(np.float64)
     return th0, grads
 
 
@@ -116,11 +119,14 @@ class GpuRun:
         from paper_2607_21224_amd.state import CpdpState, Hyper, Optimizer
         self.c = c
         self.stream = stream
-        self.st = CpdpState(c.W, c.P, c.ld, c.K, c.param_dt, device="cuda")
+        self.st = CpdpState(c.W, c.P, c.ld, c.K, c.param_dt, device="cuda", grad_dt=c.grad_dt)
         self.h = Hyper(*c.hyper32())
         self.opt = Optimizer(**c.opt32()) if c.opt is not None else None
         self.grads = torch.empty((c.W, self.st.ld), dtype=torch.float32,
                                  device="cuda")
+        # bf16 gradient rows, converted from the generated fp32 values (RNE)
+        self.grads_bf16 = (torch.empty((c.W, self.st.ld), dtype=torch.bfloat16, device="cuda")
+                           if c.grad_dt == "bf16" else None)
         th = torch.empty(max(c.P, 1), dtype=torch.float32, device="cuda")
         sdev.fill_theta0(th, c.P, c.seed, c.theta_sigma, stream=stream)
         if c.param_dt == "bf16":
@@ -134,11 +140,16 @@ class GpuRun:
         c = self.c
         sdev.fill_grads(self.grads, c.P, c.seed, step, c.grad_sigma,
                         c.outlier_rate, stream=self.stream)
+        grads = self.grads
+        if self.grads_bf16 is not None:
+            with torch.cuda.stream(self.stream or torch.cuda.current_stream()):
+                self.grads_bf16.copy_(self.grads)
+            grads = self.grads_bf16
         t = ((step - 1) % c.T) + 1 if c.T > 0 else step
         if self.opt is not None:
             return self.st.step_opt(t, self.grads, self.opt, self.h.beta, self.h.alpha,
                                     c.T, stream=self.stream, method=c.method, flags=c.flags)
-        return self.st.step(t, self.grads, self.h, c.T, stream=self.stream,
+        return self.st.step(t, grads, self.h, c.T, stream=self.stream,
                             method=c.method)
 
     def snapshot(self, idx: np.ndarray | None = None):

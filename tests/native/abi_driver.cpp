@@ -46,7 +46,8 @@ int main() {
     EXPECT(cpdp_state_init(th, pa, mo, u, an, W, P, ld, 4, 0, 1, nullptr), CPDP_ERR_DTYPE, false);
     EXPECT(cpdp_localsgd_sync(pa, mo, gr, nullptr, W, P, ld, 4, 0.1f, 0.9f, 0, 0, 0, nullptr), CPDP_OK, true);
     EXPECT(cpdp_ddp_step(pa, mo, gr, W, P, ld, 0.1f, 0.9f, 0, 0, 0, nullptr), CPDP_OK, true);
-    EXPECT(cpdp_ddp_step(pa, mo, gr, W, P, ld, 0.1f, 0.9f, 0, 1, 0, nullptr), CPDP_ERR_DTYPE, false);
+    EXPECT(cpdp_ddp_step(pa, mo, gr, W, P, ld, 0.1f, 0.9f, 0, 1, 0, nullptr), CPDP_OK, true);  // bf16 grads
+    EXPECT(cpdp_ddp_step(pa, mo, gr, W, P, ld, 0.1f, 0.9f, 0, 2, 0, nullptr), CPDP_ERR_DTYPE, false);
 
     cpdp_optimizer adam = {CPDP_OPT_ADAMW, 5e-4f, 0.9f, 0.999f, 1e-8f, 0.05f, 1};
     cpdp_optimizer sgd = {CPDP_OPT_SGD, 0.1f, 0.9f, 0.0f, 0.0f, 5e-4f, 0};

@@ -10,12 +10,12 @@ int launch_state_init(Param, const void*, void*, float*, float*, float*, float*,
                       int64_t, void*) {
     return ++g_launches, 0;
 }
-int launch_local_step(Opt, const OptParams&, Param, void*, float*, float*, const float*, int,
+int launch_local_step(Opt, const OptParams&, Param, Grad, void*, float*, float*, const void*, int,
                       int64_t, int64_t, void*) {
     return ++g_launches, 0;
 }
-int launch_sync(Sync, Opt, const OptParams&, Param, void*, float*, float*, const float*, float*,
-                float*, int, int64_t, int64_t, float, float, unsigned, void*) {
+int launch_sync(Sync, Opt, const OptParams&, Param, Grad, void*, float*, float*, const void*,
+                float*, float*, int, int64_t, int64_t, float, float, unsigned, void*) {
     return ++g_launches, 0;
 }
 int launch_state_init_plan(Param, const int64_t*, int, int, int64_t, void*) {

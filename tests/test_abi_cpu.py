@@ -114,11 +114,26 @@ def test_bad_slowmo(kw):
     assert rec(**kw) == E.CPDP_ERR_INVALID_ARG
 
 
-@pytest.mark.parametrize("kw", [dict(pdt=2), dict(gdt=1), dict(mdt=1), dict(pdt=-1)])
+@pytest.mark.parametrize("kw", [dict(pdt=2), dict(gdt=2), dict(gdt=-1), dict(mdt=1),
+                                dict(pdt=-1)])
 def test_bad_dtype(kw):
     assert rec(**kw) == E.CPDP_ERR_DTYPE
     kl = {k: v for k, v in kw.items()}
     assert loc(**kl) == E.CPDP_ERR_DTYPE
+
+
+def test_bf16_gradients_validated_at_two_bytes():
+    """bf16 gradient rows (grad_dt = CPDP_BF16) pass the storage-type check of
+    the momentum-SGD entry points and are checked at 2 bytes per element: an
+    ld of 1028 elements makes 4112-byte rows in fp32 (16-byte multiples) but
+    2056-byte rows in bf16, which the alignment rule rejects.  (Every call here
+    fails validation, so none reaches a launch.)"""
+    assert rec(gdt=0, ld=1028, slow=C) == E.CPDP_ERR_OVERLAP      # fp32: aligned
+    assert rec(gdt=1, ld=1028) == E.CPDP_ERR_MISALIGNED
+    assert loc(gdt=1, ld=1028) == E.CPDP_ERR_MISALIGNED
+    # a buffer inside the bf16 gradient block still overlaps it
+    W, ld = GOOD["W"], GOOD["ld"]
+    assert rec(gdt=1, slow=C + 2 * ((W - 1) * ld + GOOD["P"]) - 16) == E.CPDP_ERR_OVERLAP
 
 
 def test_bad_dtype_init():

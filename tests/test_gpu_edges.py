@@ -20,10 +20,25 @@ RAGGED = [(W, P) for W in (1, 2, 3, 5, 8, 32)
 def test_ragged_sizes_and_pad_canaries(W, P, dt):
     """Every ragged size matches the oracle, and the padding columns
     [P, ld) of every row keep their canary bytes."""
+    _ragged_case(W, P, dt, "f32")
+
+
+RAGGED_BF16_GRADS = [(W, P) for W in (1, 3, 8, 32) for P in (1, 5, 1025, 4097, (1 << 20) + 3)]
+
+
+@pytest.mark.parametrize("W,P", RAGGED_BF16_GRADS)
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_ragged_sizes_bf16_gradients(W, P, dt):
+    """The same with bf16 gradient rows (the 64-bit vector loads and the
+    scalar tail of the bf16 gradient path)."""
+    _ragged_case(W, P, dt, "bf16")
+
+
+def _ragged_case(W, P, dt, grad_dt):
     ld = ((P + 127) // 128) * 128 + 128
     c = Case(W=W, P=P, K=2, lr=0.1, mu=0.9, beta=0.5, alpha=1.0, steps=4,
-             param_dt=dt, ld=ld, seed=P * 100 + W)
-    log(f"[ragged] W={W} P={P} dt={dt}")
+             param_dt=dt, ld=ld, seed=P * 100 + W, grad_dt=grad_dt)
+    log(f"[ragged] W={W} P={P} dt={dt} grads={grad_dt}")
     refs = {}
     th0, grads = oracle_inputs(c, np.arange(P))
     oracle.run(th0, grads, W, c.K, c.steps, *c.hyper32(), param_dt=dt,

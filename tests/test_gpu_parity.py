@@ -22,6 +22,16 @@ def test_tiny_every_coordinate(seed):
     run_parity(case_of("tiny", seed))
 
 
+def test_stress_bf16_gradients_sampled():
+    """The stress workload with bf16 gradient rows (bf16 parameters, bf16
+    gradients, fp32 momentum, u and anchor), full size, sampled coordinates,
+    one period."""
+    w = WORKLOADS["stress"]
+    c = case_of("stress", steps=w.K)
+    c.grad_dt = "bf16"
+    run_parity(c, sample_indices(w.P, n_random=1 << 15, seed=42))
+
+
 def test_tiny_long_horizon_every_coordinate():
     """200 periods (400 steps) of the tiny workload, every coordinate compared
     every 20 periods: the anchor accumulates across periods, so this checks
@@ -60,10 +70,23 @@ SMALL = [
          theta_sigma=1.0, grad_sigma=0.1),
     Case(W=1, P=513, K=3, lr=0.1, mu=0.9, beta=0.5, alpha=1.0, steps=9),
     Case(W=2, P=64, K=2, lr=0.1, mu=0.9, beta=0.5, alpha=1.0, steps=6, ld=128),
+    # bf16 gradient rows on the momentum-SGD entry points
+    Case(W=8, P=10_007, K=4, lr=0.1, mu=0.9, beta=0.5, alpha=1.0, steps=8, grad_dt="bf16"),
+    Case(W=5, P=4_099, K=3, lr=0.2, mu=0.9, beta=0.3, alpha=1.0, steps=9, grad_dt="bf16"),
+    Case(W=16, P=2_053, K=8, lr=0.1, mu=0.9, beta=0.6, alpha=1.0, steps=16,
+         outlier_rate=0.01, grad_dt="bf16"),
+    Case(W=32, P=5_003, K=4, lr=0.1, mu=0.9, beta=0.5, alpha=1.0, steps=8,
+         param_dt="bf16", grad_dt="bf16"),
+    Case(W=4, P=3_001, K=2, lr=0.1, mu=0.9, beta=0.0, alpha=1.0, steps=6,
+         method="localsgd", grad_dt="bf16"),
+    Case(W=4, P=3_001, K=1, lr=0.1, mu=0.9, beta=0.0, alpha=1.0, steps=4,
+         method="ddp", grad_dt="bf16"),
 ]
 
 
 @pytest.mark.parametrize("c", SMALL, ids=lambda c: f"W{c.W}-P{c.P}-K{c.K}-{c.param_dt}"
-                         + (f"-T{c.T}" if c.T else ""))
+                         + (f"-T{c.T}" if c.T else "")
+                         + (f"-{c.method}" if c.method != "cpdp" else "")
+                         + ("-bf16grads" if c.grad_dt == "bf16" else ""))
 def test_small_variants(c):
     run_parity(c)
