@@ -84,7 +84,7 @@ def _oracle_slice(w, start: int, n: int, budget_s: float, method: str = "cpdp",
     if w.grad_dt == "bf16":  # the stored bf16 values are the input
         grads = [gen.bf16_round(g) for g in grads]
     grads = [g.astype(np.float64) for g in grads]
-    st = oracle.state_init(th0, w.W, w.param_dt)
+    st = oracle.state_init(th0, w.W, w.param_dt, w.mom_dt)
     mom2 = np.zeros((w.W, n))
     o = OPTIMIZERS.get(optimizer)
     if o is None:
@@ -192,6 +192,8 @@ def main() -> int:
     ap.add_argument("--grad-dtype", default="f32", choices=["f32", "bf16"],
                     help="gradient storage of the flat momentum-SGD path (bf16 halves the "
                          "gradient bytes; parameters keep the workload's type)")
+    ap.add_argument("--mom-dtype", default="f32", choices=["f32", "bf16"],
+                    help="momentum storage of the flat momentum-SGD path")
     ap.add_argument("--row-align-bytes", type=int, default=0,
                     help="round each replica row up to a multiple of this many bytes "
                          "(0 = the workload's default of 1 MiB)")
@@ -209,12 +211,12 @@ def main() -> int:
     from synth import device as sdev
 
     w = WORKLOADS[args.workload]
-    if args.grad_dtype != "f32":
+    if args.grad_dtype != "f32" or args.mom_dtype != "f32":
         if args.plan or args.graph or args.optimizer != "sgd":
-            raise SystemExit("--grad-dtype bf16 runs the flat momentum-SGD path only "
-                             "(no --plan, --graph or --optimizer)")
+            raise SystemExit("--grad-dtype / --mom-dtype bf16 run the flat momentum-SGD path "
+                             "only (no --plan, --graph or --optimizer)")
         import dataclasses
-        w = dataclasses.replace(w, grad_dt=args.grad_dtype)
+        w = dataclasses.replace(w, grad_dt=args.grad_dtype, mom_dt=args.mom_dtype)
     if args.row_align_bytes:
         import dataclasses
         assert args.row_align_bytes % 256 == 0
@@ -227,7 +229,7 @@ def main() -> int:
     if args.plan and args.graph:
         raise SystemExit("--graph captures the flat-buffer path; drop --plan")
     st = None if args.plan else CpdpState(w.W, w.P, w.ld, w.K, w.param_dt, device=dev,
-                                          grad_dt=w.grad_dt)
+                                          grad_dt=w.grad_dt, mom_dt=w.mom_dt)
     h = Hyper.fp32(w.lr, w.mu, w.beta, w.alpha)
     with torch.cuda.stream(stream):
         th = torch.empty(w.P, dtype=torch.float32, device=dev)
@@ -410,6 +412,8 @@ def main() -> int:
         f"_{args.method}_{args.optimizer}"
     if w.grad_dt == "bf16":
         variant += "_bf16grads"
+    if w.mom_dt == "bf16":
+        variant += "_bf16mom"
     if args.plan:
         variant += "_plan"
 
@@ -429,13 +433,15 @@ def main() -> int:
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": ("f32" if (w.param_dt, w.grad_dt) == ("f32", "f32") else
-                  f"{w.param_dt} params, {w.grad_dt} grads, f32 mom/state"),
+        "dtype": ("f32" if (w.param_dt, w.grad_dt, w.mom_dt) == ("f32", "f32", "f32") else
+                  f"{w.param_dt} params, {w.grad_dt} grads, {w.mom_dt} mom, f32 u/anchor"),
         "data": "synthetic",
         "config": {"workload": f"{w.name}: W={w.W} replicas, P={w.P} ({w.param_dt} params"
-                               f"{', bf16 grads' if w.grad_dt == 'bf16' else ''}), "
+                               f"{', bf16 grads' if w.grad_dt == 'bf16' else ''}"
+                               f"{', bf16 momentum' if w.mom_dt == 'bf16' else ''}), "
                                f"K={w.K}, lr={w.lr}, mu={w.mu}, beta={w.beta}, alpha={w.alpha}",
                    "W": w.W, "P": w.P, "ld": w.ld, "K": w.K, "grad_dt": w.grad_dt,
+                   "mom_dt": w.mom_dt,
                    "method": args.method, "optimizer": args.optimizer,
                    "layout": (f"multi-tensor plan: {len(w.tensors)} tensors x {w.W} replicas, "
                               "one allocation each; step 1's gradients every step"

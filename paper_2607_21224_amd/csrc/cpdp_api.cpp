@@ -82,6 +82,8 @@ cpdp::Param param_kind(int dt) { return dt == CPDP_BF16 ? cpdp::Param::BF16 : cp
 
 cpdp::Grad grad_kind(int dt) { return dt == CPDP_BF16 ? cpdp::Grad::BF16 : cpdp::Grad::F32; }
 
+cpdp::Mom mom_kind(int dt) { return dt == CPDP_BF16 ? cpdp::Mom::BF16 : cpdp::Mom::F32; }
+
 cpdp::OptParams plain_sgd(float lr, float mu) {
     cpdp::OptParams o{};
     o.lr = lr;
@@ -230,18 +232,18 @@ int cpdp_state_init(const void* theta0, void* params, void* mom, float* slow_mom
                     float* anchor, int W, int64_t P, int64_t ld, int K, int param_dt,
                     int mom_dt, void* stream) {
     if (int s = check_shape(W, P, ld, K)) return s;
-    if (!is_dtype(param_dt) || mom_dt != CPDP_F32) return CPDP_ERR_DTYPE;
+    if (!is_dtype(param_dt) || !is_dtype(mom_dt)) return CPDP_ERR_DTYPE;
     if (P == 0) return CPDP_OK;
     if (!cpdp::grid_fits(1, P)) return CPDP_ERR_INVALID_ARG;
-    const size_t sp = esize(param_dt);
+    const size_t sp = esize(param_dt), sm = esize(mom_dt);
     const void* ptrs[] = {theta0, params, mom, slow_mom, anchor};
     const Range ranges[] = {vec(theta0, P, sp), rows(params, W, P, ld, sp),
-                            rows(mom, W, P, ld, 4), vec(slow_mom, P, 4), vec(anchor, P, 4)};
-    const size_t row_es[] = {0, sp, 4, 0, 0};
+                            rows(mom, W, P, ld, sm), vec(slow_mom, P, 4), vec(anchor, P, 4)};
+    const size_t row_es[] = {0, sp, sm, 0, 0};
     if (int s = check_pointers(ptrs, ranges, row_es, 5, ld)) return s;
-    return hip_status(cpdp::launch_state_init(param_kind(param_dt), theta0, params,
-                                              static_cast<float*>(mom), nullptr, slow_mom,
-                                              anchor, W, P, ld, stream));
+    return hip_status(cpdp::launch_state_init(param_kind(param_dt), mom_kind(mom_dt), theta0,
+                                              params, mom, nullptr, slow_mom, anchor, W, P, ld,
+                                              stream));
 }
 
 int cpdp_local_step(void* params, void* mom, const void* grads, int W, int64_t P, int64_t ld,
@@ -249,19 +251,19 @@ int cpdp_local_step(void* params, void* mom, const void* grads, int W, int64_t P
                     void* stream) {
     if (int s = check_shape(W, P, ld, K)) return s;
     if (int s = check_lr_mu(lr, mu)) return s;
-    if (!is_dtype(param_dt) || !is_dtype(grad_dt) || mom_dt != CPDP_F32) return CPDP_ERR_DTYPE;
+    if (!is_dtype(param_dt) || !is_dtype(grad_dt) || !is_dtype(mom_dt)) return CPDP_ERR_DTYPE;
     if (P == 0) return CPDP_OK;
     if (!cpdp::grid_fits(W, P)) return CPDP_ERR_INVALID_ARG;
-    const size_t sp = esize(param_dt), sg = esize(grad_dt);
+    const size_t sp = esize(param_dt), sg = esize(grad_dt), sm = esize(mom_dt);
     const void* ptrs[] = {params, mom, grads};
-    const Range ranges[] = {rows(params, W, P, ld, sp), rows(mom, W, P, ld, 4),
+    const Range ranges[] = {rows(params, W, P, ld, sp), rows(mom, W, P, ld, sm),
                             rows(grads, W, P, ld, sg)};
-    const size_t row_es[] = {sp, 4, sg};
+    const size_t row_es[] = {sp, sm, sg};
     if (int s = check_pointers(ptrs, ranges, row_es, 3, ld)) return s;
     return hip_status(cpdp::launch_local_step(cpdp::Opt::SGD, plain_sgd(lr, mu),
-                                              param_kind(param_dt), grad_kind(grad_dt), params,
-                                              static_cast<float*>(mom), nullptr, grads, W, P, ld,
-                                              stream));
+                                              param_kind(param_dt), grad_kind(grad_dt),
+                                              mom_kind(mom_dt), params, mom, nullptr, grads, W,
+                                              P, ld, stream));
 }
 
 int cpdp_reconcile(void* params, void* mom, const void* grads, float* slow_mom, float* anchor,
@@ -271,18 +273,18 @@ int cpdp_reconcile(void* params, void* mom, const void* grads, float* slow_mom, 
     if (int s = check_lr_mu(lr, mu)) return s;
     if (!(beta >= 0.0f && beta < 1.0f)) return CPDP_ERR_INVALID_ARG;
     if (!(finite(alpha) && alpha > 0.0f)) return CPDP_ERR_INVALID_ARG;
-    if (!is_dtype(param_dt) || !is_dtype(grad_dt) || mom_dt != CPDP_F32) return CPDP_ERR_DTYPE;
+    if (!is_dtype(param_dt) || !is_dtype(grad_dt) || !is_dtype(mom_dt)) return CPDP_ERR_DTYPE;
     if (P == 0) return CPDP_OK;
     if (!cpdp::grid_fits(1, P)) return CPDP_ERR_INVALID_ARG;
-    const size_t sp = esize(param_dt), sg = esize(grad_dt);
+    const size_t sp = esize(param_dt), sg = esize(grad_dt), sm = esize(mom_dt);
     const void* ptrs[] = {params, mom, grads, slow_mom, anchor};
-    const Range ranges[] = {rows(params, W, P, ld, sp), rows(mom, W, P, ld, 4),
+    const Range ranges[] = {rows(params, W, P, ld, sp), rows(mom, W, P, ld, sm),
                             rows(grads, W, P, ld, sg), vec(slow_mom, P, 4), vec(anchor, P, 4)};
-    const size_t row_es[] = {sp, 4, sg, 0, 0};
+    const size_t row_es[] = {sp, sm, sg, 0, 0};
     if (int s = check_pointers(ptrs, ranges, row_es, 5, ld)) return s;
     return hip_status(cpdp::launch_sync(cpdp::Sync::CPDP, cpdp::Opt::SGD, plain_sgd(lr, mu),
-                                        param_kind(param_dt), grad_kind(grad_dt), params,
-                                        static_cast<float*>(mom), nullptr, grads, slow_mom,
+                                        param_kind(param_dt), grad_kind(grad_dt),
+                                        mom_kind(mom_dt), params, mom, nullptr, grads, slow_mom,
                                         anchor, W, P, ld, beta, alpha, 0u, stream));
 }
 
@@ -291,20 +293,20 @@ int cpdp_localsgd_sync(void* params, void* mom, const void* grads, float* anchor
                        int grad_dt, int mom_dt, void* stream) {
     if (int s = check_shape(W, P, ld, K)) return s;
     if (int s = check_lr_mu(lr, mu)) return s;
-    if (!is_dtype(param_dt) || !is_dtype(grad_dt) || mom_dt != CPDP_F32) return CPDP_ERR_DTYPE;
+    if (!is_dtype(param_dt) || !is_dtype(grad_dt) || !is_dtype(mom_dt)) return CPDP_ERR_DTYPE;
     if (P == 0) return CPDP_OK;
     if (!cpdp::grid_fits(1, P)) return CPDP_ERR_INVALID_ARG;
-    const size_t sp = esize(param_dt), sg = esize(grad_dt);
+    const size_t sp = esize(param_dt), sg = esize(grad_dt), sm = esize(mom_dt);
     // anchor is optional: validate it only when given
     const int n = anchor != nullptr ? 4 : 3;
     const void* ptrs[] = {params, mom, grads, anchor};
-    const Range ranges[] = {rows(params, W, P, ld, sp), rows(mom, W, P, ld, 4),
+    const Range ranges[] = {rows(params, W, P, ld, sp), rows(mom, W, P, ld, sm),
                             rows(grads, W, P, ld, sg), vec(anchor, P, 4)};
-    const size_t row_es[] = {sp, 4, sg, 0};
+    const size_t row_es[] = {sp, sm, sg, 0};
     if (int s = check_pointers(ptrs, ranges, row_es, n, ld)) return s;
     return hip_status(cpdp::launch_sync(cpdp::Sync::LocalSGD, cpdp::Opt::SGD, plain_sgd(lr, mu),
-                                        param_kind(param_dt), grad_kind(grad_dt), params,
-                                        static_cast<float*>(mom), nullptr, grads, nullptr,
+                                        param_kind(param_dt), grad_kind(grad_dt),
+                                        mom_kind(mom_dt), params, mom, nullptr, grads, nullptr,
                                         anchor, W, P, ld, 0.0f, 1.0f, 0u, stream));
 }
 
@@ -312,18 +314,18 @@ int cpdp_ddp_step(void* params, void* mom, const void* grads, int W, int64_t P, 
                   float lr, float mu, int param_dt, int grad_dt, int mom_dt, void* stream) {
     if (int s = check_shape(W, P, ld, 1)) return s;
     if (int s = check_lr_mu(lr, mu)) return s;
-    if (!is_dtype(param_dt) || !is_dtype(grad_dt) || mom_dt != CPDP_F32) return CPDP_ERR_DTYPE;
+    if (!is_dtype(param_dt) || !is_dtype(grad_dt) || !is_dtype(mom_dt)) return CPDP_ERR_DTYPE;
     if (P == 0) return CPDP_OK;
     if (!cpdp::grid_fits(1, P)) return CPDP_ERR_INVALID_ARG;
-    const size_t sp = esize(param_dt), sg = esize(grad_dt);
+    const size_t sp = esize(param_dt), sg = esize(grad_dt), sm = esize(mom_dt);
     const void* ptrs[] = {params, mom, grads};
-    const Range ranges[] = {rows(params, W, P, ld, sp), rows(mom, W, P, ld, 4),
+    const Range ranges[] = {rows(params, W, P, ld, sp), rows(mom, W, P, ld, sm),
                             rows(grads, W, P, ld, sg)};
-    const size_t row_es[] = {sp, 4, sg};
+    const size_t row_es[] = {sp, sm, sg};
     if (int s = check_pointers(ptrs, ranges, row_es, 3, ld)) return s;
     return hip_status(cpdp::launch_sync(cpdp::Sync::DDP, cpdp::Opt::SGD, plain_sgd(lr, mu),
-                                        param_kind(param_dt), grad_kind(grad_dt), params,
-                                        static_cast<float*>(mom), nullptr, grads, nullptr,
+                                        param_kind(param_dt), grad_kind(grad_dt),
+                                        mom_kind(mom_dt), params, mom, nullptr, grads, nullptr,
                                         nullptr, W, P, ld, 0.0f, 1.0f, 0u, stream));
 }
 
@@ -342,10 +344,9 @@ int cpdp_state_init_opt(const void* theta0, void* params, void* mom, void* mom2,
                             vec(anchor, P, 4),      rows(mom2, W, P, ld, 4)};
     const size_t row_es[] = {0, sp, 4, 0, 0, 4};
     if (int s = check_pointers(ptrs, ranges, row_es, n, ld)) return s;
-    return hip_status(cpdp::launch_state_init(param_kind(param_dt), theta0, params,
-                                              static_cast<float*>(mom),
-                                              static_cast<float*>(mom2), slow_mom, anchor, W, P,
-                                              ld, stream));
+    return hip_status(cpdp::launch_state_init(param_kind(param_dt), cpdp::Mom::F32, theta0,
+                                              params, mom, static_cast<float*>(mom2), slow_mom,
+                                              anchor, W, P, ld, stream));
 }
 
 int cpdp_local_step_opt(void* params, void* mom, void* mom2, const void* grads, int W,
@@ -362,7 +363,7 @@ int cpdp_local_step_opt(void* params, void* mom, void* mom2, const void* grads, 
     const size_t sp = esize(param_dt);
     if (int s = check_local_ptrs(params, mom, mom2, grads, W, P, ld, sp, adam)) return s;
     return hip_status(cpdp::launch_local_step(kind, o, param_kind(param_dt), cpdp::Grad::F32,
-                                              params, static_cast<float*>(mom),
+                                              cpdp::Mom::F32, params, mom,
                                               adam ? static_cast<float*>(mom2) : nullptr, grads,
                                               W, P, ld, stream));
 }
@@ -392,7 +393,7 @@ int cpdp_sync_step_opt(int strategy, void* params, void* mom, void* mom2, void* 
         return s;
     const cpdp::Sync mode = sync_mode(strategy);
     return hip_status(cpdp::launch_sync(mode, kind, o, param_kind(param_dt), cpdp::Grad::F32,
-                                        params, static_cast<float*>(mom),
+                                        cpdp::Mom::F32, params, mom,
                                         static_cast<float*>(m2), grads, slow, anc, W, P, ld,
                                         beta, alpha, flags, stream));
 }

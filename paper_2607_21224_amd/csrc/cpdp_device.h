@@ -11,7 +11,7 @@
 // there is no MFMA and no LDS.  Every thread owns VEC = 4 consecutive
 // coordinates and moves them with 128-bit (fp32) or 64-bit (bf16) vector
 // accesses (parameters, and on the plain momentum-SGD entry points also the
-// gradients, may be stored as bf16); a wavefront therefore touches 1 KiB (fp32) of each array row per
+// gradients and the momentum, may be stored as bf16); a wavefront therefore touches 1 KiB (fp32) of each array row per
 // access, fully coalesced.  Every output element is written by exactly one
 // thread, there are no atomics and no inter-block dependencies, and the
 // cross-replica sums run in a fixed order (replica 0, 1, ..., W-1) inside one
@@ -161,15 +161,17 @@ struct ParamBF16 {
 // OptParams on the host (they depend on the step count only) and enter the
 // arithmetic as fp32 values, as they do in the framework's fp32 tensor ops.
 
-template <Opt O, class PS>
+template <Opt O, class PS, class MS = ParamF32>
 __device__ __forceinline__ float opt_update(const OptParams& o, float th, float& m, float& v,
                                             float g) {
+    // the momentum buffer is stored (rounded to its storage type MS) before
+    // the parameter update reads it, as the framework's in-place buffer does
     if constexpr (O == Opt::SGD) {
-        m = fmaf(o.mu, m, g);
+        m = MS::round(fmaf(o.mu, m, g));
         return PS::round(fmaf(-o.lr, m, th));
     } else if constexpr (O == Opt::SGD_WD) {
         const float d = fmaf(o.wd, th, g);
-        m = fmaf(o.mu, m, d);
+        m = MS::round(fmaf(o.mu, m, d));
         return PS::round(fmaf(-o.lr, m, th));
     } else {
         const float t = PS::round(th * o.decay);
@@ -187,16 +189,17 @@ __device__ __forceinline__ float opt_update(const OptParams& o, float th, float&
 // per replica and tensor, replica-major).  Both expose the same accessors, so
 // the step code below is written once.
 
-template <class PS, class GS_ = ParamF32>
+template <class PS, class GS_ = ParamF32, class MS_ = ParamF32>
 struct Strided {
     using GS = GS_;  // gradient storage type
+    using MS = MS_;  // momentum storage type
     typename PS::T* params;
-    float* mom;
+    typename MS::T* mom;
     float* mom2;
     typename GS::T* grads;
     int64_t ld;
     __device__ __forceinline__ typename PS::T* prm(int i) const { return params + (int64_t)i * ld; }
-    __device__ __forceinline__ float* m(int i) const { return mom + (int64_t)i * ld; }
+    __device__ __forceinline__ typename MS::T* m(int i) const { return mom + (int64_t)i * ld; }
     __device__ __forceinline__ float* v(int i) const { return mom2 + (int64_t)i * ld; }
     __device__ __forceinline__ typename GS::T* g(int i) const { return grads + (int64_t)i * ld; }
 };
@@ -204,6 +207,7 @@ struct Strided {
 template <class PS>
 struct Table {
     using GS = ParamF32;    // plans hold fp32 gradients
+    using MS = ParamF32;    // and fp32 momentum
     const int64_t* params;  // 64-bit device addresses, entry i*n + t
     const int64_t* mom;
     const int64_t* mom2;
@@ -256,32 +260,33 @@ __device__ __forceinline__ int64_t plan_tensor(const PlanView& v, int64_t n, int
 
 // ---- local step: one replica row per block, 4 coordinates per thread -------
 
-template <Opt O, class PS, class GS, bool FULL>
+template <Opt O, class PS, class GS, class MS, bool FULL>
 __device__ __forceinline__ void local_chunk(const OptParams& o, typename PS::T* params,
-                                            float* mom, float* mom2,
+                                            typename MS::T* mom, float* mom2,
                                             const typename GS::T* grads, int n) {
     float g[kVec], m[kVec], v[kVec] = {0.0f, 0.0f, 0.0f, 0.0f}, th[kVec];
     GS::template load<FULL, kNTL>(grads, n, g);
-    load_f32<FULL, kNTL>(mom, n, m);
+    MS::template load<FULL, kNTL>(mom, n, m);
     if constexpr (O == Opt::ADAMW) load_f32<FULL, kNTL>(mom2, n, v);
     PS::template load<FULL, kNTL>(params, n, th);
 #pragma unroll
-    for (int k = 0; k < kVec; ++k) th[k] = opt_update<O, PS>(o, th[k], m[k], v[k], g[k]);
-    store_f32<FULL, kNTS>(mom, n, m);
+    for (int k = 0; k < kVec; ++k) th[k] = opt_update<O, PS, MS>(o, th[k], m[k], v[k], g[k]);
+    MS::template store<FULL, kNTS>(mom, n, m);
     if constexpr (O == Opt::ADAMW) store_f32<FULL, kNTS>(mom2, n, v);
     PS::template store<FULL, kNTS>(params, n, th);
 }
 
-template <Opt O, class PS, class GS = ParamF32>
+template <Opt O, class PS, class GS = ParamF32, class MS = ParamF32>
 __device__ __forceinline__ void local_dispatch(const OptParams& o, typename PS::T* params,
-                                               float* mom, float* mom2,
+                                               typename MS::T* mom, float* mom2,
                                                const typename GS::T* grads, int64_t p0,
                                                int64_t P) {
     if (p0 + kVec <= P)
-        local_chunk<O, PS, GS, true>(o, params + p0, mom + p0, mom2 + p0, grads + p0, kVec);
+        local_chunk<O, PS, GS, MS, true>(o, params + p0, mom + p0, mom2 + p0, grads + p0,
+                                         kVec);
     else
-        local_chunk<O, PS, GS, false>(o, params + p0, mom + p0, mom2 + p0, grads + p0,
-                                      (int)(P - p0));
+        local_chunk<O, PS, GS, MS, false>(o, params + p0, mom + p0, mom2 + p0, grads + p0,
+                                          (int)(P - p0));
 }
 
 // ---- fused synchronisation steps ----------------------------------------------
@@ -344,7 +349,7 @@ __device__ __forceinline__ void step_batch(const OptParams& o, const Rows& r, in
     for (int c = 0; c < C; ++c) {
         if constexpr (M == Sync::LocalSGD)
             Rows::GS::template load<FULL, kNTL>(r.g(i0 + c) + p0, n, g[c]);
-        load_f32<FULL, kNTL>(r.m(i0 + c) + p0, n, m[c]);
+        Rows::MS::template load<FULL, kNTL>(r.m(i0 + c) + p0, n, m[c]);
         if constexpr (kAdam) load_f32<FULL, kNTL>(r.v(i0 + c) + p0, n, v[c]);
         PS::template load<FULL, kNTL>(r.prm(i0 + c) + p0, n, th[c]);
     }
@@ -353,7 +358,8 @@ __device__ __forceinline__ void step_batch(const OptParams& o, const Rows& r, in
 #pragma unroll
         for (int k = 0; k < kVec; ++k) {
             const float gk = M == Sync::LocalSGD ? g[c][k] : z.gbar[k];
-            const float x = opt_update<O, PS>(o, th[c][k], m[c][k], v[c][k], gk);
+            const float x = opt_update<O, PS, typename Rows::MS>(o, th[c][k], m[c][k], v[c][k],
+                                                                 gk);
             if constexpr (M == Sync::CPDP) {
                 z.s[k] += x - z.a[k];
             } else if constexpr (M == Sync::LocalSGD) {
@@ -372,7 +378,7 @@ __device__ __forceinline__ void step_batch(const OptParams& o, const Rows& r, in
                 if constexpr (kAdam) z.vsum[k] += v[c][k];
             }
         } else {
-            store_f32<FULL, kNTS>(r.m(i0 + c) + p0, n, m[c]);
+            Rows::MS::template store<FULL, kNTS>(r.m(i0 + c) + p0, n, m[c]);
             if constexpr (kAdam) store_f32<FULL, kNTS>(r.v(i0 + c) + p0, n, v[c]);
         }
         if constexpr (M == Sync::DDP) PS::template store<FULL, kNTS>(r.prm(i0 + c) + p0, n, th[c]);
@@ -437,7 +443,7 @@ __device__ __forceinline__ void sync_chunk(const OptParams& o, const Rows& r, fl
             z.vsum[k] *= inv_w;
         }
         for (int i = 0; i < nw; ++i) {
-            store_f32<FULL, kNTS>(r.m(i) + p0, n, z.msum);
+            Rows::MS::template store<FULL, kNTS>(r.m(i) + p0, n, z.msum);
             if constexpr (kAdam) store_f32<FULL, kNTS>(r.v(i) + p0, n, z.vsum);
         }
     }
@@ -527,7 +533,7 @@ int launch(void (*kernel)(Args...), int64_t blocks, void* stream,
 
 struct SyncArgs {
     void* params;
-    float* mom;
+    void* mom;          // fp32 or bf16 rows (Mom)
     float* mom2;
     const void* grads;  // fp32 or bf16 rows (Grad)
     float* slow;

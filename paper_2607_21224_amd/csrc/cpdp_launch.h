@@ -10,9 +10,11 @@ namespace cpdp {
 
 enum class Param { F32, BF16 };
 
-// Gradient storage of the flat local and synchronisation steps: fp32, or bf16
-// (momentum SGD without variants only; plans and step tables take fp32).
+// Gradient and momentum storage of the flat local and synchronisation steps:
+// fp32, or bf16 (momentum SGD without variants only; the general optimizers,
+// plans and step tables take fp32).
 enum class Grad { F32, BF16 };
+enum class Mom { F32, BF16 };
 
 // The per-replica optimizer update: momentum SGD, SGD with coupled weight
 // decay, or AdamW.
@@ -45,25 +47,25 @@ enum class Sync { CPDP, LocalSGD, DDP };
 constexpr unsigned kSyncWriteGbar = 1u;
 constexpr unsigned kSyncAverageState = 2u;
 
-int launch_state_init(Param pt, const void* theta0, void* params, float* mom,
+int launch_state_init(Param pt, Mom mt, const void* theta0, void* params, void* mom,
                       float* mom2, float* slow, float* anchor, int W, int64_t P,
                       int64_t ld, void* stream);
 
-int launch_local_step(Opt opt, const OptParams& o, Param pt, Grad gt, void* params,
-                      float* mom, float* mom2, const void* grads, int W,
+int launch_local_step(Opt opt, const OptParams& o, Param pt, Grad gt, Mom mt, void* params,
+                      void* mom, float* mom2, const void* grads, int W,
                       int64_t P, int64_t ld, void* stream);
 
-int launch_sync(Sync mode, Opt opt, const OptParams& o, Param pt, Grad gt, void* params,
-                float* mom, float* mom2, const void* grads, float* slow,
+int launch_sync(Sync mode, Opt opt, const OptParams& o, Param pt, Grad gt, Mom mt,
+                void* params, void* mom, float* mom2, const void* grads, float* slow,
                 float* anchor, int W, int64_t P, int64_t ld, float beta,
                 float alpha, unsigned flags, void* stream);
 
 // launch_sync for one strategy; each is instantiated in its own translation
 // unit (kernels_sync_<strategy>.hip).
 template <Sync M>
-int launch_sync_mode(Opt opt, const OptParams& o, Param pt, Grad gt, void* params, float* mom,
-                     float* mom2, const void* grads, float* slow, float* anchor, int W,
-                     int64_t P, int64_t ld, float beta, float alpha, unsigned flags,
+int launch_sync_mode(Opt opt, const OptParams& o, Param pt, Grad gt, Mom mt, void* params,
+                     void* mom, float* mom2, const void* grads, float* slow, float* anchor,
+                     int W, int64_t P, int64_t ld, float beta, float alpha, unsigned flags,
                      void* stream);
 
 // Multi-tensor plan table in device memory, as 64-bit words:

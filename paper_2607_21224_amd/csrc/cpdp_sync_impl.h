@@ -1,6 +1,6 @@
 // The flat-layout synchronisation kernels (CPDP reconcile, LocalSGD averaging,
-// DDP gradient step) and their dispatch over update rule, parameter type,
-// gradient type and W.  Each strategy is instantiated in a translation unit of its own
+// DDP gradient step) and their dispatch over update rule, parameter,
+// gradient and momentum storage types, and W.  Each strategy is instantiated in a translation unit of its own
 // (kernels_sync_<strategy>.hip) so the three compile in parallel.
 #pragma once
 
@@ -9,9 +9,9 @@
 namespace cpdp {
 namespace {
 
-template <Sync M, Opt O, int WT, class PS, bool EXTRA, class GS>
+template <Sync M, Opt O, int WT, class PS, bool EXTRA, class GS, class MS>
 __global__ __launch_bounds__(kBlock) void sync_kernel(
-    OptParams o, typename PS::T* __restrict__ params, float* __restrict__ mom,
+    OptParams o, typename PS::T* __restrict__ params, typename MS::T* __restrict__ mom,
     float* __restrict__ mom2, GradPtr<EXTRA, GS> __restrict__ grads, float* __restrict__ slow,
     float* __restrict__ anchor, int W, int64_t ld, int64_t P, float beta, float alpha_lr,
     float inv_w, unsigned flags) {
@@ -19,7 +19,7 @@ __global__ __launch_bounds__(kBlock) void sync_kernel(
     if (p0 >= P) return;
     // Strided holds mutable row pointers; without EXTRA no store to the
     // gradient rows is instantiated
-    const Strided<PS, GS> r{params, mom, mom2, const_cast<typename GS::T*>(grads), ld};
+    const Strided<PS, GS, MS> r{params, mom, mom2, const_cast<typename GS::T*>(grads), ld};
     if (p0 + kVec <= P)
         sync_chunk<M, O, WT, PS, true, EXTRA>(o, r, slow, anchor, W, p0, kVec, beta, alpha_lr,
                                               inv_w, flags);
@@ -28,7 +28,8 @@ __global__ __launch_bounds__(kBlock) void sync_kernel(
                                                alpha_lr, inv_w, flags);
 }
 
-template <Sync M, Opt O, int WT, class PS, bool EXTRA = false, class GS = ParamF32>
+template <Sync M, Opt O, int WT, class PS, bool EXTRA = false, class GS = ParamF32,
+          class MS = ParamF32>
 int sync_w(const OptParams& o, const SyncArgs& a) {
     using T = typename PS::T;
     const float alpha_lr = a.alpha * o.lr;
@@ -37,60 +38,67 @@ int sync_w(const OptParams& o, const SyncArgs& a) {
     // mutable (flags != 0), so dropping const here restores the caller's type
     const GradPtr<EXTRA, GS> grads =
         const_cast<typename GS::T*>(static_cast<const typename GS::T*>(a.grads));
-    return launch(sync_kernel<M, O, WT, PS, EXTRA, GS>, blocks_for(a.P), a.stream, o,
-                  static_cast<T*>(a.params), a.mom, a.mom2, grads, a.slow, a.anchor, a.W,
-                  a.ld, a.P, a.beta, alpha_lr, inv_w, a.flags);
+    return launch(sync_kernel<M, O, WT, PS, EXTRA, GS, MS>, blocks_for(a.P), a.stream, o,
+                  static_cast<T*>(a.params), static_cast<typename MS::T*>(a.mom), a.mom2, grads,
+                  a.slow, a.anchor, a.W, a.ld, a.P, a.beta, alpha_lr, inv_w, a.flags);
 }
 
-template <Sync M, Opt O, class PS, class GS = ParamF32>
+template <Sync M, Opt O, class PS, class GS = ParamF32, class MS = ParamF32>
 int sync_t(const OptParams& o, const SyncArgs& a) {
-    if constexpr (std::is_same<GS, ParamF32>::value) {
+    if constexpr (std::is_same<GS, ParamF32>::value && std::is_same<MS, ParamF32>::value) {
         if (a.flags != 0) return sync_w<M, O, 0, PS, true>(o, a);
     }
     switch (a.W) {
-        case 1: return sync_w<M, O, 1, PS, false, GS>(o, a);
-        case 2: return sync_w<M, O, 2, PS, false, GS>(o, a);
-        case 4: return sync_w<M, O, 4, PS, false, GS>(o, a);
-        case 8: return sync_w<M, O, 8, PS, false, GS>(o, a);
-        case 16: return sync_w<M, O, 16, PS, false, GS>(o, a);
-        case 32: return sync_w<M, O, 32, PS, false, GS>(o, a);
-        default: return sync_w<M, O, 0, PS, false, GS>(o, a);
+        case 1: return sync_w<M, O, 1, PS, false, GS, MS>(o, a);
+        case 2: return sync_w<M, O, 2, PS, false, GS, MS>(o, a);
+        case 4: return sync_w<M, O, 4, PS, false, GS, MS>(o, a);
+        case 8: return sync_w<M, O, 8, PS, false, GS, MS>(o, a);
+        case 16: return sync_w<M, O, 16, PS, false, GS, MS>(o, a);
+        case 32: return sync_w<M, O, 32, PS, false, GS, MS>(o, a);
+        default: return sync_w<M, O, 0, PS, false, GS, MS>(o, a);
     }
 }
 
+// bf16 gradients or momentum: momentum SGD without variants only (the
+// validation layer enforces it)
+template <Sync M, class PS>
+int sync_narrow(Grad gt, Mom mt, const OptParams& o, const SyncArgs& a) {
+    if (a.flags != 0) return (int)hipErrorInvalidValue;
+    if (gt == Grad::BF16)
+        return mt == Mom::BF16 ? sync_t<M, Opt::SGD, PS, ParamBF16, ParamBF16>(o, a)
+                               : sync_t<M, Opt::SGD, PS, ParamBF16, ParamF32>(o, a);
+    return sync_t<M, Opt::SGD, PS, ParamF32, ParamBF16>(o, a);
+}
+
 template <Sync M, Opt O>
-int sync_p(Param pt, Grad gt, const OptParams& o, const SyncArgs& a) {
-    if (gt == Grad::BF16) {
-        // bf16 gradients: momentum SGD without variants only (the validation
-        // layer enforces it)
-        if constexpr (O == Opt::SGD) {
-            if (a.flags != 0) return (int)hipErrorInvalidValue;
-            return pt == Param::BF16 ? sync_t<M, O, ParamBF16, ParamBF16>(o, a)
-                                     : sync_t<M, O, ParamF32, ParamBF16>(o, a);
-        }
+int sync_p(Param pt, Grad gt, Mom mt, const OptParams& o, const SyncArgs& a) {
+    if (gt == Grad::BF16 || mt == Mom::BF16) {
+        if constexpr (O == Opt::SGD)
+            return pt == Param::BF16 ? sync_narrow<M, ParamBF16>(gt, mt, o, a)
+                                     : sync_narrow<M, ParamF32>(gt, mt, o, a);
         return (int)hipErrorInvalidValue;
     }
     return pt == Param::BF16 ? sync_t<M, O, ParamBF16>(o, a) : sync_t<M, O, ParamF32>(o, a);
 }
 
 template <Sync M>
-int sync_o(Opt opt, Param pt, Grad gt, const OptParams& o, const SyncArgs& a) {
+int sync_o(Opt opt, Param pt, Grad gt, Mom mt, const OptParams& o, const SyncArgs& a) {
     switch (opt) {
-        case Opt::SGD_WD: return sync_p<M, Opt::SGD_WD>(pt, gt, o, a);
-        case Opt::ADAMW: return sync_p<M, Opt::ADAMW>(pt, gt, o, a);
-        default: return sync_p<M, Opt::SGD>(pt, gt, o, a);
+        case Opt::SGD_WD: return sync_p<M, Opt::SGD_WD>(pt, gt, mt, o, a);
+        case Opt::ADAMW: return sync_p<M, Opt::ADAMW>(pt, gt, mt, o, a);
+        default: return sync_p<M, Opt::SGD>(pt, gt, mt, o, a);
     }
 }
 
 }  // namespace
 
 template <Sync M>
-int launch_sync_mode(Opt opt, const OptParams& o, Param pt, Grad gt, void* params, float* mom,
-                     float* mom2, const void* grads, float* slow, float* anchor, int W,
-                     int64_t P, int64_t ld, float beta, float alpha, unsigned flags,
+int launch_sync_mode(Opt opt, const OptParams& o, Param pt, Grad gt, Mom mt, void* params,
+                     void* mom, float* mom2, const void* grads, float* slow, float* anchor,
+                     int W, int64_t P, int64_t ld, float beta, float alpha, unsigned flags,
                      void* stream) {
     const SyncArgs a{params, mom, mom2, grads, slow, anchor, W, P, ld, beta, alpha, flags, stream};
-    return sync_o<M>(opt, pt, gt, o, a);
+    return sync_o<M>(opt, pt, gt, mt, o, a);
 }
 
 }  // namespace cpdp

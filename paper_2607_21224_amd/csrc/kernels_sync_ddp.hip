@@ -3,8 +3,8 @@
 
 namespace cpdp {
 
-template int launch_sync_mode<Sync::DDP>(Opt, const OptParams&, Param, Grad, void*,
-                                              float*, float*, const void*, float*, float*, int,
+template int launch_sync_mode<Sync::DDP>(Opt, const OptParams&, Param, Grad, Mom, void*,
+                                              void*, float*, const void*, float*, float*, int,
                                               int64_t, int64_t, float, float, unsigned,
                                               void*);
 

@@ -72,10 +72,12 @@ int sync_table_t(const int64_t* table, const SyncArgs& a) {
     const float* grads = static_cast<const float*>(a.grads);
     if (a.flags != 0)
         return launch(sync_table_kernel<M, O, PS, true>, blocks_for(a.P), a.stream, table,
-                      static_cast<T*>(a.params), a.mom, a.mom2, const_cast<float*>(grads),
+                      static_cast<T*>(a.params), static_cast<float*>(a.mom), a.mom2,
+                      const_cast<float*>(grads),
                       a.slow, a.anchor, a.W, a.ld, a.P, inv_w, a.flags);
     return launch(sync_table_kernel<M, O, PS, false>, blocks_for(a.P), a.stream, table,
-                  static_cast<T*>(a.params), a.mom, a.mom2, grads, a.slow, a.anchor, a.W,
+                  static_cast<T*>(a.params), static_cast<float*>(a.mom), a.mom2, grads, a.slow,
+                  a.anchor, a.W,
                   a.ld, a.P, inv_w, a.flags);
 }
 

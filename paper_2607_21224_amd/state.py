@@ -115,14 +115,16 @@ class CpdpState:
     ROW_ALIGN_BYTES = 1 << 20
 
     def __init__(self, W: int, P: int, ld: int | None = None, K: int = 1,
-                 param_dt: str = "f32", device="cuda", grad_dt: str = "f32"):
-        """grad_dt: storage type of the gradient rows the steps take, "f32", or
-        "bf16" for the momentum-SGD steps (local_step, reconcile,
-        localsgd_sync, ddp_step and step()); the general-optimizer and
-        step-table paths take fp32 gradients."""
-        if grad_dt not in ("f32", "bf16"):
-            raise ValueError(f"grad_dt must be 'f32' or 'bf16', got {grad_dt!r}")
-        self.grad_dt = grad_dt
+                 param_dt: str = "f32", device="cuda", grad_dt: str = "f32",
+                 mom_dt: str = "f32"):
+        """grad_dt / mom_dt: storage types of the gradient rows the steps take
+        and of the momentum buffers, "f32", or "bf16" for the momentum-SGD
+        path (init, local_step, reconcile, localsgd_sync, ddp_step, step());
+        the general-optimizer and step-table paths take fp32 for both."""
+        for name, dt in (("grad_dt", grad_dt), ("mom_dt", mom_dt)):
+            if dt not in ("f32", "bf16"):
+                raise ValueError(f"{name} must be 'f32' or 'bf16', got {dt!r}")
+        self.grad_dt, self.mom_dt = grad_dt, mom_dt
         self.W, self.P, self.K = int(W), int(P), int(K)
         esize = 2 if param_dt == "bf16" else 4
         align = self.ROW_ALIGN_BYTES // esize
@@ -130,7 +132,8 @@ class CpdpState:
         self.param_dt = param_dt
         tdt = torch.bfloat16 if param_dt == "bf16" else torch.float32
         self.params = torch.empty((self.W, self.ld), dtype=tdt, device=device)
-        self.mom = torch.empty((self.W, self.ld), dtype=torch.float32, device=device)
+        mdt = torch.bfloat16 if mom_dt == "bf16" else torch.float32
+        self.mom = torch.empty((self.W, self.ld), dtype=mdt, device=device)
         self.slow_mom = torch.empty(max(self.P, 1), dtype=torch.float32, device=device)
         self.anchor = torch.empty(max(self.P, 1), dtype=torch.float32, device=device)
         self.mom2 = None          # AdamW second moments, allocated by init_opt
@@ -146,19 +149,19 @@ class CpdpState:
         self._check_theta0(theta0)
         cpdp.cpdp_state_init(theta0, self.params, self.mom, self.slow_mom,
                              self.anchor, self.W, self.P, self.ld, self.K,
-                             self.param_dt, "f32", _on(stream))
+                             self.param_dt, self.mom_dt, _on(stream))
 
     def local_step(self, grads: torch.Tensor, h: Hyper, stream=None) -> None:
         self._check_grads(grads)
         cpdp.cpdp_local_step(self.params, self.mom, grads, self.W, self.P,
                              self.ld, self.K, h.lr, h.mu, self.param_dt, self.grad_dt,
-                             "f32", _on(stream))
+                             self.mom_dt, _on(stream))
 
     def reconcile(self, grads: torch.Tensor, h: Hyper, stream=None) -> None:
         self._check_grads(grads)
         cpdp.cpdp_reconcile(self.params, self.mom, grads, self.slow_mom,
                             self.anchor, self.W, self.P, self.ld, self.K, h.lr,
-                            h.mu, h.beta, h.alpha, self.param_dt, self.grad_dt, "f32",
+                            h.mu, h.beta, h.alpha, self.param_dt, self.grad_dt, self.mom_dt,
                             _on(stream))
 
     def localsgd_sync(self, grads: torch.Tensor, h: Hyper, stream=None,
@@ -169,13 +172,13 @@ class CpdpState:
         cpdp.cpdp_localsgd_sync(self.params, self.mom, grads,
                                 self.anchor if write_anchor else None, self.W,
                                 self.P, self.ld, self.K, h.lr, h.mu,
-                                self.param_dt, self.grad_dt, "f32", _on(stream))
+                                self.param_dt, self.grad_dt, self.mom_dt, _on(stream))
 
     def ddp_step(self, grads: torch.Tensor, h: Hyper, stream=None) -> None:
         """Synchronous DDP step (Sec. 3.1, Sec. 5.3)."""
         self._check_grads(grads)
         cpdp.cpdp_ddp_step(self.params, self.mom, grads, self.W, self.P,
-                           self.ld, h.lr, h.mu, self.param_dt, self.grad_dt, "f32",
+                           self.ld, h.lr, h.mu, self.param_dt, self.grad_dt, self.mom_dt,
                            _on(stream))
 
     METHODS = ("cpdp", "localsgd", "ddp")
@@ -186,6 +189,9 @@ class CpdpState:
         """Initialisation for a general optimizer (second-moment buffers for
         AdamW are allocated and zeroed too)."""
         self._check_theta0(theta0)
+        if self.mom_dt != "f32":
+            raise ValueError("the general optimizers keep fp32 momentum; "
+                             "this state was made with mom_dt='bf16'")
         if opt.kind == "adamw" and self.mom2 is None:
             self.mom2 = torch.empty_like(self.mom)
         cpdp.cpdp_state_init_opt(theta0, self.params, self.mom,
@@ -335,7 +341,8 @@ class CpdpState:
         stream are included."""
         torch.cuda.synchronize(self.params.device)
         d = {"W": self.W, "P": self.P, "ld": self.ld, "K": self.K,
-             "param_dt": self.param_dt, "grad_dt": self.grad_dt, "opt_step": self.opt_step,
+             "param_dt": self.param_dt, "grad_dt": self.grad_dt, "mom_dt": self.mom_dt,
+             "opt_step": self.opt_step,
              "params": self.params.cpu(), "mom": self.mom.cpu(),
              "slow_mom": self.slow_mom.cpu(), "anchor": self.anchor.cpu()}
         if self.mom2 is not None:
@@ -349,7 +356,7 @@ class CpdpState:
         the kernels trust the state's W and ld, so a mismatched buffer is
         rejected here rather than copied or broadcast."""
         st = cls(d["W"], d["P"], d["ld"], d["K"], d["param_dt"], device=device,
-                 grad_dt=d.get("grad_dt", "f32"))
+                 grad_dt=d.get("grad_dt", "f32"), mom_dt=d.get("mom_dt", "f32"))
         if "mom2" in d:
             st.mom2 = torch.empty_like(st.mom)
         for name in ("params", "mom", "slow_mom", "anchor") + (("mom2",) if "mom2" in d else ()):
@@ -360,9 +367,10 @@ class CpdpState:
     # The ABI takes raw addresses, so these shape checks are what keeps a
     # kernel inside the caller's buffers: they raise, they are not asserts.
     def _check_grads(self, g: torch.Tensor, fp32_only: bool = False) -> None:
-        if fp32_only and self.grad_dt != "f32":
-            raise ValueError("the general-optimizer and step-table paths take fp32 gradients; "
-                             "this state was made with grad_dt='bf16'")
+        if fp32_only and (self.grad_dt, self.mom_dt) != ("f32", "f32"):
+            raise ValueError("the general-optimizer and step-table paths take fp32 gradients "
+                             "and momentum; this state was made with "
+                             f"grad_dt={self.grad_dt!r}, mom_dt={self.mom_dt!r}")
         want = torch.bfloat16 if self.grad_dt == "bf16" else torch.float32
         if g.dtype != want or not g.is_contiguous():
             raise ValueError(f"grads must be a contiguous {want} tensor")

@@ -67,8 +67,9 @@ class Workload:
     beta: float
     alpha: float
     periods: int
-    param_dt: str = "f32"          # "f32" or "bf16"; momentum is f32
+    param_dt: str = "f32"          # "f32" or "bf16"
     grad_dt: str = "f32"           # gradient storage, "f32" or "bf16"
+    mom_dt: str = "f32"            # momentum storage, "f32" or "bf16"
     theta_sigma: float = 0.02
     grad_sigma: float = 1e-3
     outlier_rate: float = 0.0
@@ -98,11 +99,15 @@ class Workload:
     def grad_bytes(self) -> int:
         return 2 if self.grad_dt == "bf16" else 4
 
+    def mom_bytes(self) -> int:
+        return 2 if self.mom_dt == "bf16" else 4
+
     def _replica_bytes(self, adamw: bool) -> int:
         """Per replica-coordinate bytes every step moves: the gradient read,
-        the optimizer state read and written (momentum, plus AdamW's second
-        moment), the parameter read and written."""
-        return self.grad_bytes() + (16 if adamw else 8) + 2 * self.param_bytes()
+        the optimizer state read and written (momentum, plus AdamW's fp32
+        second moment), the parameter read and written."""
+        return (self.grad_bytes() + 2 * self.mom_bytes() + (8 if adamw else 0)
+                + 2 * self.param_bytes())
 
     def reconcile_bytes(self, adamw: bool = False) -> int:
         """Algorithmic HBM bytes of one reconcile: every state tensor read

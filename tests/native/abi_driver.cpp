@@ -43,7 +43,8 @@ int main() {
     EXPECT(cpdp_local_step(pa, mo, gr, W, P, ld, 4, 0.1f, 0.9f, 0, 0, 0, nullptr), CPDP_OK, true);
     EXPECT(cpdp_local_step(pa, mo, gr, W, P, ld, 4, 0.1f, 1.0f, 0, 0, 0, nullptr), CPDP_ERR_INVALID_ARG, false);
     EXPECT(cpdp_state_init(th, pa, mo, u, an, W, P, ld, 4, 0, 0, nullptr), CPDP_OK, true);
-    EXPECT(cpdp_state_init(th, pa, mo, u, an, W, P, ld, 4, 0, 1, nullptr), CPDP_ERR_DTYPE, false);
+    EXPECT(cpdp_state_init(th, pa, mo, u, an, W, P, ld, 4, 0, 1, nullptr), CPDP_OK, true);  // bf16 momentum
+    EXPECT(cpdp_state_init(th, pa, mo, u, an, W, P, ld, 4, 0, 2, nullptr), CPDP_ERR_DTYPE, false);
     EXPECT(cpdp_localsgd_sync(pa, mo, gr, nullptr, W, P, ld, 4, 0.1f, 0.9f, 0, 0, 0, nullptr), CPDP_OK, true);
     EXPECT(cpdp_ddp_step(pa, mo, gr, W, P, ld, 0.1f, 0.9f, 0, 0, 0, nullptr), CPDP_OK, true);
     EXPECT(cpdp_ddp_step(pa, mo, gr, W, P, ld, 0.1f, 0.9f, 0, 1, 0, nullptr), CPDP_OK, true);  // bf16 grads

@@ -6,15 +6,15 @@
 int g_launches = 0;
 
 namespace cpdp {
-int launch_state_init(Param, const void*, void*, float*, float*, float*, float*, int, int64_t,
+int launch_state_init(Param, Mom, const void*, void*, void*, float*, float*, float*, int, int64_t,
                       int64_t, void*) {
     return ++g_launches, 0;
 }
-int launch_local_step(Opt, const OptParams&, Param, Grad, void*, float*, float*, const void*, int,
+int launch_local_step(Opt, const OptParams&, Param, Grad, Mom, void*, void*, float*, const void*, int,
                       int64_t, int64_t, void*) {
     return ++g_launches, 0;
 }
-int launch_sync(Sync, Opt, const OptParams&, Param, Grad, void*, float*, float*, const void*,
+int launch_sync(Sync, Opt, const OptParams&, Param, Grad, Mom, void*, void*, float*, const void*,
                 float*, float*, int, int64_t, int64_t, float, float, unsigned, void*) {
     return ++g_launches, 0;
 }

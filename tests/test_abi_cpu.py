@@ -15,6 +15,18 @@ from paper_2607_21224_amd.build import ROOT
 HEADER = f"{ROOT}/include/cpdp.h"
 
 
+def _gpu_visible() -> bool:
+    import torch
+    return torch.cuda.device_count() > 0
+
+
+# These tests hand the library fake device addresses.  Every call is meant to
+# fail validation, but if one ever passed it would launch a kernel on them:
+# harmless without a GPU, a memory fault with one.  So they run only where no
+# GPU is visible (the CPU suite).
+pytestmark = pytest.mark.skipif(_gpu_visible(), reason="fake device addresses: CPU-only module")
+
+
 def declared_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
@@ -114,8 +126,8 @@ def test_bad_slowmo(kw):
     assert rec(**kw) == E.CPDP_ERR_INVALID_ARG
 
 
-@pytest.mark.parametrize("kw", [dict(pdt=2), dict(gdt=2), dict(gdt=-1), dict(mdt=1),
-                                dict(pdt=-1)])
+@pytest.mark.parametrize("kw", [dict(pdt=2), dict(gdt=2), dict(gdt=-1), dict(mdt=2),
+                                dict(mdt=-1), dict(pdt=-1)])
 def test_bad_dtype(kw):
     assert rec(**kw) == E.CPDP_ERR_DTYPE
     kl = {k: v for k, v in kw.items()}
@@ -138,7 +150,7 @@ def test_bf16_gradients_validated_at_two_bytes():
 
 def test_bad_dtype_init():
     assert ini(pdt=3) == E.CPDP_ERR_DTYPE
-    assert ini(mdt=1) == E.CPDP_ERR_DTYPE
+    assert ini(mdt=2) == E.CPDP_ERR_DTYPE
 
 
 @pytest.mark.parametrize("name", ["params", "mom", "grads", "slow", "anchor"])

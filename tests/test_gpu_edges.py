@@ -5,7 +5,8 @@ import pytest
 import torch
 
 import oracle
-from gpu_harness import Case, GpuRun, compare, log, oracle_inputs, run_parity
+from gpu_harness import (Case, GpuRun, compare, log, oracle_inputs, run_parity,
+                         tolerance_regime)
 from paper_2607_21224_amd import cpdp
 from paper_2607_21224_amd.state import CpdpState, Hyper
 
@@ -28,29 +29,31 @@ RAGGED_BF16_GRADS = [(W, P) for W in (1, 3, 8, 32) for P in (1, 5, 1025, 4097, (
 
 @pytest.mark.parametrize("W,P", RAGGED_BF16_GRADS)
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
-def test_ragged_sizes_bf16_gradients(W, P, dt):
-    """The same with bf16 gradient rows (the 64-bit vector loads and the
-    scalar tail of the bf16 gradient path)."""
-    _ragged_case(W, P, dt, "bf16")
+@pytest.mark.parametrize("mom_dt", ["f32", "bf16"])
+def test_ragged_sizes_bf16_gradients(W, P, dt, mom_dt):
+    """The same with bf16 gradient rows, and fp32 or bf16 momentum (the
+    64-bit vector loads and stores and the scalar tails of the bf16 paths)."""
+    _ragged_case(W, P, dt, "bf16", mom_dt)
 
 
-def _ragged_case(W, P, dt, grad_dt):
+def _ragged_case(W, P, dt, grad_dt, mom_dt="f32"):
     ld = ((P + 127) // 128) * 128 + 128
     c = Case(W=W, P=P, K=2, lr=0.1, mu=0.9, beta=0.5, alpha=1.0, steps=4,
-             param_dt=dt, ld=ld, seed=P * 100 + W, grad_dt=grad_dt)
-    log(f"[ragged] W={W} P={P} dt={dt} grads={grad_dt}")
+             param_dt=dt, ld=ld, seed=P * 100 + W, grad_dt=grad_dt, mom_dt=mom_dt)
+    log(f"[ragged] W={W} P={P} dt={dt} grads={grad_dt} mom={mom_dt}")
     refs = {}
     th0, grads = oracle_inputs(c, np.arange(P))
-    oracle.run(th0, grads, W, c.K, c.steps, *c.hyper32(), param_dt=dt,
+    oracle.run(th0, grads, W, c.K, c.steps, *c.hyper32(), param_dt=dt, mom_dt=mom_dt,
                callback=lambda s, k, st: refs.__setitem__(s, st.copy()))
     g = GpuRun(c)
     canary = torch.tensor(-1280.0, dtype=torch.float32)  # exact in bf16
     g.st.params[:, P:] = canary.to(g.st.params.dtype)
-    g.st.mom[:, P:] = canary
+    g.st.mom[:, P:] = canary.to(g.st.mom.dtype)
     g.grads[:, P:] = canary
     for s in range(1, c.steps + 1):
         g.step(s)
-        compare(g.snapshot(), refs[s], dt, f"W={W} P={P} step {s}", lr=c.hyper32()[0])
+        compare(g.snapshot(), refs[s], tolerance_regime(c), f"W={W} P={P} step {s}",
+                lr=c.hyper32()[0])
     torch.cuda.synchronize()
     assert (g.st.params[:, P:].float() == -1280.0).all()
     assert (g.st.mom[:, P:] == -1280.0).all()

@@ -32,6 +32,16 @@ def test_stress_bf16_gradients_sampled():
     run_parity(c, sample_indices(w.P, n_random=1 << 15, seed=42))
 
 
+def test_stress_all_bf16_replica_state_sampled():
+    """The stress workload with every per-replica family in bf16 (parameters,
+    gradients, momentum; u and anchor fp32), full size, sampled coordinates,
+    one period."""
+    w = WORKLOADS["stress"]
+    c = case_of("stress", steps=w.K)
+    c.grad_dt, c.mom_dt = "bf16", "bf16"
+    run_parity(c, sample_indices(w.P, n_random=1 << 15, seed=7))
+
+
 def test_tiny_long_horizon_every_coordinate():
     """200 periods (400 steps) of the tiny workload, every coordinate compared
     every 20 periods: the anchor accumulates across periods, so this checks
@@ -81,12 +91,23 @@ SMALL = [
          method="localsgd", grad_dt="bf16"),
     Case(W=4, P=3_001, K=1, lr=0.1, mu=0.9, beta=0.0, alpha=1.0, steps=4,
          method="ddp", grad_dt="bf16"),
+    # bf16 momentum buffers (with fp32 or bf16 gradients and parameters)
+    Case(W=8, P=10_007, K=4, lr=0.1, mu=0.9, beta=0.5, alpha=1.0, steps=8, mom_dt="bf16"),
+    Case(W=5, P=4_099, K=3, lr=0.2, mu=0.9, beta=0.3, alpha=1.0, steps=9, grad_dt="bf16",
+         mom_dt="bf16"),
+    Case(W=32, P=5_003, K=4, lr=0.1, mu=0.9, beta=0.5, alpha=1.0, steps=8,
+         param_dt="bf16", grad_dt="bf16", mom_dt="bf16"),
+    Case(W=4, P=3_001, K=2, lr=0.1, mu=0.9, beta=0.0, alpha=1.0, steps=6,
+         method="localsgd", mom_dt="bf16"),
+    Case(W=4, P=3_001, K=1, lr=0.1, mu=0.9, beta=0.0, alpha=1.0, steps=4,
+         method="ddp", grad_dt="bf16", mom_dt="bf16"),
 ]
 
 
 @pytest.mark.parametrize("c", SMALL, ids=lambda c: f"W{c.W}-P{c.P}-K{c.K}-{c.param_dt}"
                          + (f"-T{c.T}" if c.T else "")
                          + (f"-{c.method}" if c.method != "cpdp" else "")
-                         + ("-bf16grads" if c.grad_dt == "bf16" else ""))
+                         + ("-bf16grads" if c.grad_dt == "bf16" else "")
+                         + ("-bf16mom" if c.mom_dt == "bf16" else ""))
 def test_small_variants(c):
     run_parity(c)
