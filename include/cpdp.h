@@ -20,13 +20,15 @@
  *   boundary and ld * sizeof(element) must be a multiple of 16.  The ranges
  *   of different arguments must not overlap.
  *
- * Storage types (param_dt, grad_dt, mom_dt): params CPDP_F32 or CPDP_BF16;
- *   momentum CPDP_F32.  Gradients are CPDP_F32, or CPDP_BF16 on the entry
- *   points that take a grad_dt (cpdp_local_step, cpdp_reconcile,
- *   cpdp_localsgd_sync, cpdp_ddp_step); every other entry point reads fp32
- *   gradients.  All arithmetic is fp32: bf16 values are widened exactly on
- *   load, and bf16 parameters are rounded to nearest-even each time they are
- *   written.  Any other combination returns CPDP_ERR_DTYPE.
+ * Storage types (param_dt, grad_dt, mom_dt): each CPDP_F32 or CPDP_BF16 on
+ *   the entry points that take them (cpdp_state_init: params, momentum;
+ *   cpdp_local_step, cpdp_reconcile, cpdp_localsgd_sync, cpdp_ddp_step: all
+ *   three).  The general-optimizer, plan and step-table entry points take a
+ *   param_dt only and use fp32 gradients and optimizer state.  All arithmetic
+ *   is fp32: bf16 values are widened exactly on load, and every bf16 value is
+ *   rounded to nearest-even when it is written.  The momentum buffer is
+ *   rounded to its storage type before the parameter update reads it (the
+ *   framework's in-place buffer).  Any other code returns CPDP_ERR_DTYPE.
  *
  * Hyperparameters are fp32: lr > 0 and finite (Sec. 3.1), 0 <= mu < 1,
  *   0 <= beta < 1 (Sec. 3.1), alpha > 0 and finite, K >= 1 (Sec. 3.1).
