@@ -58,6 +58,10 @@ int check_pointers(const void* const* ptrs, const Range* ranges, const size_t* e
                    int64_t ld) {
     for (int k = 0; k < n; ++k)
         if (ptrs[k] == nullptr) return CPDP_ERR_NULL;
+    // a range that wraps past the end of the address space cannot be a buffer
+    // (and would slip through the overlap test as an empty range)
+    for (int k = 0; k < n; ++k)
+        if (ranges[k].hi < ranges[k].lo) return CPDP_ERR_INVALID_ARG;
     for (int k = 0; k < n; ++k) {
         if (!aligned16(ptrs[k])) return CPDP_ERR_MISALIGNED;
         if (es[k] != 0 && ((int64_t)(ld * (int64_t)es[k]) & 15) != 0) return CPDP_ERR_MISALIGNED;
@@ -433,7 +437,9 @@ int cpdp_plan_build(cpdp_plan* plan, int64_t plan_bytes, int W, int n, const int
         if (p == nullptr) return CPDP_ERR_NULL;
         if (!aligned16(p)) return CPDP_ERR_MISALIGNED;
         const uintptr_t lo = reinterpret_cast<uintptr_t>(p);
-        ranges.emplace_back(lo, lo + (uintptr_t)(elems * (int64_t)es));
+        const uintptr_t hi = lo + (uintptr_t)(elems * (int64_t)es);
+        if (hi < lo) return CPDP_ERR_INVALID_ARG;
+        ranges.emplace_back(lo, hi);
         return CPDP_OK;
     };
     int64_t chunks = 0, total = 0;
@@ -444,6 +450,9 @@ int cpdp_plan_build(cpdp_plan* plan, int64_t plan_bytes, int W, int n, const int
         cnt[t] = P;
         chunks += (P + per_block - 1) / per_block;
         total += P;
+        // W * chunks blocks must fit one launch; checked as the sum grows so
+        // that it cannot overflow
+        if (chunks > (int64_t)0x7FFFFFFF / W) return CPDP_ERR_INVALID_ARG;
         for (int i = 0; i < W; ++i) {
             const int64_t k = (int64_t)i * n + t;
             tp[k] = (int64_t)reinterpret_cast<uintptr_t>(params[k]);
@@ -466,7 +475,6 @@ int cpdp_plan_build(cpdp_plan* plan, int64_t plan_bytes, int W, int n, const int
             if (int s = add(anchor[t], P, 4)) return s;
     }
     start[n] = chunks;
-    if (chunks > (int64_t)0x7FFFFFFF / W) return CPDP_ERR_INVALID_ARG;
     std::sort(ranges.begin(), ranges.end());
     for (size_t k = 1; k < ranges.size(); ++k)
         if (ranges[k].first < ranges[k - 1].second) return CPDP_ERR_OVERLAP;

@@ -186,6 +186,16 @@ def test_overlap():
     assert ini(theta0=A + 64) == E.CPDP_ERR_OVERLAP
 
 
+def test_wrapping_range_rejected():
+    """A buffer whose byte range would run past the end of the address space
+    is rejected instead of being taken for an empty range (which no overlap
+    test would catch)."""
+    top = (1 << 64) - 4096          # 16 KB of params rows do not fit below 2^64
+    assert rec(params=top) == E.CPDP_ERR_INVALID_ARG
+    assert loc(grads=top) == E.CPDP_ERR_INVALID_ARG
+    assert ini(theta0=top + 2048) == E.CPDP_ERR_INVALID_ARG   # 4000 B past the end
+
+
 def test_p_zero_is_noop_without_pointers():
     assert rec(P=0, params=None, mom=None, grads=None, slow=None, anchor=None) == E.CPDP_OK
     assert loc(P=0, params=None, mom=None, grads=None) == E.CPDP_OK
@@ -366,6 +376,13 @@ def test_plan_build_validation():
     assert _plan_args(params=q) == E.CPDP_ERR_OVERLAP
     far = A + (1 << 44)
     assert _plan_args(anchor=[A + (1 << 30), far, far + (1 << 30)]) == E.CPDP_ERR_OVERLAP
+    # W x chunks blocks must fit one launch: 2 x 2^30 chunks of 1024 coordinates
+    # do not, and the running sum is checked before it could overflow
+    assert _plan_args(n=2, numel=(1 << 40, 1 << 40)) == E.CPDP_ERR_INVALID_ARG
+    assert _plan_args(W=1, n=3, numel=(1 << 57, 1 << 57, 1 << 57)) == E.CPDP_ERR_INVALID_ARG
+    # a tensor range that wraps past the end of the address space
+    top = (1 << 64) - 256
+    assert _plan_args(params=[top] + p[1:]) == E.CPDP_ERR_INVALID_ARG
 
 
 def test_plan_step_validation():
