@@ -177,6 +177,14 @@ def _addr(x) -> int | None:
     return int(x.data_ptr())
 
 
+def _torch_dtypes():
+    import torch
+    return {CPDP_F32: torch.float32, CPDP_BF16: torch.bfloat16}
+
+
+_TORCH_DTYPE = _torch_dtypes()
+
+
 def _esize(dt) -> int:
     return 2 if _dt(dt) == CPDP_BF16 else 4
 
@@ -186,6 +194,10 @@ def _span(x, n_elems: int, dt, name: str):
     storage type dt.  A tensor must hold at least those bytes: the ABI takes
     raw addresses and cannot see a buffer's size, so a short tensor would
     send the kernel past its end."""
+    if hasattr(x, "data_ptr"):
+        want = _TORCH_DTYPE[_dt(dt)]
+        if x.dtype != want:
+            raise ValueError(f"{name}: storage type {want} expected, the tensor is {x.dtype}")
     if hasattr(x, "data_ptr") and n_elems > 0:
         need = n_elems * _esize(dt)
         have = x.numel() * x.element_size()
@@ -432,6 +444,10 @@ def cpdp_step_table_fill(t: cpdp_step_table, table_bytes, opts, betas=None, alph
     """opts: a sequence of cpdp_optimizer (one per step); betas / alphas:
     sequences of floats or None."""
     n = len(opts)
+    # ctypes would zero-fill a short list: every step needs its own values
+    for name, xs in (("betas", betas), ("alphas", alphas)):
+        if xs is not None and len(xs) != n:
+            raise ValueError(f"{name}: {len(xs)} entries for {n} steps")
     arr = (cpdp_optimizer * n)(*opts)
     fb = (ctypes.c_float * n)(*[float(x) for x in betas]) if betas is not None else None
     fa = (ctypes.c_float * n)(*[float(x) for x in alphas]) if alphas is not None else None

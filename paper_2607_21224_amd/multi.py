@@ -16,6 +16,8 @@ class CpdpMultiState:
 
     def __init__(self, W: int, numels, K: int = 1, param_dt: str = "f32",
                  adamw: bool = False, device="cuda"):
+        if param_dt not in ("f32", "bf16"):
+            raise ValueError(f"param_dt must be 'f32' or 'bf16', got {param_dt!r}")
         self.W, self.K, self.param_dt = int(W), int(K), param_dt
         self.numels = [int(x) for x in numels]
         n = self.n = len(self.numels)
@@ -37,13 +39,17 @@ class CpdpMultiState:
         self.opt_step = 0
 
     def init(self, theta0_list, stream=None) -> None:
-        """Algorithm 1 initialisation from per-tensor initial values."""
+        """Algorithm 1 initialisation from per-tensor initial values.  The
+        values are taken in the parameter storage type (rounded to nearest
+        even if given wider), so the reference model starts equal to what
+        every replica holds, as in the flat layout."""
         if len(theta0_list) != self.n:
             raise ValueError(f"expected {self.n} initial tensors, got {len(theta0_list)}")
+        pdt = self.params[0][0].dtype
         for t, (a, th) in enumerate(zip(self.anchor, theta0_list)):
             if th.numel() != self.numels[t]:
                 raise ValueError(f"tensor {t}: {th.numel()} elements, expected {self.numels[t]}")
-            a[: th.numel()].copy_(th.reshape(-1).float())
+            a[: th.numel()].copy_(th.reshape(-1).to(pdt).float())
         torch.cuda.synchronize()
         cpdp.cpdp_state_init_plan(self.plan, _on(stream))
         self.opt_step = 0
@@ -52,13 +58,16 @@ class CpdpMultiState:
              stream=None, method: str = "cpdp", flags: int = 0) -> str:
         """Step t on the gradients currently in self.grads (see
         CpdpState.step_opt)."""
-        self.opt_step += 1
-        c = opt.c_struct(self.opt_step)
+        # the update counter advances only once the library has taken the step
+        c = opt.c_struct(self.opt_step + 1)
         if method == "ddp" or cpdp.cpdp_is_sync_step(t, self.K, T):
             cpdp.cpdp_sync_step_plan(method, self.plan, self.K, c, beta, alpha, flags, _on(stream))
-            return "reconcile"
-        cpdp.cpdp_local_step_plan(self.plan, self.K, c, _on(stream))
-        return "local"
+            kind = "reconcile"
+        else:
+            cpdp.cpdp_local_step_plan(self.plan, self.K, c, _on(stream))
+            kind = "local"
+        self.opt_step += 1
+        return kind
 
     def step_table(self, t: int, table, T: int = 0, stream=None, method: str = "cpdp",
                    flags: int = 0) -> str:

@@ -121,7 +121,7 @@ class CpdpState:
         and of the momentum buffers, "f32", or "bf16" for the momentum-SGD
         path (init, local_step, reconcile, localsgd_sync, ddp_step, step());
         the general-optimizer and step-table paths take fp32 for both."""
-        for name, dt in (("grad_dt", grad_dt), ("mom_dt", mom_dt)):
+        for name, dt in (("param_dt", param_dt), ("grad_dt", grad_dt), ("mom_dt", mom_dt)):
             if dt not in ("f32", "bf16"):
                 raise ValueError(f"{name} must be 'f32' or 'bf16', got {dt!r}")
         self.grad_dt, self.mom_dt = grad_dt, mom_dt
@@ -209,17 +209,20 @@ class CpdpState:
         self._check_grads(grads, fp32_only=True)
         if method not in self.METHODS:
             raise ValueError(method)
-        self.opt_step += 1
-        c = opt.c_struct(self.opt_step)
+        # the update counter advances only once the library has taken the step
+        c = opt.c_struct(self.opt_step + 1)
         mom2 = self.mom2 if opt.kind == "adamw" else None
         if method == "ddp" or cpdp.cpdp_is_sync_step(t, self.K, T):
             cpdp.cpdp_sync_step_opt(method, self.params, self.mom, mom2, grads,
                                     self.slow_mom, self.anchor, self.W, self.P, self.ld,
                                     self.K, c, beta, alpha, flags, self.param_dt, _on(stream))
-            return "reconcile"
-        cpdp.cpdp_local_step_opt(self.params, self.mom, mom2, grads, self.W, self.P,
-                                 self.ld, self.K, c, self.param_dt, _on(stream))
-        return "local"
+            kind = "reconcile"
+        else:
+            cpdp.cpdp_local_step_opt(self.params, self.mom, mom2, grads, self.W, self.P,
+                                     self.ld, self.K, c, self.param_dt, _on(stream))
+            kind = "local"
+        self.opt_step += 1
+        return kind
 
     def step(self, t: int, grads: torch.Tensor, h: Hyper, T: int = 0,
              stream=None, method: str = "cpdp") -> str:
@@ -316,7 +319,6 @@ class CpdpState:
         gradient buffers ``grads`` (refill them between replays).  For
         fixed-scalar steps only: the hyperparameters are baked into the graph.
         Returns (graph, kinds)."""
-        import torch
         for g in grads:
             self._check_grads(g)
         graph = torch.cuda.CUDAGraph()

@@ -418,6 +418,28 @@ def test_binding_rejects_host_and_strided_tensors():
                              [host], None, None)
 
 
+def test_binding_rejects_mistyped_tensors_and_short_lists():
+    """A tensor whose dtype is not the declared storage type of its family
+    would have its bits misread by the kernels; the binding raises instead.
+    A per-step list shorter than the optimizer list would be zero-filled by
+    ctypes; the binding raises instead.  Neither call reaches the library."""
+    import torch
+    f16 = torch.zeros(64, dtype=torch.float16)
+    f32 = torch.zeros(64)
+    with pytest.raises(ValueError, match="storage type"):
+        cpdp.cpdp_local_step(f16, f32, f32, 1, 64, 64, 1, 0.1, 0.9, param_dt="bf16")
+    with pytest.raises(ValueError, match="storage type"):
+        cpdp.cpdp_reconcile(f32, f32, f32, f32, f32, 1, 64, 64, 1, 0.1, 0.9, 0.5, 1.0,
+                            param_dt="bf16")
+    with pytest.raises(ValueError, match="storage type"):
+        cpdp.cpdp_state_init(f16, f32, f32, f32, f32, 1, 64, 64, 1)
+    opts = [opt_struct() for _ in range(3)]
+    with pytest.raises(ValueError, match="betas"):
+        cpdp.cpdp_step_table_fill(cpdp.cpdp_step_table(), 1 << 12, opts, betas=[0.5, 0.5])
+    with pytest.raises(ValueError, match="alphas"):
+        cpdp.cpdp_step_table_fill(cpdp.cpdp_step_table(), 1 << 12, opts, alphas=[1.0] * 4)
+
+
 def test_state_checks_shapes_before_the_library():
     """CpdpState validates buffer shapes, dtypes and devices itself: the ABI
     takes raw addresses and cannot see a too-small gradient buffer."""
@@ -433,6 +455,20 @@ def test_state_checks_shapes_before_the_library():
         st.init(torch.zeros(4))
     with pytest.raises(ValueError, match="device tensors"):  # shapes fine, but host memory
         st.init(torch.zeros(8))
+    with pytest.raises(ValueError, match="param_dt"):
+        CpdpState(2, 8, ld=16, param_dt="fp16", device="cpu")
+
+
+def test_rejected_optimizer_step_leaves_the_step_count():
+    """A step the library rejects is not counted: AdamW's bias correction
+    would otherwise be one step ahead after the caller fixes the call."""
+    import torch
+    from paper_2607_21224_amd.state import CpdpState, Optimizer
+    st = CpdpState(2, 8, ld=16, K=2, device="cpu")
+    opt = Optimizer("sgd", lr=0.1, momentum=0.9)
+    with pytest.raises(ValueError, match="device tensors"):
+        st.step_opt(1, torch.zeros(2, 16), opt)
+    assert st.opt_step == 0
 
 
 def test_linear_scaled_lr_matches_oracle():

@@ -213,3 +213,22 @@ def test_plan_checkpoint_resume_bitwise():
     with pytest.raises(ValueError, match=r"mom2\[1\]\[2\]"):
         c.load_state_dict(bad)
     assert torch.equal(c.gather("params", 0), before)
+
+
+def test_bf16_plan_init_rounds_the_reference_model():
+    """Initial values given wider than bf16 are taken rounded to the parameter
+    type: the reference model starts bitwise equal to every replica (as the
+    flat layout's initialisation from bf16 values does), and equal to the
+    host's round-to-nearest-even of the inputs."""
+    W = 3
+    offs = np.cumsum([0] + NUMELS)
+    th = gen.theta0(5, np.arange(sum(NUMELS)))
+    st = CpdpMultiState(W, NUMELS, 2, param_dt="bf16")
+    st.init([torch.from_numpy(th[offs[t]:offs[t + 1]]).cuda() for t in range(len(NUMELS))])
+    torch.cuda.synchronize()
+    anchor = st.gather("anchor")
+    want = torch.from_numpy(gen.bf16_round(th)).cuda()
+    assert torch.equal(anchor.view(torch.int32), want.view(torch.int32))
+    for i in range(W):
+        assert torch.equal(st.gather("params", i).float().view(torch.int32),
+                           anchor.view(torch.int32)), i
