@@ -113,6 +113,17 @@ def run_oracle(c: Case, idx: np.ndarray, on_step):
                        s, k, st, m2.copy() if o["kind"] == "adamw" else None))
 
 
+def check_sample(idx: np.ndarray, P: int) -> None:
+    """Sampled coordinates must lie in [0, P): the u and anchor vectors have
+    no padding, and an index past their end would trip the bounds assertion
+    of torch's gather kernel on the device (a GPU trap) instead of raising
+    here."""
+    idx = np.asarray(idx)
+    if idx.size and (idx.min() < 0 or idx.max() >= P):
+        raise ValueError(f"sampled coordinates span [{idx.min()}, {idx.max()}], "
+                         f"outside [0, {P})")
+
+
 class GpuRun:
     """The GPU side of a Case: state in HBM, inputs from the device generator."""
 
@@ -161,6 +172,7 @@ class GpuRun:
         if idx is None:
             get = lambda x: x[sl] if x.dim() == 2 else x[:P]  # noqa: E731
         else:
+            check_sample(idx, P)
             ti = torch.from_numpy(idx).to("cuda")
             get = lambda x: x.index_select(x.dim() - 1, ti)  # noqa: E731
         names = ["params", "mom", "slow_mom", "anchor"]
@@ -275,6 +287,8 @@ def run_parity(c: Case, idx: np.ndarray | None = None, stream=None, every: int =
     """Run a Case on both sides and compare after every ``every``-th step
     (and the last)."""
     P = c.P
+    if idx is not None:
+        check_sample(idx, P)
     sel = np.arange(P) if idx is None else idx
     log(f"[parity] {c.method} {c.opt['kind'] if c.opt else 'sgd'} W={c.W} P={P} K={c.K} "
         f"steps={c.steps} dt={c.param_dt} grads={c.grad_dt} mom={c.mom_dt} "

@@ -177,3 +177,35 @@ def test_checkpoint_resume_bitwise(tmp_path, opt):
     got = b.snapshot()
     for k in want:
         assert np.array_equal(got[k], want[k], equal_nan=True), k
+
+
+HUGE = [
+    # one row longer than 2^31 coordinates (fp32: 8.6 GB per row)
+    dict(W=2, P=(1 << 31) + 1027, dt="f32", grad_dt="f32", mom_dt="f32", gib=80),
+    # one row longer than 2^32 coordinates, every replica family in bf16
+    dict(W=1, P=(1 << 32) + 517, dt="bf16", grad_dt="bf16", mom_dt="bf16", gib=110),
+]
+
+
+@pytest.mark.parametrize("h", HUGE, ids=lambda h: f"W{h['W']}-P{h['P']}-{h['dt']}")
+def test_coordinates_beyond_32_bit_indices(h):
+    """Coordinate indices past 2^31 and 2^32 inside one row: the device
+    generator, every kernel's 64-bit index arithmetic and the ragged tail,
+    compared with the oracle on both ends, on 2048 coordinates around each
+    power-of-two boundary and on a random sample, over two periods."""
+    free, _ = torch.cuda.mem_get_info()
+    if free < h["gib"] << 30:
+        pytest.skip(f"needs about {h['gib']} GiB of free device memory, {free >> 30} GiB free")
+    P = h["P"]
+    rng = np.random.default_rng(3)
+    parts = [np.arange(2048), np.arange(P - 2048, P), rng.integers(0, P, 1 << 14)]
+    for b in (1 << 31, 1 << 32):
+        if b < P:
+            parts.append(np.arange(b - 1024, min(b + 1024, P)))
+    idx = np.unique(np.concatenate(parts)).astype(np.int64)
+    c = Case(W=h["W"], P=P, K=2, lr=0.1, mu=0.9, beta=0.5, alpha=1.0, steps=4,
+             param_dt=h["dt"], grad_dt=h["grad_dt"], mom_dt=h["mom_dt"])
+    try:
+        run_parity(c, idx)
+    finally:
+        torch.cuda.empty_cache()

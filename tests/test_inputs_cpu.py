@@ -2,7 +2,7 @@
 SplitMix64 sequence and the statistics its definition fixes, and the workload
 tensor layouts against an independent implementation of the two model
 architectures (Hugging Face ``transformers``, built from configs offline, no
-weights)."""
+weights); and the parity harness's host-side check of sampled coordinates."""
 import numpy as np
 import pytest
 
@@ -117,3 +117,16 @@ def test_vit_s_layout_matches_transformers():
     assert set(blocks.values()) == {per_block}
     assert sum(n for t, n in ours if t.startswith("head.")) == head
     assert WORKLOADS["vit_s"].P == 12 * per_block + head == sum(n for _, n in ours)
+
+
+def test_parity_sample_outside_the_state_is_rejected_on_the_host():
+    """A sampled coordinate at or past P is refused before any device work:
+    u and the anchor have no padding, so torch's gather would hit its
+    device-side bounds assertion (a GPU trap) on it."""
+    import pytest
+    from gpu_harness import Case, check_sample, run_parity
+    c = Case(W=1, P=10, K=2, lr=0.1, mu=0.9, beta=0.5, alpha=1.0, steps=2)
+    for bad in ([0, 9, 10], [-1, 3]):
+        with pytest.raises(ValueError, match="outside"):
+            run_parity(c, np.array(bad))
+    check_sample(np.array([0, 9]), 10)
