@@ -452,7 +452,7 @@ int cpdp_plan_build(cpdp_plan* plan, int64_t plan_bytes, int W, int n, const int
         total += P;
         // W * chunks blocks must fit one launch; checked as the sum grows so
         // that it cannot overflow
-        if (chunks > (int64_t)0x7FFFFFFF / W) return CPDP_ERR_INVALID_ARG;
+        if (chunks > cpdp::kMaxBlocks / W) return CPDP_ERR_INVALID_ARG;
         for (int i = 0; i < W; ++i) {
             const int64_t k = (int64_t)i * n + t;
             tp[k] = (int64_t)reinterpret_cast<uintptr_t>(params[k]);

@@ -258,6 +258,28 @@ __device__ __forceinline__ int64_t plan_tensor(const PlanView& v, int64_t n, int
     return lo;
 }
 
+// ---- XCD-contiguous order of the local step's blocks --------------------------
+//
+// The local step's blocks are the cells (replica row, column of kBlock * kVec
+// coordinates) of a W x columns grid.  The hardware hands workgroup b of a
+// launch to XCD b % kXcds (round robin), and every XCD has its own L2, so in
+// plain replica-major order each XCD would stream every eighth column.  Block
+// b instead takes cell (b % kXcds) * per + b / kXcds of the replica-major order
+// (per = ceil(cells / kXcds)): each XCD streams one contiguous eighth of the
+// state.  The grid is kXcds * per blocks; the few past the last cell exit.
+// (The fused synchronisation steps keep the plain order: every block there
+// already reads all rows at its coordinates, and the remapping was slower.)
+constexpr int kXcds = 8;
+
+inline int64_t xcd_grid(int64_t cells) { return (cells + kXcds - 1) / kXcds * kXcds; }
+
+// the cell of this block, or -1 for a padding block
+__device__ __forceinline__ int64_t xcd_cell(int64_t cells) {
+    const int64_t per = (cells + kXcds - 1) / kXcds;
+    const int64_t c = (int64_t)(blockIdx.x % kXcds) * per + (int64_t)(blockIdx.x / kXcds);
+    return c < cells ? c : -1;
+}
+
 // ---- local step: one replica row per block, 4 coordinates per thread -------
 
 template <Opt O, class PS, class GS, class MS, bool FULL>

@@ -74,7 +74,7 @@ int launch_count_unsynced(Param pt, const void* params, const float* anchor, int
 }
 
 bool grid_fits(int rows, int64_t P) {
-    return rows >= 1 && blocks_for(P) <= (int64_t)0x7FFFFFFF / rows;
+    return rows >= 1 && blocks_for(P) <= kMaxBlocks / rows;
 }
 
 const char* hip_error_string(int err) { return hipGetErrorString((hipError_t)err); }

@@ -43,9 +43,11 @@ template <Opt O, class PS, class GS, class MS>
 __global__ __launch_bounds__(kBlock) void local_step_kernel(
     OptParams o, typename PS::T* __restrict__ params, typename MS::T* __restrict__ mom,
     float* __restrict__ mom2, const typename GS::T* __restrict__ grads, int64_t ld, int64_t P,
-    int64_t blocks_per_row) {
-    const int64_t row = blockIdx.x / blocks_per_row;
-    const int64_t col = blockIdx.x - row * blocks_per_row;
+    int64_t blocks_per_row, int64_t cells) {
+    const int64_t cell = xcd_cell(cells);
+    if (cell < 0) return;
+    const int64_t row = cell / blocks_per_row;
+    const int64_t col = cell - row * blocks_per_row;
     const int64_t p0 = (col * kBlock + threadIdx.x) * kVec;
     if (p0 >= P) return;
     const int64_t off = row * ld;
@@ -66,9 +68,9 @@ int local_step_t(const OptParams& o, void* params, void* mom, float* mom2, const
                  int W, int64_t P, int64_t ld, void* stream) {
     using T = typename PS::T;
     const int64_t bpr = blocks_for(P);
-    return launch(local_step_kernel<O, PS, GS, MS>, bpr * W, stream, o, static_cast<T*>(params),
-                  static_cast<typename MS::T*>(mom), mom2,
-                  static_cast<const typename GS::T*>(grads), ld, P, bpr);
+    return launch(local_step_kernel<O, PS, GS, MS>, xcd_grid(bpr * W), stream, o,
+                  static_cast<T*>(params), static_cast<typename MS::T*>(mom), mom2,
+                  static_cast<const typename GS::T*>(grads), ld, P, bpr, bpr * W);
 }
 
 template <Opt O, class PS>

@@ -57,6 +57,6 @@ int launch_count_unsynced(Param, const void*, const float*, int, int64_t, int64_
 int64_t coords_per_block() { return 1024; }
 int g_uploaded_words = 0;
 int upload_plan(void*, const int64_t*, int64_t words) { return g_uploaded_words = (int)words, 0; }
-bool grid_fits(int rows, int64_t P) { return rows >= 1 && (P + 1023) / 1024 <= 0x7FFFFFFF / rows; }
+bool grid_fits(int rows, int64_t P) { return rows >= 1 && (P + 1023) / 1024 <= kMaxBlocks / rows; }
 const char* hip_error_string(int) { return "stub"; }
 }  // namespace cpdp
