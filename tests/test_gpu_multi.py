@@ -14,21 +14,28 @@ from synth import WORKLOADS, gen
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("name", ["r50_100", "vit_s", "r50_200"])
-def test_plan_equals_flat_model_layouts(name):
+ADAMW_VIT = dict(kind="adamw", lr=5e-4, momentum=0.9, beta2=0.999, eps=1e-8, weight_decay=0.05)
+
+
+@pytest.mark.parametrize("name,opt", [("r50_100", None), ("vit_s", None), ("r50_200", None),
+                                      ("r50_100", ADAMW_VIT)],
+                         ids=["r50_100", "vit_s", "r50_200", "r50_100-adamw"])
+def test_plan_equals_flat_model_layouts(name, opt):
     """The model's tensors (ResNet-50: 161, ViT-S: 146) x W replicas, each its
     own allocation, against the flat buffer on the same seeded inputs over two
-    periods: bitwise equal after every step."""
+    periods: bitwise equal after every step (momentum SGD, and AdamW with its
+    second moments, whose local steps take another block order)."""
     w = WORKLOADS[name]
     numels = [x for _, x in w.tensors]
     offs = np.cumsum([0] + numels)
     c = Case(W=w.W, P=w.P, K=w.K, lr=w.lr, mu=w.mu, beta=w.beta, alpha=w.alpha,
-             steps=2 * w.K, ld=w.ld, outlier_rate=w.outlier_rate)
-    log(f"[multi] {name} layout: {len(numels)} tensors, W={c.W}")
+             steps=2 * w.K, ld=w.ld, outlier_rate=w.outlier_rate, opt=opt)
+    log(f"[multi] {name} layout: {len(numels)} tensors, W={c.W}, "
+        f"{opt['kind'] if opt else 'sgd'}")
     flat = GpuRun(c)
-    multi = CpdpMultiState(c.W, numels, c.K)
+    multi = CpdpMultiState(c.W, numels, c.K, adamw=opt is not None)
     multi.init([flat.st.anchor[offs[t]:offs[t + 1]] for t in range(len(numels))])
-    opt = Optimizer("sgd", flat.h.lr, flat.h.mu)
+    opt = flat.opt if opt is not None else Optimizer("sgd", flat.h.lr, flat.h.mu)
     for s in range(1, c.steps + 1):
         kind = flat.step(s)
         for i in range(c.W):
@@ -39,6 +46,8 @@ def test_plan_equals_flat_model_layouts(name):
         for i in range(c.W):
             assert torch.equal(multi.gather("params", i), flat.st.params[i, :c.P]), (s, i)
             assert torch.equal(multi.gather("mom", i), flat.st.mom[i, :c.P]), (s, i)
+            if flat.st.mom2 is not None:
+                assert torch.equal(multi.gather("mom2", i), flat.st.mom2[i, :c.P]), (s, i)
         assert torch.equal(multi.gather("slow_mom"), flat.st.slow_mom[:c.P]), s
         assert torch.equal(multi.gather("anchor"), flat.st.anchor[:c.P]), s
 
