@@ -229,7 +229,7 @@ def main() -> int:
     if args.plan and args.graph:
         raise SystemExit("--graph captures the flat-buffer path; drop --plan")
     st = None if args.plan else CpdpState(w.W, w.P, w.ld, w.K, w.param_dt, device=dev,
-                                          grad_dt=w.grad_dt, mom_dt=w.mom_dt)
+                                          grad_dt=w.grad_dt, mom_dt=w.mom_dt, adamw=adamw)
     h = Hyper.fp32(w.lr, w.mu, w.beta, w.alpha)
     with torch.cuda.stream(stream):
         th = torch.empty(w.P, dtype=torch.float32, device=dev)

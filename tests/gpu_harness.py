@@ -132,7 +132,8 @@ class GpuRun:
         self.c = c
         self.stream = stream
         self.st = CpdpState(c.W, c.P, c.ld, c.K, c.param_dt, device="cuda", grad_dt=c.grad_dt,
-                            mom_dt=c.mom_dt)
+                            mom_dt=c.mom_dt,
+                            adamw=c.opt is not None and c.opt["kind"] == "adamw")
         self.h = Hyper(*c.hyper32())
         self.opt = Optimizer(**c.opt32()) if c.opt is not None else None
         self.grads = torch.empty((c.W, self.st.ld), dtype=torch.float32,

@@ -563,3 +563,13 @@ def test_binding_rejects_tensors_smaller_than_the_call_touches():
     with pytest.raises(ValueError, match=r"grads\[1\]"):
         cpdp.cpdp_plan_build(cpdp.cpdp_plan(), 1 << 12, 2, 1, [64], a[:2], a[2:4], None,
                              [a[4], t63], None, None)
+
+
+def test_state_reserves_adamw_rows_when_asked():
+    """adamw=True allocates the second-moment rows with the state (same shape
+    and type as the momentum rows); by default they wait for init_opt."""
+    from paper_2607_21224_amd.state import CpdpState
+    st = CpdpState(3, 10, ld=16, K=2, device="cpu", adamw=True)
+    assert st.mom2 is not None and st.mom2.shape == st.mom.shape
+    assert st.mom2.dtype == st.mom.dtype
+    assert CpdpState(3, 10, ld=16, K=2, device="cpu").mom2 is None
