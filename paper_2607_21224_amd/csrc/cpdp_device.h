@@ -268,8 +268,8 @@ __device__ __forceinline__ int64_t plan_tensor(const PlanView& v, int64_t n, int
 // (per = ceil(cells / kXcds)): each XCD streams one contiguous eighth of the
 // state.  The grid is kXcds * per blocks; the few past the last cell exit.
 // The order pays off for the momentum-SGD updates (3 read and 2 write rows
-// per replica); AdamW's local step (4 read and 3 write rows, two waves per
-// SIMD) measured level or about 1 % slower with it and keeps the plain order,
+// per replica); AdamW's local step (4 read and 3 write rows) measured level
+// or about 1 % slower with it and keeps the plain order,
 // as do the fused synchronisation steps, where every block already reads all
 // rows at its coordinates and the remapping was slower.
 constexpr int kXcds = 8;
