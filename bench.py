@@ -32,16 +32,26 @@ HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, published
 MALL_EVICT_BYTES = 512 << 20  # twice the 256 MB MALL
 
 
+def _code_only(text: str) -> str:
+    """Source text without its comments and with whitespace runs collapsed:
+    an edit to a comment or to the layout does not change a kernel."""
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
 def kernel_source_hash() -> str:
-    """Hash of the sources that decide what the kernels read and write: the
+    """Hash of the code that decides what the kernels read and write: the
     kernel translation units with their launch shapes and dispatch, the
-    shared device code and the launch interface.  (Host validation in
-    cpdp_api.cpp does not change a kernel's traffic.)"""
+    shared device code and the launch interface, comments and layout
+    ignored.  (Host validation in cpdp_api.cpp does not change a kernel's
+    traffic.)"""
     from paper_2607_21224_amd.build import KERNEL_HEADERS, KERNEL_SOURCES
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2607_21224_amd", "csrc")
     for f in (*KERNEL_SOURCES, *KERNEL_HEADERS):
-        h.update(open(os.path.join(csrc, f), "rb").read())
+        h.update(f.encode() + b"\0")
+        h.update(_code_only(open(os.path.join(csrc, f)).read()).encode())
     return h.hexdigest()[:16]
 
 

@@ -67,3 +67,12 @@ def test_traffic_summaries_name_their_sources():
         found += 1
     assert found >= 9
     assert bench.recorded_traffic("reconcile", "no_such_workload") is None
+
+
+def test_source_hash_ignores_comments_and_layout_only():
+    code = "int a = 1; // the count\n/* block\n comment */ float b;\n"
+    assert bench._code_only(code) == "int a = 1; float b;"
+    assert bench._code_only("int  a =\n 1;   float b;") == bench._code_only(code)
+    assert bench._code_only(code.replace("1", "2")) != bench._code_only(code)
+    h = bench.kernel_source_hash()
+    assert len(h) == 16 and h == bench.kernel_source_hash()
