@@ -31,3 +31,15 @@ def test_theta0_and_bf16_rounding():
     assert np.array_equal(th.cpu().numpy(), want)
     bf = th.to(torch.bfloat16).float().cpu().numpy()
     assert np.array_equal(bf, gen.bf16_round(want))
+
+
+@pytest.mark.parametrize("n", [1, 3, 4, 5, 1023, 1024, 1025, 4097, 8 * 1024 + 4, (1 << 20) + 3])
+def test_reference_copy_ragged_sizes(n):
+    """The bandwidth-reference copy moves exactly src[:n] into dst[:n] (every
+    XCD eighth and the ragged tail) and leaves the bytes after n untouched."""
+    src = torch.arange(n + 64, dtype=torch.float32, device="cuda") + 0.5
+    dst = torch.full((n + 64,), -7.0, dtype=torch.float32, device="cuda")
+    sdev.copy_f32(dst, src, n)
+    torch.cuda.synchronize()
+    assert torch.equal(dst[:n], src[:n])
+    assert (dst[n:] == -7.0).all()
