@@ -37,12 +37,24 @@ def load_exact(dst: torch.Tensor, src, name: str) -> None:
     dst.copy_(src)
 
 
+# torch's raw handle of the current stream (no Stream object built per call)
+_raw_current_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+_has_gpu = None  # torch.cuda.is_available(), asked once per process
+
+
 def _on(stream):
     """The stream a launch goes to: the one given, else torch's current
     stream, so work inside ``torch.cuda.stream(s)`` (or a graph capture on
     ``s``) stays ordered with the rest of that stream."""
-    if stream is not None or not torch.cuda.is_available():
-        return stream  # without a GPU the binding rejects the buffers itself
+    global _has_gpu
+    if stream is not None:
+        return stream
+    if _has_gpu is None:
+        _has_gpu = torch.cuda.is_available()
+    if not _has_gpu:
+        return None  # without a GPU the binding rejects the buffers itself
+    if _raw_current_stream is not None:
+        return _raw_current_stream(torch.cuda.current_device())
     return torch.cuda.current_stream()
 
 
