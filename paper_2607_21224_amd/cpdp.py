@@ -185,25 +185,31 @@ def _torch_dtypes():
 _TORCH_DTYPE = _torch_dtypes()
 
 
-def _esize(dt) -> int:
-    return 2 if _dt(dt) == CPDP_BF16 else 4
-
-
 def _span(x, n_elems: int, dt, name: str):
     """Address of a buffer argument the call touches for n_elems elements of
-    storage type dt.  A tensor must hold at least those bytes: the ABI takes
-    raw addresses and cannot see a buffer's size, so a short tensor would
-    send the kernel past its end."""
-    if hasattr(x, "data_ptr"):
-        want = _TORCH_DTYPE[_dt(dt)]
-        if x.dtype != want:
-            raise ValueError(f"{name}: storage type {want} expected, the tensor is {x.dtype}")
-    if hasattr(x, "data_ptr") and n_elems > 0:
-        need = n_elems * _esize(dt)
+    storage type dt.  A tensor must have that storage type, live on the GPU
+    (a host tensor's address would be dereferenced by a kernel), be
+    contiguous (the ABI's layouts are dense rows of stride ld) and hold at
+    least those bytes: the ABI takes raw addresses and cannot see a buffer's
+    size, so a short tensor would send the kernel past its end.  (An unknown
+    storage-type code is left to the library, which rejects it before any
+    launch.)"""
+    if x is None or isinstance(x, int):
+        return x
+    code = DTYPES[dt] if isinstance(dt, str) else int(dt)
+    want = _TORCH_DTYPE.get(code)
+    if want is not None and x.dtype is not want:
+        raise ValueError(f"{name}: storage type {want} expected, the tensor is {x.dtype}")
+    if n_elems > 0:
+        need = n_elems * (2 if code == CPDP_BF16 else 4)
         have = x.numel() * x.element_size()
         if have < need:
             raise ValueError(f"{name}: the call touches {need} bytes, the tensor holds {have}")
-    return _addr(x)
+    if not x.is_cuda:
+        raise ValueError(f"CPDP buffers must be device tensors, got one on {x.device}")
+    if not x.is_contiguous():
+        raise ValueError("CPDP buffers must be contiguous tensors")
+    return x.data_ptr()
 
 
 def _rows(x, W, P, ld, dt, name: str):
