@@ -206,6 +206,18 @@ def test_coordinates_beyond_32_bit_indices(h):
     c = Case(W=h["W"], P=P, K=2, lr=0.1, mu=0.9, beta=0.5, alpha=1.0, steps=4,
              param_dt=h["dt"], grad_dt=h["grad_dt"], mom_dt=h["mom_dt"])
     try:
-        run_parity(c, idx)
+        g = run_parity(c, idx)
+        # the consistency check over the same rows: the run ended on a
+        # reconcile, so every replica holds the reference model; one replica
+        # changed at one coordinate past the last power-of-two boundary counts 1
+        st = g.st
+        assert st.count_unsynced() == 0
+        p = P - 3
+        i = c.W - 1
+        old = st.params[i, p].clone()
+        st.params[i, p] = old + 1.0
+        assert st.count_unsynced() == 1
+        st.params[i, p] = old
+        assert st.count_unsynced() == 0
     finally:
         torch.cuda.empty_cache()
