@@ -24,6 +24,24 @@ RTOL_F32, ATOL_F32 = 1e-6, 1e-7
 # bf16 replica parameters: relative 1e-2 (atol only for exact-zero refs)
 RTOL_BF16, ATOL_BF16 = 1e-2, 1e-5
 
+# bf16 rounding flips.  A bf16 rounding of the fp32 device path and of the fp64
+# oracle fall on different sides of a tie with probability about 2^-16, so a
+# coordinate sees a flip in one of its W x steps roundings only rarely, two
+# (2e-5 of the stress coordinates over its run) very rarely, four (an expected
+# 5e-3 coordinates of the whole stress run) practically never.  The flip
+# allowance of the fp32 state driven by bf16 replicas therefore has two tiers:
+# the tight one (two flips' worth) holds for all but BF16_TIGHT_EXCEPTIONS of
+# the elements compared, the loose one everywhere.  The loose one is four
+# flips with their persistence.  A flip moves the replica mean of its period
+# by e (one bf16 ulp / W) and enters the error d of u twice, d_r = beta d_{r-1}
+# - beta d_{r-2} + (e_{r-1} - e_r) / lr (alpha = 1), whose summed impulse
+# response S(beta) is 2.64 at beta = 0.5 and 4.61 at 0.7: per flip u moves by
+# at most 2 S e / lr and the anchor (a_r = mean_r - beta lr u_{r-1}) by at most
+# (1 + 2 beta S) e.  Four flips at beta <= 0.7 stay within 18.4 (u) and 14.9
+# (anchor) times the two-flip tier, under BF16_LOOSE_FACTOR.
+BF16_TIGHT_EXCEPTIONS = 1e-4
+BF16_LOOSE_FACTOR = 20.0
+
 
 @dataclass
 class Case:
@@ -212,6 +230,7 @@ def compare(gpu: dict, ref: "oracle.OracleState", param_dt: str, tag: str,
     for name, want in pairs:
         got = gpu[name]
         assert got.shape == want.shape, (tag, name, got.shape, want.shape)
+        flip = None  # the two-flip allowance of a bf16-regime family, if it has one
         if param_dt == "f32":
             rtol, atol = RTOL_F32, ATOL_F32
             if scaled and name in ("mom", "mom2"):
@@ -225,9 +244,9 @@ def compare(gpu: dict, ref: "oracle.OracleState", param_dt: str, tag: str,
             fa = ref.anchor[np.isfinite(ref.anchor)]
             a_rms = float(np.sqrt(np.mean(fa ** 2))) if fa.size else 0.0
             rtol = RTOL_BF16
-            atol = ATOL_BF16 + (2.0 / ref.W) * 2.0 ** -7 * np.maximum(
-                np.abs(ref.anchor), a_rms)[None, :]
-            atol = np.broadcast_to(atol, want.shape)
+            flip = np.broadcast_to((2.0 / ref.W) * 2.0 ** -7 * np.maximum(
+                np.abs(ref.anchor), a_rms)[None, :], want.shape)
+            atol = ATOL_BF16 + flip
         else:
             # fp32 state driven by bf16 replicas: a one-ulp bf16 flip of one
             # replica (ulp <= 2^-7 |x|) moves the mean by up to 2^-7 |x| / W
@@ -255,6 +274,15 @@ def compare(gpu: dict, ref: "oracle.OracleState", param_dt: str, tag: str,
         lim = atol_f + rtol * np.abs(want[fin])
         margins[name] = float(np.max(err / lim)) if err.size else 0.0
         bad = err > lim
+        if bad.any() and flip is not None:
+            # rare multi-flip coordinates: within the loose tier, and few
+            flip_f = np.broadcast_to(flip, want.shape)[fin]
+            loose = lim + (BF16_LOOSE_FACTOR - 1.0) * flip_f
+            allowed = int(BF16_TIGHT_EXCEPTIONS * bad.size)
+            if int(bad.sum()) <= allowed and not (err > loose).any():
+                margins[name] = float(np.max(err / loose))
+                margins[name + " tight-tier exceptions"] = int(bad.sum())
+                bad = np.zeros_like(bad)
         if bad.any():
             k = np.argmax(err - lim)
             raise AssertionError(
