@@ -18,7 +18,8 @@
  *   All pointers are device pointers owned by the caller; the library never
  *   allocates, frees or keeps them.  Each family must start on a 16-byte
  *   boundary and ld * sizeof(element) must be a multiple of 16.  The ranges
- *   of different arguments must not overlap.
+ *   of different arguments must not overlap (CPDP_ERR_OVERLAP), and a range
+ *   that would run past the end of the address space is CPDP_ERR_INVALID_ARG.
  *
  * Storage types (param_dt, grad_dt, mom_dt): each CPDP_F32 or CPDP_BF16 on
  *   the entry points that take them (cpdp_state_init: params, momentum;
