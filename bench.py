@@ -8,12 +8,13 @@ All state and the K per-step gradient buffers are resident in HBM before the
 timed region starts (gradients stand in for the backward pass and are reused
 period to period: the kernels' cost does not depend on the values).
 
-Prints one JSON line.  value = replica-parameter updates per second over the
-whole period (W * P * K / t_period).  The reconcile and local-step kernels are
-also reported on their own (replica-params/s, algorithmic GB/s, fraction of
-the 8 TB/s HBM peak), each kernel's duration measured with HIP events on the
-stream it runs on.  cpu_baseline times the CPU oracle on a bounded sample of
-the same workload on this host.
+Prints one JSON line.  value = replica-params/s of the synchronisation kernel
+(W * P / t_reconcile for CPDP), the kernel the metric names; the whole period's
+rate (W * P * K / t_period) is reported beside it.  The reconcile and
+local-step kernels are each reported with replica-params/s, algorithmic GB/s
+and the fraction of the 8 TB/s HBM peak, their durations measured with HIP
+events on the stream they run on.  cpu_baseline times the CPU oracle on a
+bounded sample of the same workload on this host.
 """
 from __future__ import annotations
 
@@ -136,44 +137,219 @@ def _oracle_slice(w, start: int, n: int, budget_s: float, method: str = "cpdp",
             return out
 
 
+def cpu_threads() -> dict:
+    """Host cores the parallel oracle leg may use: the CPUs in this process's
+    affinity set, capped by the CPU share the environment grants the job
+    (OMP_NUM_THREADS, when set), with the counts behind the choice."""
+    affinity = len(os.sched_getaffinity(0))
+    share = os.environ.get("OMP_NUM_THREADS", "")
+    cap = int(share) if share.isdigit() and int(share) > 0 else None
+    used = min(affinity, cap) if cap else affinity
+    return {"threads": max(1, used), "host_cpu_count": os.cpu_count(),
+            "affinity_cpus": affinity, "omp_num_threads": cap}
+
+
 def cpu_baseline(w, budget_s: float = 10.0, n_coords: int = 1 << 18,
                  parallel_budget_s: float = 5.0, method: str = "cpdp",
                  optimizer: str = "sgd") -> dict:
-    """The oracle as it stands on the first n_coords coordinates of the
-    workload (coordinates are independent), repeating whole periods until
-    budget_s has elapsed, on one thread.  A second leg runs the same oracle
-    on one independent coordinate slice per thread (ctypes releases the GIL),
-    with as many threads as this process may use, capped at 16."""
+    """The oracle as it stands on bounded samples of the workload
+    (coordinates are independent), repeating whole periods of the strategy
+    and optimizer being benchmarked.  value is the oracle's rate on the
+    synchronisation step the metric names (W * coordinates / seconds spent in
+    it), summed over one independent n_coords slice per host thread on every
+    core this job may use (cpu_threads(); ctypes releases the GIL during each
+    oracle call).  A single-thread leg on the first n_coords coordinates
+    gives the per-core rate and the per-call times extrapolated to the full P;
+    both legs also report the whole-period rate."""
     from concurrent.futures import ThreadPoolExecutor
 
     n = min(n_coords, w.P)
+
+    def rates(r):
+        return (w.W * n * r["rec_n"] / r["rec_s"], w.W * n * w.K * r["periods"] / r["elapsed"])
+
     r = _oracle_slice(w, 0, n, budget_s, method, optimizer)
-    el = r["elapsed"]
     scale = w.P / n  # per-call seconds extrapolated to the whole workload
-    out = {"value": w.W * n * w.K * r["periods"] / el, "unit": "replica-params/s",
-           "cores": 1, "kind": "oracle",
-           "sample": f"first {n} of {w.P} coordinates of {w.name}, W={w.W}, "
-                     f"{r['periods']} periods of K={w.K} steps ({method}, {optimizer}), "
-                     f"fp64 C oracle, 1 thread, "
-                     f"{el:.1f} s",
-           "s_per_reconcile_full_P": round(r["rec_s"] / max(r["rec_n"], 1) * scale, 4),
-           "s_per_local_step_full_P": (round(r["loc_s"] / r["loc_n"] * scale, 4)
-                                       if r["loc_n"] else None),
-           "extrapolated": w.P > n}
-    if parallel_budget_s > 0:
-        threads = max(1, min(16, len(os.sched_getaffinity(0))))
-        with ThreadPoolExecutor(threads) as ex:
-            t0 = time.perf_counter()
-            parts = list(ex.map(lambda k: _oracle_slice(w, k * n, n, parallel_budget_s,
-                                                        method, optimizer),
-                                range(threads)))
-            wall = time.perf_counter() - t0
-        done = sum(p["periods"] for p in parts)
-        out["parallel"] = {"value": w.W * n * w.K * done / wall, "unit": "replica-params/s",
-                           "cores": threads,
-                           "sample": f"{threads} threads, each on its own {n}-coordinate "
-                                     f"slice, {done} periods in {wall:.1f} s"}
-    return out
+    sync_rate, period_rate = rates(r)
+    single = {"value": sync_rate, "unit": "replica-params/s", "cores": 1,
+              "period_replica_params_per_s": period_rate,
+              "sample": f"first {n} of {w.P} coordinates of {w.name}, W={w.W}, "
+                        f"{r['periods']} periods of K={w.K} steps ({method}, {optimizer}), "
+                        f"fp64 C oracle, 1 thread, {r['elapsed']:.1f} s",
+              "s_per_reconcile_full_P": round(r["rec_s"] / max(r["rec_n"], 1) * scale, 4),
+              "s_per_local_step_full_P": (round(r["loc_s"] / r["loc_n"] * scale, 4)
+                                          if r["loc_n"] else None),
+              "extrapolated": w.P > n}
+    if parallel_budget_s <= 0:
+        return {**single, "kind": "oracle"}
+    ct = cpu_threads()
+    threads = ct["threads"]
+    with ThreadPoolExecutor(threads) as ex:
+        t0 = time.perf_counter()
+        parts = list(ex.map(lambda k: _oracle_slice(w, k * n, n, parallel_budget_s,
+                                                    method, optimizer),
+                            range(threads)))
+        wall = time.perf_counter() - t0
+    done = sum(p["periods"] for p in parts)
+    return {"value": sum(rates(p)[0] for p in parts), "unit": "replica-params/s",
+            "cores": threads, "kind": "oracle",
+            "period_replica_params_per_s": w.W * n * w.K * done / wall,
+            "sample": f"{threads} threads, each running whole periods of K={w.K} steps "
+                      f"({method}, {optimizer}) of the fp64 C oracle on its own "
+                      f"{n}-coordinate slice of {w.name} (W={w.W}); {done} periods in "
+                      f"{wall:.1f} s; value sums each thread's rate over the time it spent "
+                      f"in the synchronisation step",
+            **{k: v for k, v in ct.items() if k != "threads"},
+            "single_thread": single}
+
+
+def sync_shape_rows(st, grads, method: str, adamw: bool):
+    """The rows the synchronisation kernel of ``method`` reads and writes on
+    the flat state, in its order (gradient rows, then each replica's
+    optimizer state and parameters, then SlowMo state and anchor), for the
+    traffic-shape kernel.  Rows the kernel updates are written back in place;
+    LocalSGD's anchor is written only."""
+    from synth.device import ShapeRow
+    W, ld = st.W, st.ld
+    rows = [] if method == "localsgd" else [ShapeRow(grads, i * ld) for i in range(W)]
+    for i in range(W):
+        if method == "localsgd":
+            rows.append(ShapeRow(grads, i * ld))
+        rows.append(ShapeRow(st.mom, i * ld, write=True))
+        if adamw:
+            rows.append(ShapeRow(st.mom2, i * ld, write=True))
+        rows.append(ShapeRow(st.params, i * ld, write=True))
+    if method == "cpdp":
+        rows += [ShapeRow(st.slow_mom, write=True), ShapeRow(st.anchor, write=True)]
+    elif method == "localsgd":
+        rows.append(ShapeRow(st.anchor, read=False))
+    return rows
+
+
+def time_launches(fn, stream, reps: int = 10, warmup: int = 3) -> float:
+    """Average milliseconds of fn(stream) over reps back-to-back launches,
+    HIP events on that stream."""
+    import torch
+    for _ in range(warmup):
+        fn(stream)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        fn(stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def shape_probe(w, only=None, reps: int = 10) -> dict:
+    """Bandwidth ceilings of traffic shapes, measured with the no-arithmetic
+    shape kernel (synth/synth.hip) on fresh buffers sized like workload w:
+      reconcile_rows*   the reconcile's exact rows in the library's layout
+                        (W rows per family at stride ld), plain block order,
+                        blocks dealt to XCDs in contiguous eighths, and read
+                        batches of 16 instead of 8;
+      reconcile_tile<T> the same rows and bytes in a coordinate-tile-major
+                        layout: tile t holds coordinates [tT, (t+1)T) of every
+                        row back to back (g_0..g_{W-1}, m_0, th_0, ..., u, a);
+      <n>R<m>W          one row of P fp32 coordinates per stream: n rows read,
+                        m written (in place on read rows first, then
+                        write-only rows);
+      full_*            read only, write only and copy over 4 GiB buffers.
+    Returns {"workload", "results": [...]}; prints one line per shape to
+    stderr as it finishes."""
+    import torch
+    from paper_2607_21224_amd.state import CpdpState
+    from synth import device as sdev
+    from synth.device import ShapePass, ShapeRow
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.Stream(device=dev)
+    W, P = w.W, w.P
+    out = []
+
+    def run(name, make_pass, note=""):
+        if only and name not in only:
+            return
+        sp = make_pass()
+        ms = time_launches(sp.launch, stream, reps)
+        gbps = sp.bytes / (ms * 1e-3) / 1e9
+        rec = {"name": name, "read_rows": sp.n_rd,
+               "written_rows": sum(r.write for r in sp.keep_rows) + sp.n_wo,
+               "bytes": sp.bytes, "ms": round(ms, 5), "GB_per_s": round(gbps, 1),
+               "frac_of_hbm_peak": round(gbps / HBM_PEAK_GBPS, 4), "note": note}
+        out.append(rec)
+        print(f"shape {name}: {gbps:.1f} GB/s ({ms:.4f} ms)", file=sys.stderr, flush=True)
+        del sp
+
+    # the reconcile's rows in the library's layout
+    st = CpdpState(W, P, w.ld, w.K, w.param_dt, device=dev)
+    st.params.zero_(); st.mom.zero_(); st.slow_mom.zero_(); st.anchor.zero_()
+    g = torch.zeros((W, w.ld), dtype=torch.float32, device=dev)
+    rows = sync_shape_rows(st, g, "cpdp", False)
+    run("reconcile_rows", lambda: ShapePass(rows, P))
+    run("reconcile_rows_xcd", lambda: ShapePass(rows, P, xcd=True),
+        "blocks in contiguous eighths per XCD")
+    run("reconcile_rows_batch16", lambda: ShapePass(rows, P, batch=16))
+    del st, g, rows
+    torch.cuda.empty_cache()
+
+    # coordinate-tile-major layouts of the same rows (fp32 state only)
+    if w.param_dt == "f32":
+        R = 3 * W + 2
+        written = [False] * W + [True] * (2 * W) + [True, True]
+        for T in (1024, 2048, 4096):
+            name = f"reconcile_tile{T}"
+            if only and name not in only:
+                continue
+            tiles = (P + T - 1) // T
+            buf = torch.zeros(tiles * R * T, dtype=torch.float32, device=dev)
+            trows = [ShapeRow(buf, r * T, write=written[r]) for r in range(R)]
+            run(name, lambda: ShapePass(trows, P, tile=T, tile_stride=R * T * 4),
+                f"tiles of {T} coordinates, {R} row segments each")
+            del buf, trows
+            torch.cuda.empty_cache()
+
+    # one row per stream
+    ld = (P + (1 << 18) - 1) // (1 << 18) * (1 << 18)  # 1 MiB rows
+    for n_inplace, n_ro, n_wo in ((0, 1, 0), (0, 0, 1), (0, 1, 1), (2, 1, 0), (1, 25, 0),
+                                  (8, 0, 0), (18, 8, 0), (10, 16, 0), (1, 0, 17)):
+        n = n_inplace + n_ro + n_wo
+        name = f"{n_inplace + n_ro}R{n_inplace + n_wo}W"
+        if only and name not in only:
+            continue
+        buf = torch.zeros((n, ld), dtype=torch.float32, device=dev)
+        srows = ([ShapeRow(buf, i * ld, write=True) for i in range(n_inplace)] +
+                 [ShapeRow(buf, (n_inplace + i) * ld) for i in range(n_ro)] +
+                 [ShapeRow(buf, (n_inplace + n_ro + i) * ld, read=False) for i in range(n_wo)])
+        run(name, lambda: ShapePass(srows, P),
+            f"{n_inplace} in place, {n_ro} read only, {n_wo} write only")
+        del buf, srows
+        torch.cuda.empty_cache()
+
+    # full size: 4 GiB streams
+    n_big = 1 << 30
+    if not only or any(x.startswith("full_") for x in only):
+        a = torch.zeros(n_big, dtype=torch.float32, device=dev)
+        b = torch.zeros(n_big, dtype=torch.float32, device=dev)
+        for xcd in (0, 1):
+            sfx = "_xcd" if xcd else ""
+            run("full_read" + sfx, lambda: ShapePass([ShapeRow(a)], n_big, xcd=bool(xcd)))
+            run("full_write" + sfx,
+                lambda: ShapePass([ShapeRow(b, read=False)], n_big, xcd=bool(xcd)))
+            run("full_copy" + sfx,
+                lambda: ShapePass([ShapeRow(a), ShapeRow(b, read=False)], n_big, xcd=bool(xcd)))
+        if not only or "full_copy_kernel" in only:
+            ms = time_launches(lambda s: sdev.copy_f32(b, a, n_big, stream=s), stream, reps)
+            gbps = 8 * n_big / (ms * 1e-3) / 1e9
+            out.append({"name": "full_copy_kernel", "read_rows": 1, "written_rows": 1,
+                        "bytes": 8 * n_big, "ms": round(ms, 5), "GB_per_s": round(gbps, 1),
+                        "frac_of_hbm_peak": round(gbps / HBM_PEAK_GBPS, 4),
+                        "note": "synth_copy_f32, the bench's copy ceiling"})
+            print(f"shape full_copy_kernel: {gbps:.1f} GB/s", file=sys.stderr, flush=True)
+        del a, b
+    return {"shape_probe": w.name, "W": W, "P": P, "ld": w.ld, "reps": reps, "results": out}
 
 
 def main() -> int:
@@ -204,6 +380,13 @@ def main() -> int:
                          "gradient bytes; parameters keep the workload's type)")
     ap.add_argument("--mom-dtype", default="f32", choices=["f32", "bf16"],
                     help="momentum storage of the flat momentum-SGD path")
+    ap.add_argument("--shape-probe", action="store_true",
+                    help="instead of the benchmark, measure the bandwidth ceilings of "
+                         "traffic shapes with the no-arithmetic shape kernel: the "
+                         "reconcile's rows in the library's layout and in coordinate-"
+                         "tile-major layouts, single-row stream mixes, 4 GiB streams")
+    ap.add_argument("--shape-only", default="",
+                    help="comma-separated shape names of --shape-probe to run")
     ap.add_argument("--row-align-bytes", type=int, default=0,
                     help="round each replica row up to a multiple of this many bytes "
                          "(0 = the workload's default of 1 MiB)")
@@ -221,6 +404,10 @@ def main() -> int:
     from synth import device as sdev
 
     w = WORKLOADS[args.workload]
+    if args.shape_probe:
+        only = [x for x in args.shape_only.split(",") if x]
+        print(json.dumps(shape_probe(w, only)), flush=True)
+        return 0
     if args.grad_dtype != "f32" or args.mom_dtype != "f32":
         if args.plan or args.graph or args.optimizer != "sgd":
             raise SystemExit("--grad-dtype / --mom-dtype bf16 run the flat momentum-SGD path "
@@ -346,6 +533,19 @@ def main() -> int:
     c1.record(stream)
     torch.cuda.synchronize()
     copy_gbps = 2 * 4 * n_copy * reps / (c0.elapsed_time(c1) * 1e-3) / 1e9
+    del csrc, cdst
+
+    # traffic-shape ceiling: the synchronisation kernel's exact rows streamed by
+    # a kernel with no arithmetic (in place, the state keeps its bits)
+    shape = None
+    if multi is None:
+        from synth.device import ShapePass
+        sp = ShapePass(sync_shape_rows(st, grads[-1], args.method, adamw), w.P)
+        assert sp.bytes == w.sync_bytes(args.method, adamw), (sp.bytes, w.sync_bytes(args.method, adamw))
+        shape_ms = time_launches(sp.launch, stream)
+        shape = {"GBps": sp.bytes / (shape_ms * 1e-3) / 1e9, "ms": shape_ms,
+                 "rows": f"{sp.n_rd} read ({sum(r.write for r in sp.keep_rows)} written back in "
+                         f"place), {sp.n_wo} write-only"}
 
     def time_replays(graph):
         for _ in range(args.warmup):
@@ -436,12 +636,18 @@ def main() -> int:
                 "avg_launch_ms": round(ms, 5),
                 "frac_of_copy_ceiling": round(ach / copy_gbps, 4)}
 
+    roof_sync = roofline(sync_kernel, rec_bytes, rec_ms)
+    if shape is not None:
+        roof_sync["shape_ceiling_GBps"] = round(shape["GBps"], 1)
+        roof_sync["frac_of_shape_ceiling"] = round(rec_gbps / shape["GBps"], 4)
+
     out = {
         "metric": "reconcile replica-params/s and achieved HBM GB/s (% of MI355X peak)",
-        "value": wp * w.K / (ms_per_step * 1e-3),
+        "value": wp / (rec_ms * 1e-3),
         "unit": "replica-params/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 5),
+        "period_replica_params_per_s": wp * w.K / (ms_per_step * 1e-3),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": ("f32" if (w.param_dt, w.grad_dt, w.mom_dt) == ("f32", "f32", "f32") else
                   f"{w.param_dt} params, {w.grad_dt} grads, {w.mom_dt} mom, f32 u/anchor"),
@@ -470,7 +676,7 @@ def main() -> int:
             "GB_per_s": round(loc_bytes / (loc_ms * 1e-3) / 1e9, 1),
             "frac_of_hbm_peak": round(loc_bytes / (loc_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
             "ms": round(loc_ms, 5), **spread(dur["local"])},
-        "roofline": roofline(sync_kernel, rec_bytes, rec_ms),
+        "roofline": roof_sync,
         "roofline_local_step": None if loc_ms is None else roofline("local_step", loc_bytes, loc_ms),
         "graph_replay": None if graph_ms is None else {
             "ms_per_step": round(graph_ms, 5),
@@ -480,6 +686,10 @@ def main() -> int:
             "replica_params_per_s": wp * w.K / (graph_table_ms * 1e-3)},
         "cold": cold,
         "copy_ceiling_GBps": round(copy_gbps, 1),
+        "shape_ceiling": None if shape is None else {
+            "GB_per_s": round(shape["GBps"], 1), "ms": round(shape["ms"], 5),
+            "kernel": "synth shape_kernel: the same rows, loads and in-place stores, no "
+                      "arithmetic", "rows": shape["rows"]},
         "wall_s_timed_region": round(wall, 4),
     }
     if not args.no_cpu_baseline:

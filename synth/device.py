@@ -22,6 +22,8 @@ def _load():
     lib.synth_fill_normal.restype = i
     lib.synth_copy_f32.argtypes = [vp, vp, i64, vp]
     lib.synth_copy_f32.restype = i
+    lib.synth_shape_stream.argtypes = [vp, i, i, i64, i64, i64, i, i, u32, vp, vp]
+    lib.synth_shape_stream.restype = i
     return lib
 
 
@@ -86,3 +88,90 @@ def copy_f32(dst, src, n: int, stream=None) -> None:
     r = lib().synth_copy_f32(dst.data_ptr(), src.data_ptr(), n, _stream(stream))
     if r != 0:
         raise RuntimeError(f"synth_copy_f32 failed ({r})")
+
+
+# ---- traffic-shape kernel -----------------------------------------------------
+
+SHAPE_MAX_READ = 256
+SHAPE_MAX_WRITE_ONLY = 64
+
+
+class ShapeRow:
+    """One row of a traffic shape: coordinates [0, P) of ``tensor`` starting
+    at element ``offset`` (plain rows), or the row's segment in every tile of
+    a tile-major layout.  ``write`` = the row is written back in place after
+    it is read; ``read`` = False makes a write-only row (fp32)."""
+
+    def __init__(self, tensor, offset: int = 0, write: bool = False, read: bool = True):
+        if not isinstance(tensor, torch.Tensor) or not tensor.is_cuda or not tensor.is_contiguous():
+            raise ValueError("a shape row lives in a contiguous GPU tensor")
+        if tensor.dtype not in (torch.float32, torch.bfloat16):
+            raise ValueError("shape rows are float32 or bfloat16")
+        if not read and (write or tensor.dtype != torch.float32):
+            raise ValueError("a write-only row is a float32 row")
+        self.tensor, self.offset, self.write, self.read = tensor, int(offset), bool(write), bool(read)
+
+    @property
+    def esize(self) -> int:
+        return self.tensor.element_size()
+
+    def nbytes(self, P: int) -> int:
+        """Bytes the pass moves on this row."""
+        return P * self.esize * (int(self.read) + int(self.write or not self.read))
+
+
+class ShapePass:
+    """A traffic shape ready to launch: the device row table and the checks
+    that every row covers what the kernel touches."""
+
+    def __init__(self, rows, P: int, tile: int = 0, tile_stride: int = 0,
+                 xcd: bool = False, batch: int = 8):
+        rows = list(rows)
+        rd = [r for r in rows if r.read]
+        wo = [r for r in rows if not r.read]
+        if not 1 <= len(rows) or len(rd) > SHAPE_MAX_READ or len(wo) > SHAPE_MAX_WRITE_ONLY:
+            raise ValueError(f"{len(rd)} read and {len(wo)} write-only rows: at most "
+                             f"{SHAPE_MAX_READ} and {SHAPE_MAX_WRITE_ONLY}")
+        if P < 0 or P % 4:
+            raise ValueError(f"P = {P} must be a non-negative multiple of 4")
+        if batch not in (8, 16):
+            raise ValueError("batch is 8 or 16")
+        if tile and (tile % 1024 or tile_stride < 0):
+            raise ValueError("tile is a multiple of 1024 coordinates")
+        dev = rows[0].tensor.device
+        t = tile if tile else max(P, 1)
+        for r in rows:
+            if r.tensor.device != dev:
+                raise ValueError("all rows on one device")
+            if tile and tile_stride % r.esize:
+                raise ValueError("tile_stride is a whole number of elements")
+            ts = tile_stride // r.esize if tile else 0
+            if P:
+                last = r.offset + ((P - 1) // t) * ts + (P - 1) % t
+                if r.offset < 0 or last >= r.tensor.numel():
+                    raise ValueError(f"row at element {r.offset} reaches element {last} of a "
+                                     f"tensor of {r.tensor.numel()}")
+            # 16-byte (fp32) / 8-byte (bf16) vector accesses at every 4th coordinate
+            if (r.tensor.data_ptr() + r.offset * r.esize) % (4 * r.esize):
+                raise ValueError("row start not aligned for 4-coordinate vectors")
+            if tile and tile_stride % (4 * r.esize):
+                raise ValueError("tile_stride not aligned for 4-coordinate vectors")
+        words = []
+        for r in rd:
+            a = r.tensor.data_ptr() + r.offset * r.esize
+            words += [a, a if r.write else 0, 1 if r.esize == 2 else 0]
+        words += [r.tensor.data_ptr() + r.offset * r.esize for r in wo]
+        self.table = torch.tensor(words, dtype=torch.int64, device=dev)
+        self.sink = torch.zeros(256, dtype=torch.int32, device=dev)
+        self.keep_rows = rows  # the rows (and their tensors) outlive the pass
+        self.n_rd, self.n_wo = len(rd), len(wo)
+        self.P, self.tile, self.tile_stride = P, tile, tile_stride
+        self.xcd, self.batch = int(bool(xcd)), batch
+        self.bytes = sum(r.nbytes(P) for r in rows)
+
+    def launch(self, stream=None, sentinel: int = 0x9E3779B9) -> None:
+        r = lib().synth_shape_stream(self.table.data_ptr(), self.n_rd, self.n_wo, self.P,
+                                     self.tile, self.tile_stride, self.xcd, self.batch,
+                                     sentinel, self.sink.data_ptr(), _stream(stream))
+        if r != 0:
+            raise RuntimeError(f"synth_shape_stream failed ({r})")

@@ -1,5 +1,7 @@
 // Device side of the seeded input generator (definition in synth/gen.py),
-// plus a plain copy kernel used to calibrate bandwidth and HBM counters.
+// plus two measurement kernels: a plain copy that calibrates bandwidth and the
+// HBM counters, and a traffic-shape kernel that streams any set of rows with
+// no arithmetic to speak of, the bandwidth ceiling of a traffic shape.
 //
 // Holds none of the CPDP arithmetic.  The generator draws the numbers that
 // stand in for the initial model and for backward-pass gradients; a GPU test
@@ -82,6 +84,96 @@ __global__ __launch_bounds__(kBlock) void copy_kernel(float* __restrict__ dst,
     }
 }
 
+
+// ---- traffic-shape kernel ------------------------------------------------------
+//
+// Moves the bytes of a streaming pass with a given set of rows and nothing
+// else: every thread loads 4 consecutive coordinates of every read row
+// (128-bit loads of fp32 rows, 64-bit of bf16 rows, nontemporal), folds the
+// loaded bits into an XOR, and stores each read row that is also written
+// back to its write address unchanged (in place, the state keeps its exact
+// bits), then the XOR into every extra write-only row.  Read rows are taken
+// in batches of B, all loads of a batch before its stores, as the reconcile
+// takes its replica batches.  One block covers 1024 coordinates, as the
+// library's flat kernels do; blocks go round robin to the XCDs, or (xcd = 1)
+// in contiguous eighths like the copy kernel.
+//
+// Row table in device memory, 64-bit words: for each read row r
+// [3r] address, [3r+1] write address (0 = read only), [3r+2] 1 for bf16
+// (2-byte) rows; then one address per write-only row (fp32, 4 bytes).
+// Coordinate p of a row with address a sits at
+//   a + (p / tile) * tile_stride + (p % tile) * esize
+// so tile = the row length with tile_stride = 0 gives plain rows, and
+// tile = T with tile_stride = rows * T * esize a tile-major layout whose
+// tiles of T coordinates hold one segment of every row back to back.
+// The XOR is written to `sink` only when it equals `sentinel`, which keeps
+// every load live; sink is a 1 KiB scratch buffer.
+constexpr int kShapeMaxRead = 256;
+constexpr int kShapeMaxWriteOnly = 64;
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+template <int B>
+__global__ __launch_bounds__(kBlock) void shape_kernel(const int64_t* __restrict__ rows, int n_rd,
+                                                       int n_wo, int64_t P, int64_t chunks,
+                                                       int64_t tile, int64_t tile_stride,
+                                                       int xcd, uint32_t sentinel,
+                                                       uint32_t* __restrict__ sink) {
+    int64_t c = blockIdx.x;
+    if (xcd) {
+        const int64_t per = (chunks + 7) / 8;
+        c = (int64_t)(blockIdx.x % 8) * per + (int64_t)(blockIdx.x / 8);
+    }
+    if (c >= chunks) return;
+    const int64_t p0 = (c * kBlock + threadIdx.x) * kVec;
+    if (p0 + kVec > P) return;  // P is a multiple of kVec (checked on the host)
+    const int64_t tile_off = (p0 / tile) * tile_stride;
+    const int64_t in_tile = p0 % tile;
+    uint32_t acc = 0;
+    for (int r0 = 0; r0 < n_rd; r0 += B) {
+        u32x4 x[B];
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+            x[b] = u32x4{0u, 0u, 0u, 0u};
+            const int r = r0 + b;
+            if (r < n_rd) {
+                const char* a = reinterpret_cast<const char*>(rows[3 * r]) + tile_off;
+                if (rows[3 * r + 2]) {
+                    const u32x2 v = __builtin_nontemporal_load(
+                        reinterpret_cast<const u32x2*>(a + in_tile * 2));
+                    x[b].x = v.x;
+                    x[b].y = v.y;
+                } else {
+                    x[b] = __builtin_nontemporal_load(
+                        reinterpret_cast<const u32x4*>(a + in_tile * 4));
+                }
+            }
+        }
+#pragma unroll
+        for (int b = 0; b < B; ++b) acc ^= x[b].x ^ x[b].y ^ x[b].z ^ x[b].w;
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+            const int r = r0 + b;
+            if (r < n_rd && rows[3 * r + 1] != 0) {
+                char* a = reinterpret_cast<char*>(rows[3 * r + 1]) + tile_off;
+                if (rows[3 * r + 2])
+                    __builtin_nontemporal_store(u32x2{x[b].x, x[b].y},
+                                                reinterpret_cast<u32x2*>(a + in_tile * 2));
+                else
+                    __builtin_nontemporal_store(x[b], reinterpret_cast<u32x4*>(a + in_tile * 4));
+            }
+        }
+    }
+    const int64_t* wo = rows + 3 * (int64_t)n_rd;
+    for (int j = 0; j < n_wo; ++j) {
+        char* a = reinterpret_cast<char*>(wo[j]) + tile_off;
+        __builtin_nontemporal_store(u32x4{acc, acc, acc, acc},
+                                    reinterpret_cast<u32x4*>(a + in_tile * 4));
+    }
+    if (acc == sentinel) sink[threadIdx.x] = acc;
+}
+
 int64_t blocks_for(int64_t n) { return (n + kBlock * kVec - 1) / (kBlock * kVec); }
 
 template <class T>
@@ -124,6 +216,38 @@ int synth_copy_f32(float* dst, const float* src, int64_t n, void* stream) {
     const int64_t chunks = blocks_for(n);
     if (chunks > 0x7FFFFFFF - 8) return -1;
     return launch(copy_kernel, (chunks + 7) / 8 * 8, stream, dst, src, n, chunks);
+}
+
+
+// One pass of the traffic-shape kernel (see shape_kernel) over coordinates
+// [0, P) of the rows described by the device table `rows` (n_read read rows,
+// n_write_only write-only rows).  tile = 0 means plain rows; otherwise tile
+// is a multiple of 1024 coordinates and tile_stride the bytes between tiles.
+// batch is 8 or 16; xcd = 1 deals blocks to the XCDs in contiguous eighths.
+// The caller guarantees that every address the table names covers the
+// coordinates the pass touches (the Python binding checks it against the
+// tensors it takes them from).  Returns 0, a HIP error code, or -1 for
+// invalid arguments.
+int synth_shape_stream(const int64_t* rows, int n_read, int n_write_only, int64_t P,
+                       int64_t tile, int64_t tile_stride, int xcd, int batch,
+                       uint32_t sentinel, uint32_t* sink, void* stream) {
+    if (rows == nullptr || sink == nullptr || n_read < 0 || n_read > kShapeMaxRead ||
+        n_write_only < 0 || n_write_only > kShapeMaxWriteOnly || n_read + n_write_only < 1 ||
+        P < 0 || P % kVec != 0 || tile < 0 || tile_stride < 0 || (xcd != 0 && xcd != 1))
+        return -1;
+    if (tile != 0 && tile % (kBlock * kVec) != 0) return -1;
+    if (P == 0) return 0;
+    const int64_t chunks = blocks_for(P);
+    if (chunks > 0x7FFFFFFF - 8) return -1;
+    const int64_t t = tile == 0 ? P : tile;
+    const int64_t blocks = xcd ? (chunks + 7) / 8 * 8 : chunks;
+    if (batch == 8)
+        return launch(shape_kernel<8>, blocks, stream, rows, n_read, n_write_only, P, chunks, t,
+                      tile == 0 ? (int64_t)0 : tile_stride, xcd, sentinel, sink);
+    if (batch == 16)
+        return launch(shape_kernel<16>, blocks, stream, rows, n_read, n_write_only, P, chunks, t,
+                      tile == 0 ? (int64_t)0 : tile_stride, xcd, sentinel, sink);
+    return -1;
 }
 
 }  // extern "C"

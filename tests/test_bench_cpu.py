@@ -17,11 +17,27 @@ def test_cpu_baseline_runs_every_strategy_and_optimizer(method, optimizer):
     r = bench.cpu_baseline(w, budget_s=0.02, n_coords=256, parallel_budget_s=0.02,
                            method=method, optimizer=optimizer)
     assert r["kind"] == "oracle" and r["unit"] == "replica-params/s"
-    assert r["cores"] == 1 and r["value"] > 0
-    assert r["parallel"]["cores"] >= 1 and r["parallel"]["value"] > 0
+    assert r["cores"] == bench.cpu_threads()["threads"] and r["value"] > 0
+    assert r["host_cpu_count"] == os.cpu_count()
+    assert r["affinity_cpus"] == len(os.sched_getaffinity(0))
     assert f"({method}, {optimizer})" in r["sample"]
-    assert r["extrapolated"] is True  # 256 of 262,144 coordinates
-    assert r["s_per_reconcile_full_P"] > 0
+    one = r["single_thread"]
+    assert one["cores"] == 1 and one["value"] > 0 and one["period_replica_params_per_s"] > 0
+    assert f"({method}, {optimizer})" in one["sample"]
+    assert one["extrapolated"] is True  # 256 of 262,144 coordinates
+    assert one["s_per_reconcile_full_P"] > 0
+
+
+def test_cpu_threads_follow_affinity_and_job_share(monkeypatch):
+    """Every CPU of the affinity set, capped by the job's CPU share."""
+    aff = len(os.sched_getaffinity(0))
+    monkeypatch.delenv("OMP_NUM_THREADS", raising=False)
+    assert bench.cpu_threads()["threads"] == aff
+    monkeypatch.setenv("OMP_NUM_THREADS", "1")
+    c = bench.cpu_threads()
+    assert c["threads"] == 1 and c["omp_num_threads"] == 1 and c["affinity_cpus"] == aff
+    monkeypatch.setenv("OMP_NUM_THREADS", str(aff + 100))
+    assert bench.cpu_threads()["threads"] == aff
 
 
 def test_oracle_slice_counts_whole_periods():

@@ -1,0 +1,92 @@
+"""The traffic-shape kernel (synth/synth.hip) that bench.py uses for the
+bandwidth ceiling of a row set: it must touch exactly the coordinates it is
+given, write back in-place rows unchanged, and fill write-only rows with the
+XOR of what it read."""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+def _words_f32(x):
+    """(n,) fp32 tensor -> (n/4, 4) uint32 words per 4-coordinate group."""
+    return x.cpu().numpy().view(np.uint32).reshape(-1, 4)
+
+
+def _words_bf16(x):
+    """(n,) bf16 tensor -> (n/4, 2) uint32 words (two bf16 per word, low first)."""
+    h = x.view(torch.int16).cpu().numpy().view(np.uint16).astype(np.uint32).reshape(-1, 2)
+    return (h[:, 0] | (h[:, 1] << 16)).reshape(-1, 2)
+
+
+def test_shape_rows_in_place_keep_bits_and_pads():
+    from synth.device import ShapePass, ShapeRow
+    dev = torch.device("cuda:0")
+    P, ld = 4 * 1024 * 3 + 8, 16384  # several blocks and a partly used last block
+    g = torch.randn((3, ld), device=dev)
+    b = torch.randn((2, ld), device=dev).to(torch.bfloat16)
+    wo = torch.full((2, ld), 7.0, device=dev)
+    g0, b0 = g.clone(), b.clone()
+    rows = [ShapeRow(g, 0), ShapeRow(g, ld, write=True), ShapeRow(b, 0, write=True),
+            ShapeRow(g, 2 * ld, write=True), ShapeRow(b, ld),
+            ShapeRow(wo, 0, read=False), ShapeRow(wo, ld, read=False)]
+    assert ShapePass(rows, P).bytes == P * (4 * 3 + 2 * 2 + 4 * 2 + 2 * 1 + 4 * 2)
+    acc = np.zeros(P // 4, dtype=np.uint32)
+    for r in range(3):
+        acc ^= np.bitwise_xor.reduce(_words_f32(g[r, :P]), axis=1)
+    for r in range(2):
+        acc ^= np.bitwise_xor.reduce(_words_bf16(b[r, :P]), axis=1)
+    for batch in (8, 16):
+        for xcd in (False, True):
+            wo.fill_(7.0)
+            ShapePass(rows, P, xcd=xcd, batch=batch).launch()
+            torch.cuda.synchronize()
+            assert torch.equal(g.view(torch.int32), g0.view(torch.int32))
+            assert torch.equal(b.view(torch.int16), b0.view(torch.int16))
+            for j in range(2):
+                got = _words_f32(wo[j, :P])
+                assert np.array_equal(got, np.repeat(acc[:, None], 4, axis=1)), (batch, xcd, j)
+                assert (wo[j, P:] == 7.0).all(), "write past P"
+
+
+def test_shape_tile_major_addressing():
+    """Tile-major rows: coordinate p of row r sits at r*T + (p // T)*R*T + p % T."""
+    from synth.device import ShapePass, ShapeRow
+    dev = torch.device("cuda:0")
+    T, R, P = 2048, 3, 2048 * 2 + 1024 + 8
+    tiles = (P + T - 1) // T
+    buf = torch.randn(tiles * R * T, device=dev)
+    out = torch.full((tiles * R * T,), -1.0, device=dev)
+    before = buf.clone()
+    rows = [ShapeRow(buf, r * T, write=(r == 1)) for r in range(R)]
+    ShapePass(rows + [ShapeRow(out, T, read=False)], P, tile=T,
+              tile_stride=R * T * 4).launch()
+    torch.cuda.synchronize()
+    assert torch.equal(buf.view(torch.int32), before.view(torch.int32))
+    p = np.arange(P)
+    pos = lambda r: r * T + (p // T) * R * T + p % T  # noqa: E731
+    host = buf.cpu()
+    acc = np.zeros(P // 4, dtype=np.uint32)
+    for r in range(R):
+        acc ^= np.bitwise_xor.reduce(_words_f32(host[pos(r)]), axis=1)
+    o = out.cpu()
+    assert np.array_equal(_words_f32(o[pos(1)]), np.repeat(acc[:, None], 4, axis=1))
+    untouched = np.ones(o.numel(), dtype=bool)
+    untouched[pos(1)] = False
+    assert (o[torch.from_numpy(untouched)] == -1.0).all()
+
+
+def test_shape_pass_rejects_rows_that_do_not_fit():
+    from synth.device import ShapePass, ShapeRow
+    dev = torch.device("cuda:0")
+    x = torch.zeros(1000, device=dev)
+    with pytest.raises(ValueError):
+        ShapePass([ShapeRow(x, 8)], 996)      # would reach element 1003
+    with pytest.raises(ValueError):
+        ShapePass([ShapeRow(x, 2)], 8)        # not 16-byte aligned
+    with pytest.raises(ValueError):
+        ShapePass([ShapeRow(x)], 10)          # P not a multiple of 4
+    with pytest.raises(ValueError):           # tile layout past the buffer
+        ShapePass([ShapeRow(x)], 1024 + 4, tile=1024, tile_stride=4096)
+    ShapePass([ShapeRow(x, 4)], 996)          # exactly fits
