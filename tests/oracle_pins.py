@@ -552,3 +552,353 @@ def pin_gradient_write_back(use=None):
 
 
 ALL_PINS += [pin_torch_state_averaging, pin_gradient_write_back]
+
+
+# ---- storage-rounding points ---------------------------------------------------
+
+def exact(expr: str):
+    """Value of a fixture expression (numbers, + - * / and ** over exact
+    rationals), e.g. "1 + 3*2**-9"."""
+    import ast
+    import operator as op
+    ops = {ast.Add: op.add, ast.Sub: op.sub, ast.Mult: op.mul, ast.Div: op.truediv,
+           ast.Pow: op.pow}
+
+    def ev(n):
+        if isinstance(n, ast.Expression):
+            return ev(n.body)
+        if isinstance(n, ast.Constant) and isinstance(n.value, int):
+            return Fraction(n.value)
+        if isinstance(n, ast.Constant) and isinstance(n.value, float):
+            return Fraction(n.value)
+        if isinstance(n, ast.UnaryOp) and isinstance(n.op, (ast.USub, ast.UAdd)):
+            v = ev(n.operand)
+            return -v if isinstance(n.op, ast.USub) else v
+        if isinstance(n, ast.BinOp) and type(n.op) in ops:
+            return ops[type(n.op)](ev(n.left), ev(n.right))
+        raise ValueError(f"not an exact expression: {expr!r}")
+
+    return ev(ast.parse(str(expr), mode="eval"))
+
+
+def _f(expr) -> float:
+    v = exact(expr)
+    assert Fraction(float(v)) == v, f"{expr} is not a double"
+    return float(v)
+
+
+def _fixture_state(case, dts, use):
+    """The case's input state as an OracleState (P = number of coordinates)."""
+    W, cs = case["W"], case["coords"]
+    P = len(cs)
+    st = oracle.state_init(np.zeros(P), W, dts["param"], dts["mom"], dts["aux"], use=use)
+    for p, c in enumerate(cs):
+        for i in range(W):
+            st.params[i, p] = _f(c["in"]["params"][i])
+            st.mom[i, p] = _f(c["in"]["mom"][i])
+        st.slow[p] = _f(c["in"]["u"])
+        st.anchor[p] = _f(c["in"]["anchor"])
+    mom2 = None
+    if "mom2" in cs[0]["in"]:
+        mom2 = np.array([[_f(c["in"]["mom2"][i]) for c in cs] for i in range(W)])
+    g = np.array([[_f(c["grads"][i]) for c in cs] for i in range(W)])
+    return st, mom2, g
+
+
+def _check_fixture_out(case, st, mom2, tag):
+    for p, c in enumerate(case["coords"]):
+        want = c["out"]
+        got = {"params": st.params[:, p], "mom": st.mom[:, p], "u": st.slow[p],
+               "anchor": st.anchor[p]}
+        if "mom2" in want:
+            got["mom2"] = mom2[:, p]
+        for k, w in want.items():
+            w = [_f(x) for x in w] if isinstance(w, list) else _f(w)
+            g = np.atleast_1d(got[k])
+            assert np.array_equal(g, np.atleast_1d(w)), \
+                f"{tag} coordinate {p} ({c['pins']}): {k} = {g.tolist()}, want {w}"
+
+
+def pin_rounding_points(use=None):
+    """Every storage-rounding point of init, the local steps and the three
+    synchronisation steps, on the plain functions and on the general-optimizer
+    ones, against the hand derivations of tests/golden/rounding_points_bf16.json
+    (Algorithm 1 and Sec. 4.2: tensors are stored in their storage types where
+    the implementation writes them)."""
+    fx = json.load(open(os.path.join(GOLDEN, "rounding_points_bf16.json")))
+    dts = fx["dtypes"]
+    hp = {k: _f(v) for k, v in fx["hyper"].items()}
+    lr, mu, beta, alpha = hp["lr"], hp["mu"], hp["beta"], hp["alpha"]
+    for case in fx["cases"]:
+        op = case["op"]
+        if op == "init":
+            cs = case["coords"]
+            st = oracle.state_init(np.array([_f(c["theta0"]) for c in cs]), case["W"],
+                                   dts["param"], dts["mom"], dts["aux"], use=use)
+            _check_fixture_out(case, st, None, "init")
+            continue
+        if op == "reconcile_vform":  # the paper's own variables; st.slow holds v
+            st, _, g = _fixture_state(case, dts, use)
+            oracle.reconcile_vform(st, g, lr, mu, beta)
+            _check_fixture_out(case, st, None, op)
+            continue
+        if op in ("local", "reconcile", "localsgd", "ddp"):
+            # the plain momentum-SGD functions
+            st, _, g = _fixture_state(case, dts, use)
+            if op == "local":
+                oracle.local_step(st, g, lr, mu)
+            elif op == "reconcile":
+                oracle.reconcile(st, g, lr, mu, beta, alpha)
+            elif op == "localsgd":
+                oracle.localsgd_sync(st, g, lr, mu)
+            else:
+                oracle.ddp_step(st, g, lr, mu)
+            _check_fixture_out(case, st, None, op)
+            # the general-optimizer functions with plain momentum SGD
+            st, _, g = _fixture_state(case, dts, use)
+            o = oracle.sgd(lr, mu, 0.0)
+            if op == "local":
+                oracle.local_step_opt(st, g, o)
+            else:
+                method = {"reconcile": "cpdp", "localsgd": "localsgd", "ddp": "ddp"}[op]
+                oracle.sync_opt(st, method, g, o, beta, alpha)
+            _check_fixture_out(case, st, None, op + " (general optimizer)")
+            continue
+        if op == "ddp_average_state":  # a variant of the general functions only
+            st, _, g = _fixture_state(case, dts, use)
+            oracle.sync_opt(st, "ddp", g, oracle.sgd(lr, mu, 0.0), beta, alpha,
+                            flags=oracle.SYNC_AVERAGE_STATE)
+            _check_fixture_out(case, st, None, op)
+            continue
+        o = {k: (_f(v) if isinstance(v, str) else v) for k, v in case["opt"].items()}
+        st, mom2, g = _fixture_state(case, dts, use)
+        if op == "local_sgd_wd":
+            oracle.local_step_opt(st, g, oracle.sgd(o["lr"], o["mu"], o["wd"]))
+        elif op == "local_adamw":
+            mom2 = np.ascontiguousarray(mom2)
+            oracle.local_step_opt(st, g, oracle.adamw(o["lr"], o["beta1"], o["beta2"],
+                                                      o["eps"], o["wd"], o["step"]), mom2)
+        else:
+            raise ValueError(op)
+        _check_fixture_out(case, st, mom2, op)
+
+
+ALL_PINS.insert(0, pin_rounding_points)
+
+
+def pin_brute_force_rounded(use=None, seed=41):
+    """The oracle's stored state equals, bit for bit, an exact rational run of
+    the same steps that rounds to the storage types only where a tensor is
+    written (tests/brute_rounded.py), on tiny random inputs: every dtype
+    combination the library takes, the three strategies, the plain momentum-
+    SGD functions, the v-form, and the general functions with SGD + weight
+    decay and AdamW, with and without the two sync-step variants."""
+    import brute_rounded as br
+    rng = np.random.default_rng(seed)
+    f32 = lambda x: float(np.float32(x))  # noqa: E731
+    lr, mu, beta, alpha = f32(0.1), f32(0.9), f32(0.5), 1.0
+    W, P, K, n = 3, 5, 3, 7
+    combos = [("f32", "f32", "f32"), ("bf16", "f32", "f32"), ("bf16", "bf16", "f32"),
+              ("f32", "bf16", "f32")]
+
+    def compare(st, bst, tag, mom2=None):
+        fl = lambda rows: np.array([[float(x) for x in r] for r in rows])  # noqa: E731
+        for name, a, b in (("params", st.params, fl(bst.params)), ("mom", st.mom, fl(bst.mom)),
+                           ("u", st.slow, np.array([float(x) for x in bst.u])),
+                           ("anchor", st.anchor, np.array([float(x) for x in bst.ref]))):
+            assert np.array_equal(a, b), f"{tag}: {name} {a.ravel()[:4]} want {b.ravel()[:4]}"
+        if mom2 is not None:
+            assert np.array_equal(mom2, fl(bst.mom2)), f"{tag}: mom2"
+
+    for pdt, mdt, adt in combos:
+        theta0 = rng.normal(0, 0.02, P).astype(np.float32).astype(np.float64)
+        grads = [rng.normal(0, 1e-3, (W, P)).astype(np.float32).astype(np.float64)
+                 for _ in range(n)]
+        # plain momentum-SGD functions, and the v-form
+        for method in ("cpdp", "localsgd", "ddp", "vform"):
+            st = oracle.state_init(theta0, W, pdt, mdt, adt, use=use)
+            bst = br.State(theta0, W, pdt, mdt, adt)
+            o = br.Opt("sgd", lr, mu)
+            for s in range(1, n + 1):
+                g = grads[s - 1]
+                tag = f"{method} {pdt}/{mdt}/{adt} step {s}"
+                if method == "ddp":
+                    oracle.ddp_step(st, g, lr, mu)
+                    br.sync_step(bst, "ddp", g, o)
+                elif s % K:
+                    oracle.local_step(st, g, lr, mu)
+                    br.local_step(bst, g, o)
+                elif method == "cpdp":
+                    oracle.reconcile(st, g, lr, mu, beta, alpha)
+                    br.sync_step(bst, "cpdp", g, o, beta, alpha)
+                elif method == "localsgd":
+                    oracle.localsgd_sync(st, g, lr, mu)
+                    br.sync_step(bst, "localsgd", g, o)
+                else:
+                    oracle.reconcile_vform(st, g, lr, mu, beta)
+                    br.sync_vform(bst, g, o, beta)
+                compare(st, bst, tag)
+        # general-optimizer functions
+        opts = [("sgd_wd", lambda t: oracle.sgd(lr, mu, f32(5e-4)),
+                 lambda t: br.Opt("sgd", lr, mu, wd=f32(5e-4))),
+                ("adamw", lambda t: oracle.adamw(f32(1e-2), mu, f32(0.999), f32(1e-8), f32(0.05), t),
+                 lambda t: br.Opt("adamw", f32(1e-2), mu, f32(0.05), f32(0.999), f32(1e-8), t))]
+        for method in ("cpdp", "localsgd", "ddp"):
+            for oname, mk, bmk in opts:
+                for flags in (0, 3):
+                    st = oracle.state_init(theta0, W, pdt, mdt, adt, use=use)
+                    bst = br.State(theta0, W, pdt, mdt, adt)
+                    mom2 = np.zeros((W, P))
+                    for s in range(1, n + 1):
+                        g = grads[s - 1]
+                        tag = f"{method} {oname} flags={flags} {pdt}/{mdt}/{adt} step {s}"
+                        if method == "ddp" or s % K == 0:
+                            gout = oracle.sync_opt(st, method, g, mk(s), beta, alpha, mom2,
+                                                   flags=flags)
+                            bg = br.sync_step(bst, method, g, bmk(s), beta, alpha, flags)
+                            assert np.array_equal(gout, np.array([[float(x) for x in r]
+                                                                  for r in bg])), tag + " grads"
+                        else:
+                            oracle.local_step_opt(st, g, mk(s), mom2)
+                            br.local_step(bst, g, bmk(s))
+                        compare(st, bst, tag, mom2)
+
+
+ALL_PINS.append(pin_brute_force_rounded)
+
+
+def _ulps(a, b):
+    """|a - b| in units of the fp32 spacing at b (elementwise)."""
+    b32 = np.asarray(b, dtype=np.float32)
+    return np.abs(np.asarray(a, dtype=np.float64) - b32.astype(np.float64)) / \
+        np.spacing(np.abs(b32)).astype(np.float64)
+
+
+def pin_torch_fp32_optimizers(use=None):
+    """fp32 storage against PyTorch's own fp32 optimizers (one worker, local
+    steps): torch.optim.SGD (momentum, coupled weight decay) and
+    torch.optim.AdamW on float32 parameters.  torch multiplies its fp32
+    tensors by AdamW's decay factor 1 - lr*wd, step size lr/(1 - b1^t) and
+    sqrt(1 - b2^t) as fp32 values, which is the oracle's reading.  The two
+    differ only in the rounding of intermediate tensor operations (torch
+    rounds after each of mul_, add_, lerp_, sqrt, div), so the parameters
+    stay within 2 fp32 ulps over 24 steps (parameters of size 1..2, SGD
+    gradients of size 0.01).  lr = 1e-3 and wd = 0.02 make
+    1 - lr*wd lose 0.46 ulp in fp32; with the factor kept exact, parameters
+    of size 1..2 drift by about a quarter to half an ulp per step."""
+    import torch
+    rng = np.random.default_rng(43)
+    f32 = lambda x: float(np.float32(x))  # noqa: E731
+    P, n = 2048, 24
+    theta0 = (rng.choice([-1.0, 1.0], P) * (1 + rng.random(P))).astype(np.float32)
+    grads = {"adamw": [rng.normal(0, 1, (1, P)).astype(np.float32) for _ in range(n)],
+             # SGD steps scale with the gradient: small ones keep theta in its
+             # binade, so ulps at theta measure the update's rounding, not a
+             # cancellation
+             "sgd": [rng.normal(0, 1e-2, (1, P)).astype(np.float32) for _ in range(n)]}
+    cfgs = [("adamw", dict(lr=f32(1e-3), betas=(f32(0.9), f32(0.999)), eps=f32(1e-8),
+                           weight_decay=f32(0.02)),
+             lambda t: oracle.adamw(f32(1e-3), f32(0.9), f32(0.999), f32(1e-8), f32(0.02), t)),
+            ("sgd", dict(lr=f32(0.1), momentum=f32(0.9), weight_decay=f32(5e-4)),
+             lambda t: oracle.sgd(f32(0.1), f32(0.9), f32(5e-4)))]
+    for kind, tkw, mk in cfgs:
+        p = torch.nn.Parameter(torch.from_numpy(theta0.copy()))
+        opt = (torch.optim.AdamW([p], foreach=False, **tkw) if kind == "adamw"
+               else torch.optim.SGD([p], foreach=False, **tkw))
+        st = oracle.state_init(theta0.astype(np.float64), 1, "f32", "f32", "f32", use=use)
+        mom2 = np.zeros((1, P))
+        for t in range(1, n + 1):
+            g = grads[kind][t - 1]
+            p.grad = torch.from_numpy(g[0].copy())
+            opt.step()
+            oracle.local_step_opt(st, g.astype(np.float64), mk(t), mom2)
+            d = _ulps(st.params[0], p.detach().numpy())
+            assert d.max() <= 2, f"{kind} step {t}: {int((d > 2).sum())} parameters more " \
+                                 f"than 2 ulps from torch (max {d.max():.1f})"
+
+
+ALL_PINS.append(pin_torch_fp32_optimizers)
+
+
+def _torch_bf16_cpdp(theta0, grads, W, K, lr, mu, beta, alpha):
+    """CPDP with SlowMo written with torch tensor operations in the stress
+    storage types: bf16 parameter tensors, fp32 momentum buffers, fp32 mean
+    gradient, u and reference model.  In the order of Sec. 4.2: the local
+    optimizer step writes each replica's bf16 parameter tensor; at a sync the
+    mean gradient is formed, the optimizer step writes the parameter tensors,
+    and only then are they averaged, SlowMo applied and the result copied
+    back.  Returns the (params, mom, u, anchor) arrays after every step."""
+    import torch
+    bf, f32 = torch.bfloat16, torch.float32
+    ps = [torch.tensor(theta0, dtype=f32).to(bf) for _ in range(W)]
+    bufs = [torch.zeros(len(theta0), dtype=f32) for _ in range(W)]
+    u = torch.zeros(len(theta0), dtype=f32)
+    ref = ps[0].to(f32)
+    out = []
+    for s, g in enumerate(grads, start=1):
+        gt = torch.tensor(g, dtype=f32)
+        sync = s % K == 0
+        gbar = gt.mean(0) if sync else None
+        for i in range(W):
+            bufs[i].mul_(mu).add_(gbar if sync else gt[i])
+            ps[i].copy_((ps[i].to(f32) - lr * bufs[i]).to(bf))
+        if sync:
+            avg = torch.stack([p.to(f32) for p in ps]).mean(0)
+            u = beta * u + (ref - avg) / lr
+            ref = ref - alpha * lr * u
+            for p in ps:
+                p.copy_(ref.to(bf))
+        out.append((np.stack([p.to(f32).numpy() for p in ps]).astype(np.float64),
+                    np.stack([b.numpy() for b in bufs]).astype(np.float64),
+                    u.numpy().astype(np.float64), ref.numpy().astype(np.float64)))
+    return out
+
+
+def pin_torch_bf16_params(use=None):
+    """The stress storage types (bf16 parameters, fp32 momentum, u and
+    anchor) against the torch rendition above.  torch rounds after every
+    tensor operation where the oracle rounds once per stored tensor, so:
+      * fp32 momentum agrees to a few ulps of the updates' operands (a result
+        may cancel, so ulps are taken at the largest |m| or summed gradient
+        the coordinate has seen so far);
+      * a bf16 parameter may land one bf16 ulp away where such a difference
+        meets a rounding boundary; that must stay rare (at most 1 % of the
+        coordinates over the run) and be exactly one ulp;
+      * until its first parameter flip, a coordinate's anchor and lr*u agree
+        to a few fp32 ulps of the anchor (after a flip the mean and so the
+        SlowMo state legitimately move by up to a bf16 ulp / W)."""
+    rng = np.random.default_rng(47)
+    f32 = lambda x: float(np.float32(x))  # noqa: E731
+    W, P, K, n = 4, 512, 2, 10
+    lr, mu, beta, alpha = f32(0.1), f32(0.9), f32(0.5), 1.0
+    theta0 = rng.normal(0, 0.02, P).astype(np.float32).astype(np.float64)
+    grads = [rng.normal(0, 1e-3, (W, P)).astype(np.float32).astype(np.float64)
+             for _ in range(n)]
+    ref = _torch_bf16_cpdp(theta0, grads, W, K, lr, mu, beta, alpha)
+    rec = []
+    oracle.run(theta0, lambda s, W_, P_: grads[s - 1], W, K, n, lr, mu, beta, alpha,
+               param_dt="bf16", mom_dt="f32", aux_dt="f32", use=use,
+               callback=lambda s, kind, st: rec.append(st.copy()))
+    sp = lambda x: np.spacing(np.abs(np.asarray(x)).astype(np.float32)).astype(np.float64)  # noqa: E731
+    flipped = np.zeros(P, dtype=bool)
+    m_scale = np.zeros((W, P))
+    for s, (st, (p_ref, m_ref, u_ref, a_ref)) in enumerate(zip(rec, ref), start=1):
+        tag = f"bf16 rendition step {s}"
+        off = np.abs(st.params - p_ref)
+        assert ((off == 0) | (off == sp(p_ref) * 2 ** 16)).all(), \
+            tag + f": a parameter differs by other than one bf16 ulp ({off.max():.2e})"
+        flipped |= (off > 0).any(axis=0)
+        assert flipped.mean() <= 0.01, tag + f": {flipped.mean():.3f} of coordinates flipped"
+        g = grads[s - 1]
+        # operands of the buffer update: the gradient rows it sums (at a sync,
+        # all W of them) and the buffer itself
+        g_ops = np.tile(np.abs(g).max(axis=0), (W, 1)) if s % K == 0 else np.abs(g)
+        m_scale = np.maximum(m_scale, np.maximum(np.abs(m_ref), g_ops))
+        assert (np.abs(st.mom - m_ref) <= 4 * sp(m_scale)).all(), tag + ": mom"
+        ok = ~flipped
+        scale = sp(a_ref)
+        assert (np.abs(st.anchor - a_ref) <= 8 * scale)[ok].all(), tag + ": anchor"
+        assert (np.abs(lr * (st.slow - u_ref)) <= 8 * scale)[ok].all(), tag + ": lr*u"
+
+
+ALL_PINS.append(pin_torch_bf16_params)
