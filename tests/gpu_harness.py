@@ -202,9 +202,21 @@ class GpuRun:
         return out
 
 
+def state_from_grads(opt: dict | None, mom_dt: str = "f32") -> bool:
+    """True when the optimizer state (momentum, AdamW's moments) is a function
+    of the gradients alone and stored in fp32: momentum SGD without weight
+    decay, or AdamW.  Such state never reads a parameter, so bf16 parameter
+    flips cannot reach it and it keeps the fp32 gate in a bf16 run (SGD with
+    coupled weight decay reads theta, bf16 momentum is itself rounded to
+    bf16)."""
+    if mom_dt != "f32":
+        return False
+    return opt is None or opt.get("kind") == "adamw" or not opt.get("weight_decay", 0.0)
+
+
 def compare(gpu: dict, ref: "oracle.OracleState", param_dt: str, tag: str,
             mom2=None, scaled: bool = False, velocity_lr: float | None = None,
-            lr: float | None = None):
+            lr: float | None = None, fp32_state: bool = False):
     """Assert the GPU snapshot matches the oracle state within tolerance.
     scaled=True additionally tightens the fp32 absolute tolerance of the
     optimizer-state families (mom, mom2) to 1e-6 of their RMS: AdamW moments
@@ -231,7 +243,7 @@ def compare(gpu: dict, ref: "oracle.OracleState", param_dt: str, tag: str,
         got = gpu[name]
         assert got.shape == want.shape, (tag, name, got.shape, want.shape)
         flip = None  # the two-flip allowance of a bf16-regime family, if it has one
-        if param_dt == "f32":
+        if param_dt == "f32" or (fp32_state and name in ("mom", "mom2")):
             rtol, atol = RTOL_F32, ATOL_F32
             if scaled and name in ("mom", "mom2"):
                 fw = want[np.isfinite(want)]
@@ -338,7 +350,8 @@ def run_parity(c: Case, idx: np.ndarray | None = None, stream=None, every: int =
         vlr = c.opt32()["lr"] if c.opt is not None and c.opt["kind"] == "adamw" else None
         m = compare(snap, ref, tolerance_regime(c), f"step {s} ({kind})", mom2=m2,
                     scaled=c.opt is not None, velocity_lr=vlr,
-                    lr=c.opt32()["lr"] if c.opt is not None else c.hyper32()[0])
+                    lr=c.opt32()["lr"] if c.opt is not None else c.hyper32()[0],
+                    fp32_state=state_from_grads(c.opt, c.mom_dt))
         for k, v in m.items():
             worst[k] = max(worst.get(k, 0.0), v)
         if kind == "reconcile" and c.method != "ddp":

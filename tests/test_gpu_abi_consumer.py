@@ -12,7 +12,7 @@ import subprocess
 import numpy as np
 import pytest
 
-from gpu_harness import Case, compare, log, run_oracle
+from gpu_harness import Case, compare, log, run_oracle, state_from_grads
 from synth import gen
 
 pytestmark = pytest.mark.gpu
@@ -64,4 +64,5 @@ def test_torch_free_consumer_matches_oracle(c, tmp_path):
                 c.W, c.P).astype(np.float64),
             "slow_mom": np.fromfile(tmp_path / "slow.bin", dtype=np.float32).astype(np.float64),
             "anchor": np.fromfile(tmp_path / "anchor.bin", dtype=np.float32).astype(np.float64)}
-    compare(snap, refs[c.steps][1], c.param_dt, f"consumer {c.param_dt} final", lr=lr)
+    compare(snap, refs[c.steps][1], c.param_dt, f"consumer {c.param_dt} final", lr=lr,
+            fp32_state=state_from_grads(None))

@@ -6,7 +6,7 @@ import torch
 
 import oracle
 from gpu_harness import (Case, GpuRun, compare, log, oracle_inputs, run_parity,
-                         tolerance_regime)
+                         state_from_grads, tolerance_regime)
 from paper_2607_21224_amd import cpdp
 from paper_2607_21224_amd.state import CpdpState, Hyper
 
@@ -53,7 +53,7 @@ def _ragged_case(W, P, dt, grad_dt, mom_dt="f32"):
     for s in range(1, c.steps + 1):
         g.step(s)
         compare(g.snapshot(), refs[s], tolerance_regime(c), f"W={W} P={P} step {s}",
-                lr=c.hyper32()[0])
+                lr=c.hyper32()[0], fp32_state=state_from_grads(None, mom_dt))
     torch.cuda.synchronize()
     assert (g.st.params[:, P:].float() == -1280.0).all()
     assert (g.st.mom[:, P:] == -1280.0).all()

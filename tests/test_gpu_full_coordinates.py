@@ -1,6 +1,6 @@
 """Every coordinate of the four full-size workloads for one whole period (K-1
 local steps and the reconcile) against the oracle, after every step, in the
-benchmark's launch configuration:
+benchmark's launch configuration (longer runs on request, below):
   r50_100  ResNet-50/CIFAR-100-sized, W=8, P=23,712,932 in 161 tensors, K=4
   vit_s    ViT-S-sized, W=8, P=21,332,068, K=4
   r50_200  ResNet-50/TinyImageNet-sized, W=16, P=23,917,832, K=8, gradients
@@ -18,7 +18,15 @@ types it rounds to at every store (fp32 or bf16 parameters, fp32 momentum, u
 and anchor).  That is lossless, and every store-back asserts it.  Coordinates
 are independent, so slices of 2^21 coordinates are stepped in a thread pool
 (the oracle's C calls and numpy release the GIL), each compared with the same
-slice of the GPU state after every step."""
+slice of the GPU state after every step.
+
+By default each workload runs one period at seed 42.  Environment variables
+widen the run (a whole configured run takes several minutes per workload):
+  CPDP_FULL_PERIODS=all   the workload's configured number of periods
+  CPDP_FULL_SEEDS=42,123,777   the seeds to run (comma-separated)
+  CPDP_FULL_VARIANTS=1    also the stress state's other storage readings:
+                          bf16 gradients, and bf16 gradients and momentum"""
+import os
 from concurrent.futures import ThreadPoolExecutor
 
 import numpy as np
@@ -26,7 +34,8 @@ import pytest
 import torch
 
 import oracle
-from gpu_harness import Case, GpuRun, check_replicas_reconciled, compare, log
+from gpu_harness import (Case, GpuRun, check_replicas_reconciled, compare, log,
+                         state_from_grads, tolerance_regime)
 from synth import WORKLOADS, gen
 from synth import device as sdev
 
@@ -34,6 +43,13 @@ pytestmark = pytest.mark.gpu
 
 SLICE = 1 << 21
 WORKERS = 12
+
+WHOLE_RUN = os.environ.get("CPDP_FULL_PERIODS", "1") == "all"
+SEEDS = [int(x) for x in os.environ.get("CPDP_FULL_SEEDS", "42").split(",") if x]
+CASES = [("r50_100", "f32", "f32"), ("vit_s", "f32", "f32"), ("r50_200", "f32", "f32"),
+         ("stress", "f32", "f32")]
+if os.environ.get("CPDP_FULL_VARIANTS") == "1":
+    CASES += [("stress", "bf16", "f32"), ("stress", "bf16", "bf16")]
 
 
 def _exact_f32(x64: np.ndarray) -> np.ndarray:
@@ -55,35 +71,40 @@ def _from_bits(bits: np.ndarray) -> np.ndarray:
 class CompactState:
     """The oracle state of all coordinates in its storage types."""
 
-    def __init__(self, W: int, P: int, param_dt: str):
-        self.W, self.param_dt = W, param_dt
+    def __init__(self, W: int, P: int, param_dt: str, mom_dt: str = "f32"):
+        self.W, self.param_dt, self.mom_dt = W, param_dt, mom_dt
         self.params = np.empty((W, P), dtype=np.uint16 if param_dt == "bf16" else np.float32)
-        self.mom = np.empty((W, P), dtype=np.float32)
+        self.mom = np.empty((W, P), dtype=np.uint16 if mom_dt == "bf16" else np.float32)
         self.slow = np.empty(P, dtype=np.float32)
         self.anchor = np.empty(P, dtype=np.float32)
 
     def load(self, lo: int, hi: int) -> oracle.OracleState:
         p = self.params[:, lo:hi]
         params = _from_bits(p) if self.param_dt == "bf16" else p.astype(np.float64)
-        return oracle.OracleState(self.W, hi - lo, params, self.mom[:, lo:hi].astype(np.float64),
+        m = self.mom[:, lo:hi]
+        mom = _from_bits(m) if self.mom_dt == "bf16" else m.astype(np.float64)
+        return oracle.OracleState(self.W, hi - lo, params, mom,
                                   self.slow[lo:hi].astype(np.float64),
-                                  self.anchor[lo:hi].astype(np.float64), self.param_dt, "f32",
-                                  "f32")
+                                  self.anchor[lo:hi].astype(np.float64), self.param_dt,
+                                  self.mom_dt, "f32")
 
     def store(self, st: oracle.OracleState, lo: int, hi: int) -> None:
         self.params[:, lo:hi] = (_bf16_bits(st.params) if self.param_dt == "bf16"
                                  else _exact_f32(st.params))
-        self.mom[:, lo:hi] = _exact_f32(st.mom)
+        self.mom[:, lo:hi] = (_bf16_bits(st.mom) if self.mom_dt == "bf16"
+                              else _exact_f32(st.mom))
         self.slow[lo:hi] = _exact_f32(st.slow)
         self.anchor[lo:hi] = _exact_f32(st.anchor)
 
 
-@pytest.mark.parametrize("name", ["r50_100", "vit_s", "r50_200", "stress"])
-def test_one_period_every_coordinate(name):
+@pytest.mark.parametrize("seed", SEEDS)
+@pytest.mark.parametrize("name,gdt,mdt", CASES, ids=[f"{n}-grads_{g}-mom_{m}" for n, g, m in CASES])
+def test_every_coordinate(name, gdt, mdt, seed):
     w = WORKLOADS[name]
-    c = Case(W=w.W, P=w.P, K=w.K, lr=w.lr, mu=w.mu, beta=w.beta, alpha=w.alpha, steps=w.K,
-             param_dt=w.param_dt, ld=w.ld, seed=42, theta_sigma=w.theta_sigma,
-             grad_sigma=w.grad_sigma, outlier_rate=w.outlier_rate)
+    c = Case(W=w.W, P=w.P, K=w.K, lr=w.lr, mu=w.mu, beta=w.beta, alpha=w.alpha,
+             steps=w.steps if WHOLE_RUN else w.K, param_dt=w.param_dt, ld=w.ld, seed=seed,
+             theta_sigma=w.theta_sigma, grad_sigma=w.grad_sigma,
+             outlier_rate=w.outlier_rate, grad_dt=gdt, mom_dt=mdt)
     P, W = c.P, c.W
     lr, mu, beta, alpha = c.hyper32()
     rng = np.random.default_rng(0)
@@ -98,12 +119,13 @@ def test_one_period_every_coordinate(name):
                           gen.theta0(c.seed, sample, c.theta_sigma).view(np.uint32))
 
     slices = [(lo, min(P, lo + SLICE)) for lo in range(0, P, SLICE)]
-    ref = CompactState(W, P, c.param_dt)
+    ref = CompactState(W, P, c.param_dt, c.mom_dt)
     oracle.lib()  # load once before the worker threads call into it
 
     def init(sl):
         lo, hi = sl
-        ref.store(oracle.state_init(th0[lo:hi].astype(np.float64), W, c.param_dt), lo, hi)
+        ref.store(oracle.state_init(th0[lo:hi].astype(np.float64), W, c.param_dt, c.mom_dt),
+                  lo, hi)
 
     g = GpuRun(c)
     with ThreadPoolExecutor(WORKERS) as pool:
@@ -115,10 +137,17 @@ def test_one_period_every_coordinate(name):
             assert np.array_equal(got.view(np.uint32),
                                   gen.grads(c.seed, s, W, sample, c.grad_sigma,
                                             c.outlier_rate).view(np.uint32))
+            if c.grad_dt == "bf16":  # the rows the library read: RNE of the generated values
+                gb = g.grads_bf16[:, sample].float().cpu().numpy()
+                assert np.array_equal(gb.view(np.uint32), gen.bf16_round(got).view(np.uint32))
 
             def work(sl, s=s, kind=kind):
                 lo, hi = sl
-                g64 = g.grads[:, lo:hi].cpu().numpy().astype(np.float64)
+                g32 = g.grads[:, lo:hi].cpu().numpy()
+                if c.grad_dt == "bf16":  # the oracle steps on the stored bf16 values
+                    g32 = gen.bf16_round(g32)
+                g64 = g32.astype(np.float64)
+                del g32
                 st = ref.load(lo, hi)
                 if kind == "reconcile":
                     oracle.reconcile(st, g64, lr, mu, beta, alpha)
@@ -127,11 +156,13 @@ def test_one_period_every_coordinate(name):
                 del g64
                 ref.store(st, lo, hi)
                 snap = {"params": g.st.params[:, lo:hi].float().cpu().numpy().astype(np.float64),
-                        "mom": g.st.mom[:, lo:hi].cpu().numpy().astype(np.float64),
+                        "mom": g.st.mom[:, lo:hi].float().cpu().numpy().astype(np.float64),
                         "slow_mom": g.st.slow_mom[lo:hi].cpu().numpy().astype(np.float64),
                         "anchor": g.st.anchor[lo:hi].cpu().numpy().astype(np.float64)}
-                tag = f"{name} every coordinate, step {s} ({kind}), coordinates [{lo}, {hi})"
-                m = compare(snap, st, c.param_dt, tag, lr=lr)
+                tag = (f"{name} grads {c.grad_dt} mom {c.mom_dt} seed {c.seed} every coordinate, "
+                       f"step {s} ({kind}), coordinates [{lo}, {hi})")
+                m = compare(snap, st, tolerance_regime(c), tag, lr=lr,
+                            fp32_state=state_from_grads(None, c.mom_dt))
                 if kind == "reconcile":
                     check_replicas_reconciled(snap, c.param_dt, tag)
                 return m
@@ -140,6 +171,7 @@ def test_one_period_every_coordinate(name):
             for m in pool.map(work, slices):
                 for k, v in m.items():
                     worst[k] = max(worst.get(k, 0.0), v)
-            log(f"[full-coords] {name} step {s} {kind}: {W}x{P} coordinates match; worst "
+            log(f"[full-coords] {name} grads {c.grad_dt} mom {c.mom_dt} seed {c.seed} step {s} "
+                f"{kind}: {W}x{P} coordinates match; worst "
                 f"error / tolerance " + ", ".join(f"{k} {v:.3g}" for k, v in worst.items()))
     assert kind == "reconcile"

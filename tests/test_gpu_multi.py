@@ -6,7 +6,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_harness import Case, GpuRun, compare, log
+from gpu_harness import Case, GpuRun, compare, log, state_from_grads
 from paper_2607_21224_amd.multi import CpdpMultiState
 from paper_2607_21224_amd.state import Optimizer
 from synth import WORKLOADS, gen
@@ -116,7 +116,9 @@ def test_plan_ragged_matches_oracle(method, kind, dt, flags):
             snap["mom2"] = np.stack([multi.gather("mom2", i).cpu().numpy()
                                      for i in range(W)]).astype(np.float64)
         compare(snap, ref, dt, f"{method} {kind} step {s}", mom2=m2 if kind == "adamw" else None,
-                scaled=True, velocity_lr=opt.lr if kind == "adamw" else None, lr=opt.lr)
+                scaled=True, velocity_lr=opt.lr if kind == "adamw" else None, lr=opt.lr,
+                fp32_state=state_from_grads({"kind": opt.kind,
+                                             "weight_decay": opt.weight_decay}))
 
 
 @pytest.mark.parametrize("method,flags", [("cpdp", 0), ("cpdp", 3), ("localsgd", 0), ("ddp", 1)])

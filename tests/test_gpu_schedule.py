@@ -7,7 +7,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_harness import Case, GpuRun, compare, oracle_inputs
+from gpu_harness import Case, GpuRun, compare, oracle_inputs, state_from_grads
 from paper_2607_21224_amd import cpdp
 from paper_2607_21224_amd.state import Hyper
 
@@ -46,5 +46,5 @@ def test_warmup_and_lr_schedule(method, dt):
         # during the warmup ramp (lr 0.02 ... 0.1) one fp32-ulp flip of one
         # replica moves u by ulp/(W*lr), at the edge of a 1e-6 relative gate
         compare(g.snapshot(), ref, dt, f"{method} step {s} ({kind})",
-                velocity_lr=lr_gpu[s - 1])
+                velocity_lr=lr_gpu[s - 1], fp32_state=state_from_grads(None))
     torch.cuda.synchronize()
