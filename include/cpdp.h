@@ -64,7 +64,9 @@ typedef enum {
     CPDP_ERR_MISALIGNED = 3,  /* pointer or row stride not 16-byte aligned   */
     CPDP_ERR_OVERLAP = 4,     /* two argument ranges overlap                 */
     CPDP_ERR_DTYPE = 5,       /* unsupported storage-type combination        */
-    CPDP_ERR_HIP = 6          /* the HIP runtime rejected the launch         */
+    CPDP_ERR_HIP = 6,         /* the HIP runtime rejected the launch         */
+    CPDP_ERR_TOO_LARGE = 7    /* beyond a fixed library buffer
+                                 (cpdp_plan_build_static)                    */
 } cpdp_status;
 
 /*
@@ -274,6 +276,35 @@ int cpdp_plan_build(cpdp_plan* plan, int64_t plan_bytes, int W, int n_tensors,
                     void* const* mom, void* const* mom2, void* const* grads,
                     float* const* slow_mom, float* const* anchor,
                     int param_dt);
+
+/* Bytes of the library's own plan table on each GPU (cpdp_plan_build_static). */
+#define CPDP_PLAN_STATIC_BYTES 262144
+
+/*
+ * cpdp_plan_build for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Same arguments and checks as cpdp_plan_build, but the table is a fixed
+ * array of CPDP_PLAN_STATIC_BYTES that the library keeps on every GPU it runs
+ * on until the process ends; plan->table is set to that array's address on
+ * the current device (its input value is ignored).  The call allocates
+ * nothing, on the device or on the host; it copies the table synchronously,
+ * like cpdp_plan_build.
+ *   - CPDP_ERR_TOO_LARGE when cpdp_plan_bytes(W, n_tensors) exceeds
+ *     CPDP_PLAN_STATIC_BYTES (no HIP call is made); CPDP_ERR_HIP when the
+ *     array's address cannot be resolved or the copy fails.
+ *   - One table per GPU: a static build replaces the table of the previous
+ *     static build on that GPU.  Step calls on a plan from an earlier static
+ *     build then return CPDP_ERR_INVALID_ARG instead of reading the new
+ *     table; cpdp_plan_build never writes into this array.
+ *   - A static build while kernels of an earlier static plan on that GPU may
+ *     still be running races with them: synchronize the GPU first.  Static
+ *     builds themselves are serialised by the library.
+ */
+int cpdp_plan_build_static(cpdp_plan* plan, int W, int n_tensors,
+                           const int64_t* numel, void* const* params,
+                           void* const* mom, void* const* mom2, void* const* grads,
+                           float* const* slow_mom, float* const* anchor,
+                           int param_dt);
 
 /*
  * Initialisation of Algorithm 1 over a plan: the reference model (the plan's

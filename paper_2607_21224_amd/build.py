@@ -31,6 +31,8 @@ KERNEL_SOURCES = ("kernels_flat.hip", "kernels_sync_cpdp.hip", "kernels_sync_loc
 # headers the kernel sources include (part of what the recorded traffic is for)
 KERNEL_HEADERS = ("cpdp_device.h", "cpdp_sync_impl.h", "cpdp_plan_impl.h", "cpdp_launch.h")
 HOST_SOURCES = ("cpdp_api.cpp",)
+# the library's own device memory (no kernels): the static plan table
+SCRATCH_SOURCES = ("plan_scratch.hip",)
 OBJ_ROOT = os.path.join(ROOT, "_build")
 
 
@@ -45,7 +47,7 @@ def build_cpdp(out: str = LIB_CPDP, extra=()) -> str:
     csrc = os.path.join(PKG, "csrc")
     objdir = os.path.join(OBJ_ROOT, os.path.basename(out) + ".objs")
     os.makedirs(objdir, exist_ok=True)
-    sources = KERNEL_SOURCES + HOST_SOURCES
+    sources = KERNEL_SOURCES + HOST_SOURCES + SCRATCH_SOURCES
 
     def compile_one(name):
         obj = os.path.join(objdir, name + ".o")

@@ -28,6 +28,8 @@ CPDP_ERR_MISALIGNED = 3
 CPDP_ERR_OVERLAP = 4
 CPDP_ERR_DTYPE = 5
 CPDP_ERR_HIP = 6
+CPDP_ERR_TOO_LARGE = 7
+CPDP_PLAN_STATIC_BYTES = 262144
 
 DTYPES = {"f32": CPDP_F32, "bf16": CPDP_BF16}
 
@@ -36,7 +38,7 @@ EXPORTS = ("cpdp_state_init", "cpdp_local_step", "cpdp_reconcile",
            "cpdp_localsgd_sync", "cpdp_ddp_step", "cpdp_state_init_opt",
            "cpdp_local_step_opt", "cpdp_sync_step_opt", "cpdp_is_sync_step",
            "cpdp_period_for_epoch", "cpdp_lr_at", "cpdp_linear_scaled_lr",
-           "cpdp_plan_bytes", "cpdp_plan_build",
+           "cpdp_plan_bytes", "cpdp_plan_build", "cpdp_plan_build_static",
            "cpdp_state_init_plan", "cpdp_local_step_plan", "cpdp_sync_step_plan",
            "cpdp_step_table_bytes", "cpdp_step_table_fill", "cpdp_step_table_set_position",
            "cpdp_step_table_advance", "cpdp_step_table_position", "cpdp_local_step_table",
@@ -110,6 +112,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                     ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp),
                                     ctypes.POINTER(vp), ctypes.POINTER(vp), i]
     lib.cpdp_plan_build.restype = i
+    lib.cpdp_plan_build_static.argtypes = [pp, i, i, ctypes.POINTER(i64), ctypes.POINTER(vp),
+                                           ctypes.POINTER(vp), ctypes.POINTER(vp),
+                                           ctypes.POINTER(vp), ctypes.POINTER(vp),
+                                           ctypes.POINTER(vp), i]
+    lib.cpdp_plan_build_static.restype = i
     lib.cpdp_state_init_plan.argtypes = [pp, vp]
     lib.cpdp_state_init_plan.restype = i
     lib.cpdp_local_step_plan.argtypes = [pp, i, op, vp]
@@ -390,13 +397,12 @@ def _ptr_array(xs):
     return ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p)), arr
 
 
-def cpdp_plan_build(plan: cpdp_plan, plan_bytes, W, n_tensors, numel, params, mom, mom2,
-                    grads, slow_mom, anchor, param_dt=CPDP_F32, check=True):
-    """numel: n ints; params/mom/grads/mom2: W*n tensors or addresses,
-    replica-major ([i*n + t]); slow_mom/anchor: n tensors or None."""
+def _plan_arrays(W, n_tensors, numel, params, mom, mom2, grads, slow_mom, anchor, param_dt):
+    """The host arrays of a plan build, checked against the tensors they
+    name.  Returns (numel array, [params, mom, mom2, grads, slow_mom, anchor]
+    pointer arrays, the Python objects that must outlive the call)."""
     keep = []
     numel = [int(x) for x in numel]
-
     if len(numel) != int(n_tensors):
         raise ValueError(f"numel has {len(numel)} entries for {n_tensors} tensors")
 
@@ -415,12 +421,35 @@ def cpdp_plan_build(plan: cpdp_plan, plan_bytes, W, n_tensors, numel, params, mo
         return r[0]
     wn = int(W) * len(numel) if int(W) > 0 else 0
     nm = (ctypes.c_int64 * len(numel))(*numel)
+    ptrs = [arr(params, param_dt, "params", wn), arr(mom, CPDP_F32, "mom", wn),
+            arr(mom2, CPDP_F32, "mom2", wn), arr(grads, CPDP_F32, "grads", wn),
+            arr(slow_mom, CPDP_F32, "slow_mom", len(numel)),
+            arr(anchor, CPDP_F32, "anchor", len(numel))]
+    return nm, ptrs, keep
+
+
+def cpdp_plan_build(plan: cpdp_plan, plan_bytes, W, n_tensors, numel, params, mom, mom2,
+                    grads, slow_mom, anchor, param_dt=CPDP_F32, check=True):
+    """numel: n ints; params/mom/grads/mom2: W*n tensors or addresses,
+    replica-major ([i*n + t]); slow_mom/anchor: n tensors or None."""
+    nm, ptrs, keep = _plan_arrays(W, n_tensors, numel, params, mom, mom2, grads, slow_mom,
+                                  anchor, param_dt)
     s = lib.cpdp_plan_build(ctypes.byref(plan), int(plan_bytes), int(W), int(n_tensors), nm,
-                            arr(params, param_dt, "params", wn), arr(mom, CPDP_F32, "mom", wn),
-                            arr(mom2, CPDP_F32, "mom2", wn), arr(grads, CPDP_F32, "grads", wn),
-                            arr(slow_mom, CPDP_F32, "slow_mom", len(numel)),
-                            arr(anchor, CPDP_F32, "anchor", len(numel)), _dt(param_dt))
+                            *ptrs, _dt(param_dt))
+    del keep
     return _done(s, "cpdp_plan_build", check)
+
+
+def cpdp_plan_build_static(plan: cpdp_plan, W, n_tensors, numel, params, mom, mom2, grads,
+                           slow_mom, anchor, param_dt=CPDP_F32, check=True):
+    """cpdp_plan_build into the library's own table on the current device
+    (no allocation anywhere); sets plan.table.  Arguments as cpdp_plan_build."""
+    nm, ptrs, keep = _plan_arrays(W, n_tensors, numel, params, mom, mom2, grads, slow_mom,
+                                  anchor, param_dt)
+    s = lib.cpdp_plan_build_static(ctypes.byref(plan), int(W), int(n_tensors), nm, *ptrs,
+                                   _dt(param_dt))
+    del keep
+    return _done(s, "cpdp_plan_build_static", check)
 
 
 def cpdp_state_init_plan(plan: cpdp_plan, stream=None, check=True):

@@ -9,10 +9,12 @@
 #include <cmath>
 #include <cstdint>
 #include <limits>
+#include <mutex>
 #include <utility>
 #include <vector>
 
 #include "cpdp_launch.h"
+#include "plan_scratch.h"
 
 namespace {
 
@@ -407,24 +409,22 @@ int64_t cpdp_plan_bytes(int W, int n_tensors) {
     return cpdp::plan_words(W, n_tensors) * (int64_t)sizeof(int64_t);
 }
 
-int cpdp_plan_build(cpdp_plan* plan, int64_t plan_bytes, int W, int n, const int64_t* numel,
-                    void* const* params, void* const* mom, void* const* mom2,
-                    void* const* grads, float* const* slow_mom, float* const* anchor,
-                    int param_dt) {
-    if (plan == nullptr || numel == nullptr || params == nullptr || mom == nullptr ||
-        grads == nullptr)
-        return CPDP_ERR_NULL;
-    if (W < 1 || n < 1 || W > 4096 || n > (1 << 24)) return CPDP_ERR_INVALID_ARG;
-    if (!is_dtype(param_dt)) return CPDP_ERR_DTYPE;
-    if (plan->table == nullptr) return CPDP_ERR_NULL;
-    if ((reinterpret_cast<uintptr_t>(plan->table) & 7u) != 0) return CPDP_ERR_MISALIGNED;
-    const int64_t words = cpdp::plan_words(W, n);
-    if (plan_bytes < words * (int64_t)sizeof(int64_t)) return CPDP_ERR_INVALID_ARG;
+namespace {
 
+using Span = std::pair<uintptr_t, uintptr_t>;
+
+// Fill the words of a plan table (layout in cpdp_launch.h) and validate every
+// described range: non-NULL, 16-byte aligned, no overlaps.  `ranges` has room
+// for at least 4*W*n + 2*n entries (sorted in place).  On success *chunks and
+// *total hold the plan's chunk and element counts.
+int fill_plan(int64_t* tab, int64_t words, Span* ranges, int W, int n, const int64_t* numel,
+              void* const* params, void* const* mom, void* const* mom2, void* const* grads,
+              float* const* slow_mom, float* const* anchor, int param_dt, int64_t* chunks_out,
+              int64_t* total_out) {
     const int64_t per_block = cpdp::coords_per_block();
     const size_t sp = esize(param_dt);
-    std::vector<int64_t> tab((size_t)words, 0);
-    int64_t* start = tab.data() + cpdp::kPlanHeaderWords;
+    std::fill(tab, tab + words, (int64_t)0);
+    int64_t* start = tab + cpdp::kPlanHeaderWords;
     int64_t* cnt = start + (n + 1);
     int64_t* tp = cnt + n;
     int64_t* tm = tp + (int64_t)W * n;
@@ -432,14 +432,14 @@ int cpdp_plan_build(cpdp_plan* plan, int64_t plan_bytes, int W, int n, const int
     int64_t* tg = tv + (int64_t)W * n;
     int64_t* ts = tg + (int64_t)W * n;
     int64_t* ta = ts + n;
-    std::vector<std::pair<uintptr_t, uintptr_t>> ranges;
+    size_t nr = 0;
     auto add = [&](const void* p, int64_t elems, size_t es) -> int {
         if (p == nullptr) return CPDP_ERR_NULL;
         if (!aligned16(p)) return CPDP_ERR_MISALIGNED;
         const uintptr_t lo = reinterpret_cast<uintptr_t>(p);
         const uintptr_t hi = lo + (uintptr_t)(elems * (int64_t)es);
         if (hi < lo) return CPDP_ERR_INVALID_ARG;
-        ranges.emplace_back(lo, hi);
+        ranges[nr++] = Span(lo, hi);
         return CPDP_OK;
     };
     int64_t chunks = 0, total = 0;
@@ -475,22 +475,110 @@ int cpdp_plan_build(cpdp_plan* plan, int64_t plan_bytes, int W, int n, const int
             if (int s = add(anchor[t], P, 4)) return s;
     }
     start[n] = chunks;
-    std::sort(ranges.begin(), ranges.end());
-    for (size_t k = 1; k < ranges.size(); ++k)
+    std::sort(ranges, ranges + nr);
+    for (size_t k = 1; k < nr; ++k)
         if (ranges[k].first < ranges[k - 1].second) return CPDP_ERR_OVERLAP;
     tab[0] = W;
     tab[1] = n;
     tab[2] = chunks;
-    if (cpdp::upload_plan(plan->table, tab.data(), words) != 0) return CPDP_ERR_HIP;
+    *chunks_out = chunks;
+    *total_out = total;
+    return CPDP_OK;
+}
+
+void set_plan_fields(cpdp_plan* plan, int W, int n, int param_dt, bool has_mom2, bool has_slow,
+                     bool has_anchor, int64_t chunks, int64_t total) {
     plan->W = W;
     plan->n_tensors = n;
     plan->param_dt = param_dt;
-    plan->has_mom2 = mom2 != nullptr;
-    plan->has_slow_mom = slow_mom != nullptr;
-    plan->has_anchor = anchor != nullptr;
+    plan->has_mom2 = has_mom2;
+    plan->has_slow_mom = has_slow;
+    plan->has_anchor = has_anchor;
     plan->total_chunks = chunks;
     plan->total_numel = total;
+}
+
+int check_plan_args(const cpdp_plan* plan, int W, int n, const int64_t* numel,
+                    void* const* params, void* const* mom, void* const* grads, int param_dt) {
+    if (plan == nullptr || numel == nullptr || params == nullptr || mom == nullptr ||
+        grads == nullptr)
+        return CPDP_ERR_NULL;
+    if (W < 1 || n < 1 || W > 4096 || n > (1 << 24)) return CPDP_ERR_INVALID_ARG;
+    if (!is_dtype(param_dt)) return CPDP_ERR_DTYPE;
+    return CPDP_OK;
+}
+
+// The static plan tables (cpdp_plan_build_static): host buffers the build
+// fills before its copy, and per device the seal of the plan its table
+// currently holds.  One lock serialises static builds and seal lookups.
+constexpr int kStaticDevices = 64;
+std::mutex g_static_mu;
+int64_t g_static_words[cpdp::kPlanScratchWords];
+Span g_static_ranges[cpdp::kPlanScratchWords];
+uint64_t g_static_seal[kStaticDevices];    // seal handed out by the last build (0: none)
+uint64_t g_static_fields[kStaticDevices];  // plan_seal() of that build's handle fields
+uint64_t g_static_builds = 0;
+
+}  // namespace
+
+int cpdp_plan_build(cpdp_plan* plan, int64_t plan_bytes, int W, int n, const int64_t* numel,
+                    void* const* params, void* const* mom, void* const* mom2,
+                    void* const* grads, float* const* slow_mom, float* const* anchor,
+                    int param_dt) {
+    if (int s = check_plan_args(plan, W, n, numel, params, mom, grads, param_dt)) return s;
+    if (plan->table == nullptr) return CPDP_ERR_NULL;
+    if ((reinterpret_cast<uintptr_t>(plan->table) & 7u) != 0) return CPDP_ERR_MISALIGNED;
+    // a table the library owns is filled by cpdp_plan_build_static only
+    if (cpdp::plan_scratch_device(plan->table) >= 0) return CPDP_ERR_INVALID_ARG;
+    const int64_t words = cpdp::plan_words(W, n);
+    if (plan_bytes < words * (int64_t)sizeof(int64_t)) return CPDP_ERR_INVALID_ARG;
+
+    std::vector<int64_t> tab((size_t)words, 0);
+    std::vector<Span> ranges((size_t)(4 * (int64_t)W * n + 2 * (int64_t)n));
+    int64_t chunks = 0, total = 0;
+    if (int s = fill_plan(tab.data(), words, ranges.data(), W, n, numel, params, mom, mom2,
+                          grads, slow_mom, anchor, param_dt, &chunks, &total))
+        return s;
+    if (cpdp::upload_plan(plan->table, tab.data(), words) != 0) return CPDP_ERR_HIP;
+    set_plan_fields(plan, W, n, param_dt, mom2 != nullptr, slow_mom != nullptr,
+                    anchor != nullptr, chunks, total);
     plan->seal = plan_seal(plan);
+    return CPDP_OK;
+}
+
+int cpdp_plan_build_static(cpdp_plan* plan, int W, int n, const int64_t* numel,
+                           void* const* params, void* const* mom, void* const* mom2,
+                           void* const* grads, float* const* slow_mom, float* const* anchor,
+                           int param_dt) {
+    if (int s = check_plan_args(plan, W, n, numel, params, mom, grads, param_dt)) return s;
+    const int64_t words = cpdp::plan_words(W, n);
+    if (words > cpdp::kPlanScratchWords) return CPDP_ERR_TOO_LARGE;
+
+    std::lock_guard<std::mutex> lock(g_static_mu);
+    int64_t chunks = 0, total = 0;
+    if (int s = fill_plan(g_static_words, words, g_static_ranges, W, n, numel, params, mom, mom2,
+                          grads, slow_mom, anchor, param_dt, &chunks, &total))
+        return s;
+    void* table = nullptr;
+    if (cpdp::plan_scratch(&table) != 0) return CPDP_ERR_HIP;
+    const int dev = cpdp::plan_scratch_device(table);
+    if (dev < 0 || dev >= kStaticDevices) return CPDP_ERR_HIP;
+    // plans built on this device before now stop working from here on, even
+    // if the copy below fails: their table is about to change
+    g_static_seal[dev] = 0;
+    if (cpdp::upload_plan(table, g_static_words, words) != 0) return CPDP_ERR_HIP;
+    plan->table = table;
+    set_plan_fields(plan, W, n, param_dt, mom2 != nullptr, slow_mom != nullptr,
+                    anchor != nullptr, chunks, total);
+    // the seal also carries the build count, so a handle from an earlier static
+    // build on this device no longer matches
+    const uint64_t build = ++g_static_builds;
+    const uint64_t fields = plan_seal(plan);
+    uint64_t seal = fields ^ (build * 0x9E3779B97F4A7C15ull);
+    if (seal == 0) seal = 1;  // 0 marks a device without a valid static plan
+    plan->seal = seal;
+    g_static_fields[dev] = fields;
+    g_static_seal[dev] = seal;
     return CPDP_OK;
 }
 
@@ -503,7 +591,18 @@ static int check_plan(const cpdp_plan* plan) {
 
 // The launch shape and the table layout the kernels assume come from the
 // handle, so a step call runs only on the exact fields cpdp_plan_build wrote.
+// A plan on a device's static table must carry the seal of that table's last
+// static build, with the fields that build wrote.
 static int check_seal(const cpdp_plan* plan) {
+    const int dev = cpdp::plan_scratch_device(plan->table);
+    if (dev >= 0) {
+        const uint64_t fields = plan_seal(plan);
+        std::lock_guard<std::mutex> lock(g_static_mu);
+        return dev < kStaticDevices && g_static_seal[dev] != 0 &&
+                       plan->seal == g_static_seal[dev] && fields == g_static_fields[dev]
+                   ? CPDP_OK
+                   : CPDP_ERR_INVALID_ARG;
+    }
     return plan->seal == plan_seal(plan) ? CPDP_OK : CPDP_ERR_INVALID_ARG;
 }
 
@@ -751,6 +850,9 @@ const char* cpdp_status_str(int status) {
         case CPDP_ERR_OVERLAP: return "CPDP_ERR_OVERLAP: argument ranges overlap";
         case CPDP_ERR_DTYPE: return "CPDP_ERR_DTYPE: unsupported storage-type combination";
         case CPDP_ERR_HIP: return "CPDP_ERR_HIP: the HIP runtime rejected the launch";
+        case CPDP_ERR_TOO_LARGE:
+            return "CPDP_ERR_TOO_LARGE: the plan table exceeds the library's fixed "
+                   "CPDP_PLAN_STATIC_BYTES buffer";
         default: return "CPDP: unknown status";
     }
 }

@@ -115,6 +115,25 @@ int main() {
         EXPECT(cpdp_sync_step_plan(2, &plan, 4, &sgd, 0.5f, 1.0f, 0u, nullptr), CPDP_OK, true);
         adam.step = 1;
         EXPECT(cpdp_local_step_plan(&plan, 4, &adam, nullptr), CPDP_ERR_NULL, false);
+
+        // the allocation-free build: the library's own table, stale handles
+        // rejected, oversized plans refused before any runtime call
+        cpdp_plan sp = {};
+        EXPECT(cpdp_plan_build_static(&sp, W, n, numel, tp, tm, tv, tg, ts, ta, 0), CPDP_OK, false);
+        if (sp.table == nullptr || sp.total_chunks != 3) { std::printf("FAIL static plan\n"); ++failures; }
+        EXPECT(cpdp_local_step_plan(&sp, 4, &sgd, nullptr), CPDP_OK, true);
+        cpdp_plan sp2 = {};
+        EXPECT(cpdp_plan_build_static(&sp2, W, n - 1, numel, tp, tm, tv, tg, ts, ta, 0), CPDP_OK, false);
+        EXPECT(cpdp_local_step_plan(&sp, 4, &sgd, nullptr), CPDP_ERR_INVALID_ARG, false);
+        EXPECT(cpdp_local_step_plan(&sp2, 4, &sgd, nullptr), CPDP_OK, true);
+        cpdp_plan into = sp2;  // cpdp_plan_build never writes the library's table
+        EXPECT(cpdp_plan_build(&into, bytes, W, n, numel, tp, tm, tv, tg, ts, ta, 0), CPDP_ERR_INVALID_ARG, false);
+        EXPECT(cpdp_local_step_plan(&sp2, 4, &sgd, nullptr), CPDP_OK, true);
+        sp2.W += 1;  // an edited static handle fails its seal too
+        EXPECT(cpdp_local_step_plan(&sp2, 4, &sgd, nullptr), CPDP_ERR_INVALID_ARG, false);
+        EXPECT(cpdp_plan_build_static(&sp, 4096, 1024, numel, tp, tm, tv, tg, ts, ta, 0), CPDP_ERR_TOO_LARGE, false);
+        EXPECT(cpdp_plan_build_static(nullptr, W, n, numel, tp, tm, tv, tg, ts, ta, 0), CPDP_ERR_NULL, false);
+        EXPECT(cpdp_plan_build_static(&sp, W, n, numel, tp, tm, tv, tg, ts, ta, 9), CPDP_ERR_DTYPE, false);
     }
 
     {

@@ -2,6 +2,7 @@
 // (cpdp_api.cpp) can be built with g++ under AddressSanitizer/UBSan on a
 // machine without a GPU.  Every launcher records that it was reached.
 #include "cpdp_launch.h"
+#include "plan_scratch.h"
 
 int g_launches = 0;
 
@@ -59,4 +60,8 @@ int g_uploaded_words = 0;
 int upload_plan(void*, const int64_t*, int64_t words) { return g_uploaded_words = (int)words, 0; }
 bool grid_fits(int rows, int64_t P) { return rows >= 1 && (P + 1023) / 1024 <= kMaxBlocks / rows; }
 const char* hip_error_string(int) { return "stub"; }
+// a host array stands in for the device's static plan table
+alignas(256) int64_t g_plan_scratch[kPlanScratchWords];
+int plan_scratch(void** ptr) { return *ptr = g_plan_scratch, 0; }
+int plan_scratch_device(const void* table) { return table == g_plan_scratch ? 0 : -1; }
 }  // namespace cpdp
