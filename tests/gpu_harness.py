@@ -216,7 +216,7 @@ def state_from_grads(opt: dict | None, mom_dt: str = "f32") -> bool:
 
 def compare(gpu: dict, ref: "oracle.OracleState", param_dt: str, tag: str,
             mom2=None, scaled: bool = False, velocity_lr: float | None = None,
-            lr: float | None = None, fp32_state: bool = False):
+            lr: float | None = None, fp32_state: bool = False, exceptions: list | None = None):
     """Assert the GPU snapshot matches the oracle state within tolerance.
     scaled=True additionally tightens the fp32 absolute tolerance of the
     optimizer-state families (mom, mom2) to 1e-6 of their RMS: AdamW moments
@@ -294,6 +294,12 @@ def compare(gpu: dict, ref: "oracle.OracleState", param_dt: str, tag: str,
             if int(bad.sum()) <= allowed and not (err > loose).any():
                 margins[name] = float(np.max(err / loose))
                 margins[name + " tight-tier exceptions"] = int(bad.sum())
+                if exceptions is not None:
+                    where = np.argwhere(fin)[np.nonzero(bad)[0]]
+                    for w_, k in zip(where, np.nonzero(bad)[0]):
+                        row, col = (int(w_[0]), int(w_[1])) if w_.size == 2 else (0, int(w_[0]))
+                        exceptions.append((name, row, col, float(got[fin][k]), float(want[fin][k]),
+                                           float(err[k] / lim[k]), float(err[k] / loose[k])))
                 bad = np.zeros_like(bad)
         if bad.any():
             k = np.argmax(err - lim)

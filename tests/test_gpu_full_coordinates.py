@@ -161,8 +161,14 @@ def test_every_coordinate(name, gdt, mdt, seed):
                         "anchor": g.st.anchor[lo:hi].cpu().numpy().astype(np.float64)}
                 tag = (f"{name} grads {c.grad_dt} mom {c.mom_dt} seed {c.seed} every coordinate, "
                        f"step {s} ({kind}), coordinates [{lo}, {hi})")
+                exc = []
                 m = compare(snap, st, tolerance_regime(c), tag, lr=lr,
-                            fp32_state=state_from_grads(None, c.mom_dt))
+                            fp32_state=state_from_grads(None, c.mom_dt), exceptions=exc)
+                for fam, row, col, got_v, want_v, r_tight, r_loose in exc:
+                    log(f"[full-coords] {name} seed {c.seed} step {s}: tight-tier exception "
+                        f"{fam} replica {row} coordinate {lo + col}: got {got_v!r} want "
+                        f"{want_v!r} ({r_tight:.3f} of the tight limit, {r_loose:.3f} of the "
+                        f"loose one)")
                 if kind == "reconcile":
                     check_replicas_reconciled(snap, c.param_dt, tag)
                 return m
