@@ -246,9 +246,10 @@ def shape_probe(w, only=None, reps: int = 10) -> dict:
     """Bandwidth ceilings of traffic shapes, measured with the no-arithmetic
     shape kernel (synth/synth.hip) on fresh buffers sized like workload w:
       reconcile_rows*   the reconcile's exact rows in the library's layout
-                        (W rows per family at stride ld), plain block order,
-                        blocks dealt to XCDs in contiguous eighths, and read
-                        batches of 16 instead of 8;
+                        (W rows per family at stride ld) and its block shape
+                        (64 threads), plain block order; blocks dealt to XCDs
+                        in contiguous eighths; read batches of 16 instead of
+                        8; blocks of 128 ... 1024 threads;
       reconcile_tile<T> the same rows and bytes in a coordinate-tile-major
                         layout: tile t holds coordinates [tT, (t+1)T) of every
                         row back to back (g_0..g_{W-1}, m_0, th_0, ..., u, a);
@@ -292,6 +293,9 @@ def shape_probe(w, only=None, reps: int = 10) -> dict:
     run("reconcile_rows_xcd", lambda: ShapePass(rows, P, xcd=True),
         "blocks in contiguous eighths per XCD")
     run("reconcile_rows_batch16", lambda: ShapePass(rows, P, batch=16))
+    for th in (128, 256, 512, 1024):
+        run(f"reconcile_rows_t{th}", lambda: ShapePass(rows, P, threads=th),
+            f"blocks of {th} threads ({4 * th} coordinates)")
     del st, g, rows
     torch.cuda.empty_cache()
 

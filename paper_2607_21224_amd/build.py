@@ -11,9 +11,9 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
 LIB_CPDP = os.path.join(PKG, "libcpdp.so")
-# the same sources with 64-thread blocks: a different launch shape for the
+# the same sources with 256-thread blocks: a different launch shape for the
 # tests that check results do not depend on it
-LIB_CPDP_BLOCK64 = os.path.join(PKG, "libcpdp_block64.so")
+LIB_CPDP_BLOCK256 = os.path.join(PKG, "libcpdp_block256.so")
 LIB_SYNTH = os.path.join(ROOT, "synth", "libsynth.so")
 
 # -ffp-contract=off: only the explicit fmaf calls fuse, so the arithmetic is
@@ -87,7 +87,7 @@ def build_all() -> None:
     from concurrent.futures import ThreadPoolExecutor
     with ThreadPoolExecutor(3) as ex:
         jobs = [ex.submit(build_cpdp), ex.submit(build_synth),
-                ex.submit(build_cpdp, LIB_CPDP_BLOCK64, ("-DCPDP_BLOCK=64",))]
+                ex.submit(build_cpdp, LIB_CPDP_BLOCK256, ("-DCPDP_BLOCK=256",))]
         for j in jobs:
             j.result()
     build_consumer()

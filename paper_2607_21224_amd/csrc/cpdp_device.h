@@ -35,8 +35,13 @@
 namespace cpdp {
 namespace {
 
+// One wavefront per block.  On MI355X 64-thread blocks ran the reconcile
+// 2.6-3.1 % and the local step 1-3.7 % faster than 256-thread blocks on the
+// fp32 ResNet-50 / ViT-S sized states (level on the 32-replica bf16 state):
+// single-wave blocks refill a CU's wave slots one at a time.  Results do not
+// depend on it (every thread owns its 4 coordinates).
 #ifndef CPDP_BLOCK
-#define CPDP_BLOCK 256
+#define CPDP_BLOCK 64
 #endif
 constexpr int kBlock = CPDP_BLOCK;
 constexpr int kVec = 4;
@@ -348,8 +353,12 @@ __device__ __forceinline__ void local_dispatch(const OptParams& o, typename PS::
 // kSyncAverageState replaces every replica's optimizer state by the replica
 // mean after the step.
 
+// Replica batch of the synchronisation steps.  With 64-thread blocks,
+// batches of 4 were level with or up to 1.5 % faster than batches of 8 (and
+// batches of 2 slower) on the reconcile of the four full-size states; the
+// batching does not change the arithmetic or its order.
 #ifndef CPDP_RECON_CHUNK
-#define CPDP_RECON_CHUNK 8
+#define CPDP_RECON_CHUNK 4
 #endif
 constexpr int kChunk = CPDP_RECON_CHUNK;
 

@@ -22,7 +22,7 @@ def _load():
     lib.synth_fill_normal.restype = i
     lib.synth_copy_f32.argtypes = [vp, vp, i64, vp]
     lib.synth_copy_f32.restype = i
-    lib.synth_shape_stream.argtypes = [vp, i, i, i64, i64, i64, i, i, u32, vp, vp]
+    lib.synth_shape_stream.argtypes = [vp, i, i, i64, i64, i64, i, i, i, u32, vp, vp]
     lib.synth_shape_stream.restype = i
     return lib
 
@@ -125,7 +125,7 @@ class ShapePass:
     that every row covers what the kernel touches."""
 
     def __init__(self, rows, P: int, tile: int = 0, tile_stride: int = 0,
-                 xcd: bool = False, batch: int = 8):
+                 xcd: bool = False, batch: int = 8, threads: int = 64):
         rows = list(rows)
         rd = [r for r in rows if r.read]
         wo = [r for r in rows if not r.read]
@@ -136,8 +136,10 @@ class ShapePass:
             raise ValueError(f"P = {P} must be a non-negative multiple of 4")
         if batch not in (8, 16):
             raise ValueError("batch is 8 or 16")
-        if tile and (tile % 1024 or tile_stride < 0):
-            raise ValueError("tile is a multiple of 1024 coordinates")
+        if threads not in (64, 128, 256, 512, 1024):
+            raise ValueError("threads per block is a power of two in [64, 1024]")
+        if tile and (tile % (4 * threads) or tile_stride < 0):
+            raise ValueError("tile is a multiple of 4 * threads coordinates")
         dev = rows[0].tensor.device
         t = tile if tile else max(P, 1)
         for r in rows:
@@ -166,12 +168,13 @@ class ShapePass:
         self.keep_rows = rows  # the rows (and their tensors) outlive the pass
         self.n_rd, self.n_wo = len(rd), len(wo)
         self.P, self.tile, self.tile_stride = P, tile, tile_stride
-        self.xcd, self.batch = int(bool(xcd)), batch
+        self.xcd, self.batch, self.threads = int(bool(xcd)), batch, threads
         self.bytes = sum(r.nbytes(P) for r in rows)
 
     def launch(self, stream=None, sentinel: int = 0x9E3779B9) -> None:
         r = lib().synth_shape_stream(self.table.data_ptr(), self.n_rd, self.n_wo, self.P,
                                      self.tile, self.tile_stride, self.xcd, self.batch,
-                                     sentinel, self.sink.data_ptr(), _stream(stream))
+                                     self.threads, sentinel, self.sink.data_ptr(),
+                                     _stream(stream))
         if r != 0:
             raise RuntimeError(f"synth_shape_stream failed ({r})")

@@ -94,9 +94,9 @@ __global__ __launch_bounds__(kBlock) void copy_kernel(float* __restrict__ dst,
 // back to its write address unchanged (in place, the state keeps its exact
 // bits), then the XOR into every extra write-only row.  Read rows are taken
 // in batches of B, all loads of a batch before its stores, as the reconcile
-// takes its replica batches.  One block covers 1024 coordinates, as the
-// library's flat kernels do; blocks go round robin to the XCDs, or (xcd = 1)
-// in contiguous eighths like the copy kernel.
+// takes its replica batches.  A block of T threads covers 4T coordinates
+// (the library's kernels use T = 64, 256 coordinates); blocks go round robin
+// to the XCDs, or (xcd = 1) in contiguous eighths like the copy kernel.
 //
 // Row table in device memory, 64-bit words: for each read row r
 // [3r] address, [3r+1] write address (0 = read only), [3r+2] 1 for bf16
@@ -114,8 +114,10 @@ constexpr int kShapeMaxWriteOnly = 64;
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
+constexpr int kShapeMaxThreads = 1024;
+
 template <int B>
-__global__ __launch_bounds__(kBlock) void shape_kernel(const int64_t* __restrict__ rows, int n_rd,
+__global__ __launch_bounds__(kShapeMaxThreads) void shape_kernel(const int64_t* __restrict__ rows, int n_rd,
                                                        int n_wo, int64_t P, int64_t chunks,
                                                        int64_t tile, int64_t tile_stride,
                                                        int xcd, uint32_t sentinel,
@@ -126,7 +128,7 @@ __global__ __launch_bounds__(kBlock) void shape_kernel(const int64_t* __restrict
         c = (int64_t)(blockIdx.x % 8) * per + (int64_t)(blockIdx.x / 8);
     }
     if (c >= chunks) return;
-    const int64_t p0 = (c * kBlock + threadIdx.x) * kVec;
+    const int64_t p0 = (c * (int64_t)blockDim.x + threadIdx.x) * kVec;
     if (p0 + kVec > P) return;  // P is a multiple of kVec (checked on the host)
     const int64_t tile_off = (p0 / tile) * tile_stride;
     const int64_t in_tile = p0 % tile;
@@ -171,7 +173,7 @@ __global__ __launch_bounds__(kBlock) void shape_kernel(const int64_t* __restrict
         __builtin_nontemporal_store(u32x4{acc, acc, acc, acc},
                                     reinterpret_cast<u32x4*>(a + in_tile * 4));
     }
-    if (acc == sentinel) sink[threadIdx.x] = acc;
+    if (acc == sentinel) sink[threadIdx.x % 256] = acc;
 }
 
 int64_t blocks_for(int64_t n) { return (n + kBlock * kVec - 1) / (kBlock * kVec); }
@@ -229,25 +231,29 @@ int synth_copy_f32(float* dst, const float* src, int64_t n, void* stream) {
 // tensors it takes them from).  Returns 0, a HIP error code, or -1 for
 // invalid arguments.
 int synth_shape_stream(const int64_t* rows, int n_read, int n_write_only, int64_t P,
-                       int64_t tile, int64_t tile_stride, int xcd, int batch,
+                       int64_t tile, int64_t tile_stride, int xcd, int batch, int threads,
                        uint32_t sentinel, uint32_t* sink, void* stream) {
     if (rows == nullptr || sink == nullptr || n_read < 0 || n_read > kShapeMaxRead ||
         n_write_only < 0 || n_write_only > kShapeMaxWriteOnly || n_read + n_write_only < 1 ||
-        P < 0 || P % kVec != 0 || tile < 0 || tile_stride < 0 || (xcd != 0 && xcd != 1))
+        P < 0 || P % kVec != 0 || tile < 0 || tile_stride < 0 || (xcd != 0 && xcd != 1) ||
+        threads < 64 || threads > kShapeMaxThreads || (threads & (threads - 1)) != 0)
         return -1;
-    if (tile != 0 && tile % (kBlock * kVec) != 0) return -1;
+    const int64_t per_block = (int64_t)threads * kVec;
+    if (tile != 0 && tile % per_block != 0) return -1;
     if (P == 0) return 0;
-    const int64_t chunks = blocks_for(P);
+    const int64_t chunks = (P + per_block - 1) / per_block;
     if (chunks > 0x7FFFFFFF - 8) return -1;
     const int64_t t = tile == 0 ? P : tile;
     const int64_t blocks = xcd ? (chunks + 7) / 8 * 8 : chunks;
-    if (batch == 8)
-        return launch(shape_kernel<8>, blocks, stream, rows, n_read, n_write_only, P, chunks, t,
-                      tile == 0 ? (int64_t)0 : tile_stride, xcd, sentinel, sink);
-    if (batch == 16)
-        return launch(shape_kernel<16>, blocks, stream, rows, n_read, n_write_only, P, chunks, t,
-                      tile == 0 ? (int64_t)0 : tile_stride, xcd, sentinel, sink);
-    return -1;
+    const int64_t ts = tile == 0 ? (int64_t)0 : tile_stride;
+    void* argv[] = {&rows, &n_read, &n_write_only, &P, const_cast<int64_t*>(&chunks),
+                    const_cast<int64_t*>(&t), const_cast<int64_t*>(&ts), &xcd, &sentinel, &sink};
+    const void* k = batch == 8    ? reinterpret_cast<const void*>(shape_kernel<8>)
+                    : batch == 16 ? reinterpret_cast<const void*>(shape_kernel<16>)
+                                  : nullptr;
+    if (k == nullptr) return -1;
+    return (int)hipLaunchKernel(k, dim3((unsigned)blocks), dim3((unsigned)threads), argv, 0,
+                                static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

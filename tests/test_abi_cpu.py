@@ -376,7 +376,7 @@ def test_plan_build_validation():
     assert _plan_args(params=q) == E.CPDP_ERR_OVERLAP
     far = A + (1 << 44)
     assert _plan_args(anchor=[A + (1 << 30), far, far + (1 << 30)]) == E.CPDP_ERR_OVERLAP
-    # W x chunks blocks must fit one launch: 2 x 2^30 chunks of 1024 coordinates
+    # W x chunks blocks must fit one launch: 2 x 2^32 chunks of 256 coordinates
     # do not, and the running sum is checked before it could overflow
     assert _plan_args(n=2, numel=(1 << 40, 1 << 40)) == E.CPDP_ERR_INVALID_ARG
     assert _plan_args(W=1, n=3, numel=(1 << 57, 1 << 57, 1 << 57)) == E.CPDP_ERR_INVALID_ARG

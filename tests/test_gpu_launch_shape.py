@@ -1,6 +1,6 @@
-"""Results do not depend on the launch shape: the library built with 64-thread
-blocks (4x the blocks, one wavefront each) gives bitwise the same state as the
-default 256-thread build after every step.  The cross-replica sums run in a
+"""Results do not depend on the launch shape: the library built with 256-thread
+blocks (a quarter of the blocks, four wavefronts each) gives bitwise the same
+state as the default 64-thread build after every step.  The cross-replica sums run in a
 fixed order inside one thread, so the grid only decides which thread owns which
 four coordinates."""
 import ctypes
@@ -62,10 +62,10 @@ def _drive(lib, st, grads, s, h, opt, flags, method, stream):
 
 
 @pytest.mark.parametrize("case", CASES, ids=lambda c: f"W{c[0]}-P{c[1]}-{c[3]}-{c[4]}-f{c[5]}-{c[6]}")
-def test_block64_build_bitwise_equal(case):
+def test_block256_build_bitwise_equal(case):
     W, P, K, pdt, kind, flags, method = case
     log(f"[launch-shape] W={W} P={P} K={K} {pdt} {kind} flags={flags} {method}")
-    lib64 = cpdp.load_library(build.LIB_CPDP_BLOCK64)
+    lib256 = cpdp.load_library(build.LIB_CPDP_BLOCK256)
     stream = torch.cuda.Stream()
     h = Hyper.fp32(0.1, 0.9, 0.5, 1.0)
     opt = None
@@ -91,7 +91,7 @@ def test_block64_build_bitwise_equal(case):
             sdev.fill_grads(grads[0], P, 7, s, 1e-3, 0.01, stream=stream)
             grads[1].copy_(grads[0])
         _drive(cpdp.lib, states[0], grads[0], s, h, opt, flags, method, stream)
-        _drive(lib64, states[1], grads[1], s, h, opt, flags, method, stream)
+        _drive(lib256, states[1], grads[1], s, h, opt, flags, method, stream)
         stream.synchronize()
         for fam in ("params", "mom", "mom2", "slow_mom", "anchor"):
             a, b = getattr(states[0], fam), getattr(states[1], fam)

@@ -37,17 +37,18 @@ def test_shape_rows_in_place_keep_bits_and_pads():
         acc ^= np.bitwise_xor.reduce(_words_f32(g[r, :P]), axis=1)
     for r in range(2):
         acc ^= np.bitwise_xor.reduce(_words_bf16(b[r, :P]), axis=1)
-    for batch in (8, 16):
-        for xcd in (False, True):
-            wo.fill_(7.0)
-            ShapePass(rows, P, xcd=xcd, batch=batch).launch()
-            torch.cuda.synchronize()
-            assert torch.equal(g.view(torch.int32), g0.view(torch.int32))
-            assert torch.equal(b.view(torch.int16), b0.view(torch.int16))
-            for j in range(2):
-                got = _words_f32(wo[j, :P])
-                assert np.array_equal(got, np.repeat(acc[:, None], 4, axis=1)), (batch, xcd, j)
-                assert (wo[j, P:] == 7.0).all(), "write past P"
+    for batch, xcd, threads in ((8, False, 256), (16, False, 256), (8, True, 256),
+                                (16, True, 64), (8, False, 1024), (8, True, 128)):
+        wo.fill_(7.0)
+        ShapePass(rows, P, xcd=xcd, batch=batch, threads=threads).launch()
+        torch.cuda.synchronize()
+        assert torch.equal(g.view(torch.int32), g0.view(torch.int32))
+        assert torch.equal(b.view(torch.int16), b0.view(torch.int16))
+        for j in range(2):
+            got = _words_f32(wo[j, :P])
+            assert np.array_equal(got, np.repeat(acc[:, None], 4, axis=1)), \
+                (batch, xcd, threads, j)
+            assert (wo[j, P:] == 7.0).all(), "write past P"
 
 
 def test_shape_tile_major_addressing():
