@@ -24,6 +24,8 @@ def _load():
     lib.synth_copy_f32.restype = i
     lib.synth_shape_stream.argtypes = [vp, i, i, i64, i64, i64, i, i, i, u32, vp, vp]
     lib.synth_shape_stream.restype = i
+    lib.synth_shape_sync.argtypes = [vp, i, i, i, i, i, i, i64, u32, vp, vp]
+    lib.synth_shape_sync.restype = i
     return lib
 
 
@@ -178,3 +180,57 @@ class ShapePass:
                                      _stream(stream))
         if r != 0:
             raise RuntimeError(f"synth_shape_stream failed ({r})")
+
+
+SYNC_KINDS = {"cpdp": 0, "localsgd": 1, "ddp": 2}
+SYNC_ORDER_W = (4, 8, 16, 32)
+
+
+class ShapeSyncPass(ShapePass):
+    """The rows of a synchronisation step (as bench.sync_shape_rows lists
+    them) streamed in the library's own load and store order with no
+    arithmetic (shape_sync_kernel in synth/synth.hip).  The rows must follow
+    the kernel's fixed pattern for ``method`` with W replicas; anything else
+    is refused before a launch."""
+
+    def __init__(self, rows, P: int, method: str, adamw: bool, W: int):
+        rows = list(rows)
+        super().__init__(rows, P)
+        if method not in SYNC_KINDS:
+            raise ValueError(f"method {method!r}: one of {sorted(SYNC_KINDS)}")
+        if W not in SYNC_ORDER_W:
+            raise ValueError(f"W = {W}: the order kernel is built for W in {SYNC_ORDER_W}")
+        if P * 4 >= 2 ** 32:
+            raise ValueError(f"P = {P}: byte offsets must fit 32 bits")
+        R = 3 if adamw else 2
+        fam = ["m", "v", "t"] if adamw else ["m", "t"]
+        if method == "localsgd":
+            roles = [r for _ in range(W) for r in ["g"] + fam]
+        else:
+            roles = ["g"] * W + fam * W + (["u", "a"] if method == "cpdp" else [])
+        rd = [r for r in rows if r.read]
+        wo = [r for r in rows if not r.read]
+        if len(rd) != len(roles) or len(wo) != (1 if method == "localsgd" else 0):
+            raise ValueError(f"{len(rd)} read and {len(wo)} write-only rows do not follow the "
+                             f"{method} pattern at W = {W} ({len(roles)} read rows)")
+        narrow = {}
+        for role, r in zip(roles, rd):
+            if r.write != (role != "g"):
+                raise ValueError(f"row {role}: written back = {r.write}, the pattern says "
+                                 f"{role != 'g'}")
+            n = r.esize == 2
+            if narrow.setdefault(role, n) != n:
+                raise ValueError(f"the {role} rows mix bf16 and fp32")
+        if narrow.get("v", False) or narrow.get("u", False) or narrow.get("a", False):
+            raise ValueError("second-moment, SlowMo and anchor rows are fp32")
+        if (narrow["g"] or narrow["m"]) and (method != "cpdp" or adamw):
+            raise ValueError("bf16 gradient or momentum rows only on the momentum-SGD reconcile")
+        self.kind, self.adam, self.W, self.R = SYNC_KINDS[method], int(bool(adamw)), W, R
+        self.np, self.ng, self.nm = int(narrow["t"]), int(narrow["g"]), int(narrow["m"])
+
+    def launch(self, stream=None, sentinel: int = 0x9E3779B9) -> None:
+        r = lib().synth_shape_sync(self.table.data_ptr(), self.kind, self.adam, self.W, self.np,
+                                   self.ng, self.nm, self.P, sentinel, self.sink.data_ptr(),
+                                   _stream(stream))
+        if r != 0:
+            raise RuntimeError(f"synth_shape_sync failed ({r})")

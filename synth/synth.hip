@@ -9,6 +9,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace {
 
 constexpr int kBlock = 256;
@@ -176,6 +178,177 @@ __global__ __launch_bounds__(kShapeMaxThreads) void shape_kernel(const int64_t* 
     if (acc == sentinel) sink[threadIdx.x % 256] = acc;
 }
 
+// ---- traffic shape in the synchronisation steps' own order -------------------
+//
+// The same rows as the shape kernel above, loaded and stored in the order the
+// library's synchronisation kernels issue them, with no arithmetic: one
+// 64-thread block per 256 coordinates, replica batches of 4, and
+//   S = 0, the reconcile: the W gradient rows in batches of 4; the anchor and
+//          the SlowMo row; per batch the momentum (and second-moment) rows
+//          and the parameter rows of 4 replicas, then their momentum stores;
+//          the SlowMo and anchor stores; the W parameter stores last (they
+//          carry the broadcast, which exists only after the parameter mean);
+//   S = 1, the LocalSGD sync: per batch each replica's gradient, momentum
+//          (second-moment) and parameter rows, then the momentum stores;
+//          the write-only anchor; the W parameter stores last;
+//   S = 2, the DDP step: the W gradient rows in batches of 4; per batch the
+//          momentum (second-moment) and parameter rows, then per replica its
+//          momentum, (second-moment) and parameter stores.
+// Every store writes back the bits its row held (the parameter rows are
+// kept in registers until the end), the write-only anchor gets the XOR.
+// The table is the shape kernel's, in a fixed order (n = W gradient rows,
+// R = 2, or 3 with second moments):
+//   S = 0  g_0..g_{W-1}, then (m_i, [v_i], theta_i) for i < W, then u, anchor
+//   S = 1  (g_i, m_i, [v_i], theta_i) for i < W; write-only: the anchor
+//   S = 2  g_0..g_{W-1}, then (m_i, [v_i], theta_i) for i < W
+// NP: the parameter rows are bf16 (held as 2 words).
+
+// Row access of the order kernel: a scalar base (from the table) plus a 32-bit
+// byte offset, the form the library's loads take; N = bf16 row.
+template <bool N>
+__device__ __forceinline__ u32x4 shape_ld(const int64_t* __restrict__ rows, int r, uint32_t p0) {
+    const char* a = reinterpret_cast<const char*>(rows[3 * r]);
+    if constexpr (N) {
+        const u32x2 v = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(a + p0 * 2u));
+        return u32x4{v.x, v.y, 0u, 0u};
+    } else {
+        return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(a + p0 * 4u));
+    }
+}
+
+template <bool N>
+__device__ __forceinline__ void shape_st(const int64_t* __restrict__ rows, int r, uint32_t p0,
+                                         u32x4 x) {
+    char* a = reinterpret_cast<char*>(rows[3 * r + 1]);
+    if constexpr (N)
+        __builtin_nontemporal_store(u32x2{x.x, x.y}, reinterpret_cast<u32x2*>(a + p0 * 2u));
+    else
+        __builtin_nontemporal_store(x, reinterpret_cast<u32x4*>(a + p0 * 4u));
+}
+
+__device__ __forceinline__ uint32_t fold(u32x4 x) { return x.x ^ x.y ^ x.z ^ x.w; }
+
+// NP, NG, NM: parameter, gradient, momentum rows are bf16 (the second-moment,
+// SlowMo and anchor rows are fp32)
+template <int S, bool ADAM, int W, bool NP, bool NG, bool NM>
+__global__ __launch_bounds__(64) void shape_sync_kernel(const int64_t* __restrict__ rows,
+                                                        int64_t P, uint32_t sentinel,
+                                                        uint32_t* __restrict__ sink) {
+    constexpr int C = W < 4 ? W : 4;
+    constexpr int R = ADAM ? 3 : 2;
+    constexpr int G = S == 1 ? 1 : 0;  // LocalSGD: gradient row inside the replica's rows
+    // P * 4 < 2^32 (checked on the host), so coordinates and byte offsets fit 32 bits
+    const uint32_t p0 = (blockIdx.x * 64u + threadIdx.x) * kVec;
+    if ((int64_t)p0 + kVec > P) return;  // P is a multiple of kVec (checked on the host)
+    auto row_g = [](int i) { return S == 1 ? i * (R + 1) : i; };
+    auto row_m = [](int i) { return S == 1 ? i * (R + 1) + 1 : W + i * R; };
+    auto row_t = [](int i) { return S == 1 ? i * (R + 1) + R : W + i * R + R - 1; };
+    uint32_t acc = 0;
+    if constexpr (S != 1) {
+#pragma unroll
+        for (int i0 = 0; i0 < W; i0 += C) {
+            u32x4 g[C];
+#pragma unroll
+            for (int c = 0; c < C; ++c) g[c] = shape_ld<NG>(rows, row_g(i0 + c), p0);
+#pragma unroll
+            for (int c = 0; c < C; ++c) acc ^= fold(g[c]);
+        }
+    }
+    u32x4 a{0u, 0u, 0u, 0u}, u{0u, 0u, 0u, 0u};
+    if constexpr (S == 0) {
+        a = shape_ld<false>(rows, W + W * R + 1, p0);
+        u = shape_ld<false>(rows, W + W * R, p0);
+        acc ^= fold(a) ^ fold(u);
+    }
+    using PT = typename std::conditional<NP, u32x2, u32x4>::type;
+    PT late[S == 2 ? 1 : W];
+#pragma unroll
+    for (int i0 = 0; i0 < W; i0 += C) {
+        u32x4 g[C], m[C], v[C], th[C];
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            if constexpr (G) g[c] = shape_ld<NG>(rows, row_g(i0 + c), p0);
+            m[c] = shape_ld<NM>(rows, row_m(i0 + c), p0);
+            if constexpr (ADAM) v[c] = shape_ld<false>(rows, row_m(i0 + c) + 1, p0);
+            th[c] = shape_ld<NP>(rows, row_t(i0 + c), p0);
+        }
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            if constexpr (G) acc ^= fold(g[c]);
+            acc ^= fold(m[c]) ^ fold(th[c]);
+            if constexpr (ADAM) acc ^= fold(v[c]);
+        }
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            shape_st<NM>(rows, row_m(i0 + c), p0, m[c]);
+            if constexpr (ADAM) shape_st<false>(rows, row_m(i0 + c) + 1, p0, v[c]);
+            if constexpr (S == 2) {
+                shape_st<NP>(rows, row_t(i0 + c), p0, th[c]);
+            } else if constexpr (NP) {
+                late[i0 + c] = u32x2{th[c].x, th[c].y};
+            } else {
+                late[i0 + c] = th[c];
+            }
+        }
+    }
+    if constexpr (S == 0) {
+        shape_st<false>(rows, W + W * R, p0, u);
+        shape_st<false>(rows, W + W * R + 1, p0, a);
+    }
+    if constexpr (S == 1) {
+        char* an = reinterpret_cast<char*>(rows[3 * W * (R + 1)]);
+        __builtin_nontemporal_store(u32x4{acc, acc, acc, acc},
+                                    reinterpret_cast<u32x4*>(an + p0 * 4u));
+    }
+    if constexpr (S != 2) {
+#pragma unroll
+        for (int i = 0; i < W; ++i) {
+            if constexpr (NP)
+                shape_st<true>(rows, row_t(i), p0, u32x4{late[i].x, late[i].y, 0u, 0u});
+            else
+                shape_st<false>(rows, row_t(i), p0, late[i]);
+        }
+    }
+    if (acc == sentinel) sink[threadIdx.x] = acc;
+}
+
+template <int S, bool ADAM, bool NP, bool NG, bool NM>
+const void* shape_sync_for_w(int W) {
+    switch (W) {
+        case 4: return reinterpret_cast<const void*>(shape_sync_kernel<S, ADAM, 4, NP, NG, NM>);
+        case 8: return reinterpret_cast<const void*>(shape_sync_kernel<S, ADAM, 8, NP, NG, NM>);
+        case 16: return reinterpret_cast<const void*>(shape_sync_kernel<S, ADAM, 16, NP, NG, NM>);
+        case 32: return reinterpret_cast<const void*>(shape_sync_kernel<S, ADAM, 32, NP, NG, NM>);
+        default: return nullptr;
+    }
+}
+
+// bf16 gradient and momentum rows exist on the momentum-SGD reconcile only,
+// as in the library
+template <int S>
+const void* shape_sync_for(bool adam, bool np, bool ng, bool nm, int W) {
+    if (adam && (ng || nm)) return nullptr;
+    if (adam) return np ? shape_sync_for_w<S, true, true, false, false>(W)
+                        : shape_sync_for_w<S, true, false, false, false>(W);
+    if constexpr (S != 0) {
+        if (ng || nm) return nullptr;
+        return np ? shape_sync_for_w<S, false, true, false, false>(W)
+                  : shape_sync_for_w<S, false, false, false, false>(W);
+    } else {
+        const int k = (np ? 4 : 0) | (ng ? 2 : 0) | (nm ? 1 : 0);
+        switch (k) {
+            case 0: return shape_sync_for_w<S, false, false, false, false>(W);
+            case 1: return shape_sync_for_w<S, false, false, false, true>(W);
+            case 2: return shape_sync_for_w<S, false, false, true, false>(W);
+            case 3: return shape_sync_for_w<S, false, false, true, true>(W);
+            case 4: return shape_sync_for_w<S, false, true, false, false>(W);
+            case 5: return shape_sync_for_w<S, false, true, false, true>(W);
+            case 6: return shape_sync_for_w<S, false, true, true, false>(W);
+            default: return shape_sync_for_w<S, false, true, true, true>(W);
+        }
+    }
+}
+
 int64_t blocks_for(int64_t n) { return (n + kBlock * kVec - 1) / (kBlock * kVec); }
 
 template <class T>
@@ -253,6 +426,34 @@ int synth_shape_stream(const int64_t* rows, int n_read, int n_write_only, int64_
                                   : nullptr;
     if (k == nullptr) return -1;
     return (int)hipLaunchKernel(k, dim3((unsigned)blocks), dim3((unsigned)threads), argv, 0,
+                                static_cast<hipStream_t>(stream));
+}
+
+// One pass of the traffic shape of a synchronisation step in the library's
+// own load and store order (see shape_sync_kernel): sync 0 = the reconcile,
+// 1 = the LocalSGD sync, 2 = the DDP step; adam = second-moment rows present;
+// W in {4, 8, 16, 32}; param_bf16, grad_bf16, mom_bf16 = those rows are bf16
+// (gradient and momentum rows only on the reconcile without second moments).
+// The table `rows` follows the layout stated at shape_sync_kernel, its bf16
+// flags unread; the caller guarantees that every address covers coordinates
+// [0, P).  Returns 0, a HIP error code, or -1 for invalid arguments.
+int synth_shape_sync(const int64_t* rows, int sync, int adam, int W, int param_bf16,
+                     int grad_bf16, int mom_bf16, int64_t P, uint32_t sentinel, uint32_t* sink,
+                     void* stream) {
+    if (rows == nullptr || sink == nullptr || sync < 0 || sync > 2 || (adam != 0 && adam != 1) ||
+        (param_bf16 != 0 && param_bf16 != 1) || (grad_bf16 != 0 && grad_bf16 != 1) ||
+        (mom_bf16 != 0 && mom_bf16 != 1) || P < 0 || P % kVec != 0 ||
+        P > (int64_t)0x3FFFFFFF)
+        return -1;
+    const bool a = adam, np = param_bf16, ng = grad_bf16, nm = mom_bf16;
+    const void* k = sync == 0   ? shape_sync_for<0>(a, np, ng, nm, W)
+                    : sync == 1 ? shape_sync_for<1>(a, np, ng, nm, W)
+                                : shape_sync_for<2>(a, np, ng, nm, W);
+    if (k == nullptr) return -1;
+    if (P == 0) return 0;
+    const int64_t blocks = (P + 64 * kVec - 1) / (64 * kVec);
+    void* argv[] = {&rows, &P, &sentinel, &sink};
+    return (int)hipLaunchKernel(k, dim3((unsigned)blocks), dim3(64), argv, 0,
                                 static_cast<hipStream_t>(stream));
 }
 

@@ -91,3 +91,79 @@ def test_shape_pass_rejects_rows_that_do_not_fit():
     with pytest.raises(ValueError):           # tile layout past the buffer
         ShapePass([ShapeRow(x)], 1024 + 4, tile=1024, tile_stride=4096)
     ShapePass([ShapeRow(x, 4)], 996)          # exactly fits
+
+
+def _fill_state(st, grads, seed):
+    """Random bits in every row the synchronisation steps touch (finite
+    values; the order kernel never looks at them) and a canary in the pads."""
+    gen = torch.Generator(device="cpu").manual_seed(seed)
+    for t in [st.params, st.mom, st.slow_mom, st.anchor, grads] + \
+             ([st.mom2] if st.mom2 is not None else []):
+        t.copy_(torch.randn(t.shape, generator=gen).to(t.dtype))
+        if t.dim() == 2:
+            t[:, st.P:] = 3.0
+
+
+@pytest.mark.parametrize("method,adamw,W,pdt,gdt,mdt", [
+    ("cpdp", False, 8, "f32", "f32", "f32"),
+    ("cpdp", False, 4, "bf16", "f32", "f32"),
+    ("cpdp", False, 8, "bf16", "bf16", "bf16"),
+    ("cpdp", False, 16, "f32", "bf16", "f32"),
+    ("cpdp", True, 8, "f32", "f32", "f32"),
+    ("localsgd", False, 8, "f32", "f32", "f32"),
+    ("localsgd", True, 4, "bf16", "f32", "f32"),
+    ("ddp", False, 8, "f32", "f32", "f32"),
+    ("ddp", True, 16, "bf16", "f32", "f32"),
+])
+def test_shape_sync_order_keeps_state_bits(method, adamw, W, pdt, gdt, mdt):
+    """The library-order shape pass over a live state's rows: every row it
+    writes back keeps its bits, the pads are untouched, and LocalSGD's
+    write-only anchor gets the XOR of every row read."""
+    import bench
+    from paper_2607_21224_amd.state import CpdpState
+    from synth.device import ShapeSyncPass
+    P = 256 * 20 + 12  # twenty full 256-coordinate blocks and a partly used last one
+    st = CpdpState(W, P, K=2, param_dt=pdt, grad_dt=gdt, mom_dt=mdt, adamw=adamw)
+    grads = torch.empty((W, st.ld), device="cuda",
+                        dtype=torch.bfloat16 if gdt == "bf16" else torch.float32)
+    _fill_state(st, grads, seed=W * 7 + len(method))
+    rows = bench.sync_shape_rows(st, grads, method, adamw)
+    before = [r.tensor.clone() for r in rows]
+    ShapeSyncPass(rows, P, method, adamw, W).launch()
+    torch.cuda.synchronize()
+    acc = np.zeros(P // 4, dtype=np.uint32)
+    for r, b in zip(rows, before):
+        if not r.read:
+            continue
+        view = torch.int16 if r.esize == 2 else torch.int32
+        assert torch.equal(r.tensor.view(view), b.view(view)), (method, r.offset)
+        seg = r.tensor.view(-1)[r.offset:r.offset + P]
+        words = _words_bf16(seg) if r.esize == 2 else _words_f32(seg)
+        acc ^= np.bitwise_xor.reduce(words, axis=1)
+    if method == "localsgd":
+        got = _words_f32(st.anchor[:P])
+        assert np.array_equal(got, np.repeat(acc[:, None], 4, axis=1))
+
+
+def test_shape_sync_pass_refuses_other_patterns():
+    import bench
+    from paper_2607_21224_amd.state import CpdpState
+    from synth.device import ShapeRow, ShapeSyncPass
+    st = CpdpState(8, 1024, K=2)
+    grads = torch.zeros((8, st.ld), device="cuda")
+    rows = bench.sync_shape_rows(st, grads, "cpdp", False)
+    ShapeSyncPass(rows, 1024, "cpdp", False, 8)
+    with pytest.raises(ValueError):
+        ShapeSyncPass(rows, 1024, "ddp", False, 8)        # two rows too many
+    with pytest.raises(ValueError):
+        ShapeSyncPass(rows[::-1], 1024, "cpdp", False, 8)  # order
+    with pytest.raises(ValueError):
+        ShapeSyncPass(rows, 1024, "cpdp", True, 8)        # no second moments
+    swapped = list(rows)
+    swapped[0] = ShapeRow(st.mom, 0, write=True)          # a written row where g is read only
+    with pytest.raises(ValueError):
+        ShapeSyncPass(swapped, 1024, "cpdp", False, 8)
+    st2 = CpdpState(2, 1024, K=2)
+    with pytest.raises(ValueError):                       # W without an order kernel
+        ShapeSyncPass(bench.sync_shape_rows(st2, grads[:2], "cpdp", False), 1024,
+                      "cpdp", False, 2)
