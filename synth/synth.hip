@@ -116,6 +116,20 @@ constexpr int kShapeMaxWriteOnly = 64;
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
+// The row addresses are integers from a table; these casts put the accesses in
+// the global address space, so that they compile to global loads and stores
+// like the library's (a generic pointer gives flat accesses, which also count
+// against the LDS counter).
+#define SHAPE_GLOBAL __attribute__((address_space(1)))
+template <class V>
+__device__ __forceinline__ V gload(const char* p) {
+    return __builtin_nontemporal_load((const SHAPE_GLOBAL V*)p);
+}
+template <class V>
+__device__ __forceinline__ void gstore(V v, char* p) {
+    __builtin_nontemporal_store(v, (SHAPE_GLOBAL V*)p);
+}
+
 constexpr int kShapeMaxThreads = 1024;
 
 template <int B>
@@ -144,13 +158,11 @@ __global__ __launch_bounds__(kShapeMaxThreads) void shape_kernel(const int64_t* 
             if (r < n_rd) {
                 const char* a = reinterpret_cast<const char*>(rows[3 * r]) + tile_off;
                 if (rows[3 * r + 2]) {
-                    const u32x2 v = __builtin_nontemporal_load(
-                        reinterpret_cast<const u32x2*>(a + in_tile * 2));
+                    const u32x2 v = gload<u32x2>(a + in_tile * 2);
                     x[b].x = v.x;
                     x[b].y = v.y;
                 } else {
-                    x[b] = __builtin_nontemporal_load(
-                        reinterpret_cast<const u32x4*>(a + in_tile * 4));
+                    x[b] = gload<u32x4>(a + in_tile * 4);
                 }
             }
         }
@@ -162,18 +174,16 @@ __global__ __launch_bounds__(kShapeMaxThreads) void shape_kernel(const int64_t* 
             if (r < n_rd && rows[3 * r + 1] != 0) {
                 char* a = reinterpret_cast<char*>(rows[3 * r + 1]) + tile_off;
                 if (rows[3 * r + 2])
-                    __builtin_nontemporal_store(u32x2{x[b].x, x[b].y},
-                                                reinterpret_cast<u32x2*>(a + in_tile * 2));
+                    gstore(u32x2{x[b].x, x[b].y}, a + in_tile * 2);
                 else
-                    __builtin_nontemporal_store(x[b], reinterpret_cast<u32x4*>(a + in_tile * 4));
+                    gstore(x[b], a + in_tile * 4);
             }
         }
     }
     const int64_t* wo = rows + 3 * (int64_t)n_rd;
     for (int j = 0; j < n_wo; ++j) {
         char* a = reinterpret_cast<char*>(wo[j]) + tile_off;
-        __builtin_nontemporal_store(u32x4{acc, acc, acc, acc},
-                                    reinterpret_cast<u32x4*>(a + in_tile * 4));
+        gstore(u32x4{acc, acc, acc, acc}, a + in_tile * 4);
     }
     if (acc == sentinel) sink[threadIdx.x % 256] = acc;
 }
@@ -209,10 +219,10 @@ template <bool N>
 __device__ __forceinline__ u32x4 shape_ld(const int64_t* __restrict__ rows, int r, uint32_t p0) {
     const char* a = reinterpret_cast<const char*>(rows[3 * r]);
     if constexpr (N) {
-        const u32x2 v = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(a + p0 * 2u));
+        const u32x2 v = gload<u32x2>(a + p0 * 2u);
         return u32x4{v.x, v.y, 0u, 0u};
     } else {
-        return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(a + p0 * 4u));
+        return gload<u32x4>(a + p0 * 4u);
     }
 }
 
@@ -221,9 +231,9 @@ __device__ __forceinline__ void shape_st(const int64_t* __restrict__ rows, int r
                                          u32x4 x) {
     char* a = reinterpret_cast<char*>(rows[3 * r + 1]);
     if constexpr (N)
-        __builtin_nontemporal_store(u32x2{x.x, x.y}, reinterpret_cast<u32x2*>(a + p0 * 2u));
+        gstore(u32x2{x.x, x.y}, a + p0 * 2u);
     else
-        __builtin_nontemporal_store(x, reinterpret_cast<u32x4*>(a + p0 * 4u));
+        gstore(x, a + p0 * 4u);
 }
 
 __device__ __forceinline__ uint32_t fold(u32x4 x) { return x.x ^ x.y ^ x.z ^ x.w; }
@@ -297,8 +307,7 @@ __global__ __launch_bounds__(64) void shape_sync_kernel(const int64_t* __restric
     }
     if constexpr (S == 1) {
         char* an = reinterpret_cast<char*>(rows[3 * W * (R + 1)]);
-        __builtin_nontemporal_store(u32x4{acc, acc, acc, acc},
-                                    reinterpret_cast<u32x4*>(an + p0 * 4u));
+        gstore(u32x4{acc, acc, acc, acc}, an + p0 * 4u);
     }
     if constexpr (S != 2) {
 #pragma unroll
