@@ -37,9 +37,10 @@ namespace {
 
 // One wavefront per block.  On MI355X 64-thread blocks ran the reconcile
 // 2.6-3.1 % and the local step 1-3.7 % faster than 256-thread blocks on the
-// fp32 ResNet-50 / ViT-S sized states (level on the 32-replica bf16 state):
-// single-wave blocks refill a CU's wave slots one at a time.  Results do not
-// depend on it (every thread owns its 4 coordinates).
+// fp32 ResNet-50 / ViT-S sized states (level on the 32-replica bf16 state);
+// a kernel streaming the reconcile's rows with no arithmetic gains as much,
+// so the difference is in how the memory system sees the blocks, not in the
+// code.  Results do not depend on it (every thread owns its 4 coordinates).
 #ifndef CPDP_BLOCK
 #define CPDP_BLOCK 64
 #endif
