@@ -205,10 +205,11 @@ def cpu_baseline(w, budget_s: float = 10.0, n_coords: int = 1 << 18,
 
 def sync_shape_rows(st, grads, method: str, adamw: bool):
     """The rows the synchronisation kernel of ``method`` reads and writes on
-    the flat state, in its order (gradient rows, then each replica's
-    optimizer state and parameters, then SlowMo state and anchor), for the
-    traffic-shape kernel.  Rows the kernel updates are written back in place;
-    LocalSGD's anchor is written only."""
+    the flat state, for the traffic-shape kernels, in the fixed table layout
+    both take (gradient rows, then each replica's optimizer state and
+    parameters, then the SlowMo state and anchor; LocalSGD: each replica's
+    gradient, optimizer state and parameters).  Rows the kernel updates are
+    written back in place; LocalSGD's anchor is written only."""
     from synth.device import ShapeRow
     W, ld = st.W, st.ld
     rows = [] if method == "localsgd" else [ShapeRow(grads, i * ld) for i in range(W)]
@@ -544,11 +545,11 @@ def main() -> int:
     copy_gbps = 2 * 4 * n_copy * reps / (c0.elapsed_time(c1) * 1e-3) / 1e9
     del csrc, cdst
 
-    # traffic-shape ceiling: the synchronisation kernel's exact rows streamed by
-    # a kernel with no arithmetic (in place, the state keeps its bits)
-    # Two orders of the same loads and stores: each batch of 8 rows written
-    # back right after it is read, and the library's own order; the ceiling is
-    # the faster, each timed as the best of three batches of launches.
+    # traffic-shape ceiling: the synchronisation kernel's exact rows streamed
+    # with no arithmetic (in place, the state keeps its bits), in two orders:
+    # each batch of 8 rows written back right after it is read, and the
+    # library's own order.  The ceiling is the faster, each order timed as the
+    # best of three batches of launches.
     shape = None
     if multi is None:
         from synth.device import SYNC_ORDER_W, ShapePass, ShapeSyncPass
