@@ -264,41 +264,22 @@ __device__ __forceinline__ int64_t plan_tensor(const PlanView& v, int64_t n, int
     return lo;
 }
 
-// ---- XCD-contiguous order of the local step's blocks --------------------------
+// ---- block order of the local step ---------------------------------------------
 //
 // The local step's blocks are the cells (replica row, column of kBlock * kVec
-// coordinates) of a W x columns grid.  The hardware hands workgroup b of a
-// launch to XCD b % kXcds (round robin), and every XCD has its own L2, so in
-// plain replica-major order each XCD would stream every eighth column.  Block
-// b instead takes cell (b % kXcds) * per + b / kXcds of the replica-major order
-// (per = ceil(cells / kXcds)): each XCD streams one contiguous eighth of the
-// state.  The grid is kXcds * per blocks; the few past the last cell exit.
-// The order pays off for the momentum-SGD updates (3 read and 2 write rows
-// per replica); AdamW's local step (4 read and 3 write rows) measured level
-// or about 1 % slower with it and keeps the plain order,
-// as do the fused synchronisation steps, where every block already reads all
-// rows at its coordinates and the remapping was slower.
-constexpr int kXcds = 8;
-
-template <Opt O>
-constexpr bool kXcdOrder = O != Opt::ADAMW;
+// coordinates) of a W x columns grid, taken in plain replica-major order: the
+// hardware hands workgroup b of a launch to XCD b % 8, so each XCD streams
+// every eighth column.  Dealing the blocks to the XCDs in contiguous eighths
+// of the state instead was 4-5 % faster for the momentum-SGD update with
+// 256-thread blocks, but 0.6-2.9 % slower with the 64-thread blocks used
+// here (and level for AdamW), so the plain order stays.
 
 // blocks of a local-step launch over `cells` cells
-template <Opt O>
-inline int64_t local_grid(int64_t cells) {
-    return kXcdOrder<O> ? (cells + kXcds - 1) / kXcds * kXcds : cells;
-}
+inline int64_t local_grid(int64_t cells) { return cells; }
 
-// the cell of this block, or -1 for a padding block
-template <Opt O>
+// the cell of this block, or -1 for a block past the last cell
 __device__ __forceinline__ int64_t local_cell(int64_t cells) {
-    if constexpr (kXcdOrder<O>) {
-        const int64_t per = (cells + kXcds - 1) / kXcds;
-        const int64_t c = (int64_t)(blockIdx.x % kXcds) * per + (int64_t)(blockIdx.x / kXcds);
-        return c < cells ? c : -1;
-    } else {
-        return (int64_t)blockIdx.x < cells ? (int64_t)blockIdx.x : -1;
-    }
+    return (int64_t)blockIdx.x < cells ? (int64_t)blockIdx.x : -1;
 }
 
 // ---- local step: one replica row per block, 4 coordinates per thread -------

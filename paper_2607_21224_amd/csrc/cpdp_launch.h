@@ -147,8 +147,7 @@ int64_t coords_per_block();
 // Synchronous host-to-device copy of a plan table; returns the HIP status.
 int upload_plan(void* dev, const int64_t* host, int64_t words);
 
-// Most blocks a launch may cover before its grid is padded to a multiple of
-// the 8 XCDs (the padded grid stays within 2^31 - 1 blocks).
+// Most blocks a launch may cover (a grid holds at most 2^31 - 1).
 constexpr int64_t kMaxBlocks = 0x7FFFFFFF - 8;
 
 // True when a launch over P coordinates (rows = W for the row-parallel local

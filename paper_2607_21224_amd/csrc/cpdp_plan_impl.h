@@ -16,7 +16,7 @@ __global__ __launch_bounds__(kBlock) void local_step_plan_kernel(Src src,
                                                                  const int64_t* __restrict__ plan,
                                                                  int W, int n,
                                                                  int64_t total_chunks) {
-    const int64_t cell = local_cell<O>(total_chunks * W);
+    const int64_t cell = local_cell(total_chunks * W);
     if (cell < 0) return;
     const PlanView v = plan_view(plan, W, n);
     const int64_t row = cell / total_chunks;
@@ -60,7 +60,7 @@ __global__ __launch_bounds__(kBlock) void sync_plan_kernel(Src src,
 template <Opt O, class Src>
 int local_plan_o(Param pt, Src src, const int64_t* plan, int W, int n, int64_t total_chunks,
                  void* stream) {
-    const int64_t blocks = local_grid<O>(total_chunks * W);
+    const int64_t blocks = local_grid(total_chunks * W);
     return pt == Param::BF16 ? launch(local_step_plan_kernel<O, ParamBF16, Src>, blocks, stream,
                                       src, plan, W, n, total_chunks)
                              : launch(local_step_plan_kernel<O, ParamF32, Src>, blocks, stream,

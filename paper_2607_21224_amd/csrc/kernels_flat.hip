@@ -44,7 +44,7 @@ __global__ __launch_bounds__(kBlock) void local_step_kernel(
     OptParams o, typename PS::T* __restrict__ params, typename MS::T* __restrict__ mom,
     float* __restrict__ mom2, const typename GS::T* __restrict__ grads, int64_t ld, int64_t P,
     int64_t blocks_per_row, int64_t cells) {
-    const int64_t cell = local_cell<O>(cells);
+    const int64_t cell = local_cell(cells);
     if (cell < 0) return;
     const int64_t row = cell / blocks_per_row;
     const int64_t col = cell - row * blocks_per_row;
@@ -68,7 +68,7 @@ int local_step_t(const OptParams& o, void* params, void* mom, float* mom2, const
                  int W, int64_t P, int64_t ld, void* stream) {
     using T = typename PS::T;
     const int64_t bpr = blocks_for(P);
-    return launch(local_step_kernel<O, PS, GS, MS>, local_grid<O>(bpr * W), stream, o,
+    return launch(local_step_kernel<O, PS, GS, MS>, local_grid(bpr * W), stream, o,
                   static_cast<T*>(params), static_cast<typename MS::T*>(mom), mom2,
                   static_cast<const typename GS::T*>(grads), ld, P, bpr, bpr * W);
 }

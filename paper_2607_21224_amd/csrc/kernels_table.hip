@@ -10,7 +10,7 @@ __global__ __launch_bounds__(kBlock) void local_step_table_kernel(
     const int64_t* __restrict__ table, typename PS::T* __restrict__ params,
     float* __restrict__ mom, float* __restrict__ mom2, const float* __restrict__ grads,
     int64_t ld, int64_t P, int64_t blocks_per_row, int64_t cells) {
-    const int64_t cell = local_cell<O>(cells);
+    const int64_t cell = local_cell(cells);
     if (cell < 0) return;
     const int64_t row = cell / blocks_per_row;
     const int64_t col = cell - row * blocks_per_row;
@@ -60,10 +60,10 @@ int local_table_o(Param pt, const int64_t* table, void* params, float* mom, floa
                   const float* grads, int W, int64_t P, int64_t ld, void* stream) {
     const int64_t bpr = blocks_for(P);
     if (pt == Param::BF16)
-        return launch(local_step_table_kernel<O, ParamBF16>, local_grid<O>(bpr * W), stream,
+        return launch(local_step_table_kernel<O, ParamBF16>, local_grid(bpr * W), stream,
                       table, static_cast<uint16_t*>(params), mom, mom2, grads, ld, P, bpr,
                       bpr * W);
-    return launch(local_step_table_kernel<O, ParamF32>, local_grid<O>(bpr * W), stream, table,
+    return launch(local_step_table_kernel<O, ParamF32>, local_grid(bpr * W), stream, table,
                   static_cast<float*>(params), mom, mom2, grads, ld, P, bpr, bpr * W);
 }
 
