@@ -36,7 +36,7 @@ def test_theta0_and_bf16_rounding():
 @pytest.mark.parametrize("n", [1, 3, 4, 5, 1023, 1024, 1025, 4097, 8 * 1024 + 4, (1 << 20) + 3])
 def test_reference_copy_ragged_sizes(n):
     """The bandwidth-reference copy moves exactly src[:n] into dst[:n] (every
-    XCD eighth and the ragged tail) and leaves the bytes after n untouched."""
+    block and the ragged tail) and leaves the bytes after n untouched."""
     src = torch.arange(n + 64, dtype=torch.float32, device="cuda") + 0.5
     dst = torch.full((n + 64,), -7.0, dtype=torch.float32, device="cuda")
     sdev.copy_f32(dst, src, n)
