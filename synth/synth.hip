@@ -97,7 +97,7 @@ __global__ __launch_bounds__(kCopyBlock) void copy_kernel(float* __restrict__ ds
 // in batches of B, all loads of a batch before its stores, as the reconcile
 // takes its replica batches.  A block of T threads covers 4T coordinates
 // (the library's kernels use T = 64, 256 coordinates); blocks go round robin
-// to the XCDs, or (xcd = 1) in contiguous eighths like the copy kernel.
+// to the XCDs, or (xcd = 1) in contiguous eighths of the coordinates.
 //
 // Row table in device memory, 64-bit words: for each read row r
 // [3r] address, [3r+1] write address (0 = read only), [3r+2] 1 for bf16
