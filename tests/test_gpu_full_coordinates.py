@@ -6,6 +6,9 @@ benchmark's launch configuration (longer runs on request, below):
   r50_200  ResNet-50/TinyImageNet-sized, W=16, P=23,917,832, K=8, gradients
            with 1 % outliers x100
   stress   W=32 bf16 replicas, P=10^8, fp32 gradients, momentum, u, anchor, K=4
+and vit_s once more with AdamW, the optimizer the paper trains ViT-S with
+(Table 3: lr 5e-4, betas 0.9 / 0.999, eps 1e-8, decoupled weight decay 0.05),
+second moments included.
 
 Inputs come from the seeded generator: on the device for the HIP path, copied
 to the host for the oracle (the generator is the one module both sides share;
@@ -46,10 +49,17 @@ WORKERS = 12
 
 WHOLE_RUN = os.environ.get("CPDP_FULL_PERIODS", "1") == "all"
 SEEDS = [int(x) for x in os.environ.get("CPDP_FULL_SEEDS", "42").split(",") if x]
-CASES = [("r50_100", "f32", "f32"), ("vit_s", "f32", "f32"), ("r50_200", "f32", "f32"),
-         ("stress", "f32", "f32")]
+ADAMW = dict(kind="adamw", lr=5e-4, momentum=0.9, beta2=0.999, eps=1e-8, weight_decay=0.05)
+CASES = [("r50_100", "f32", "f32", None), ("vit_s", "f32", "f32", None),
+         ("r50_200", "f32", "f32", None), ("stress", "f32", "f32", None),
+         ("vit_s", "f32", "f32", ADAMW)]
 if os.environ.get("CPDP_FULL_VARIANTS") == "1":
-    CASES += [("stress", "bf16", "f32"), ("stress", "bf16", "bf16")]
+    CASES += [("stress", "bf16", "f32", None), ("stress", "bf16", "bf16", None)]
+
+
+def _case_id(case) -> str:
+    name, g, m, opt = case
+    return f"{name}-adamw" if opt is not None else f"{name}-grads_{g}-mom_{m}"
 
 
 def _exact_f32(x64: np.ndarray) -> np.ndarray:
@@ -71,12 +81,20 @@ def _from_bits(bits: np.ndarray) -> np.ndarray:
 class CompactState:
     """The oracle state of all coordinates in its storage types."""
 
-    def __init__(self, W: int, P: int, param_dt: str, mom_dt: str = "f32"):
+    def __init__(self, W: int, P: int, param_dt: str, mom_dt: str = "f32", adamw: bool = False):
         self.W, self.param_dt, self.mom_dt = W, param_dt, mom_dt
         self.params = np.empty((W, P), dtype=np.uint16 if param_dt == "bf16" else np.float32)
         self.mom = np.empty((W, P), dtype=np.uint16 if mom_dt == "bf16" else np.float32)
         self.slow = np.empty(P, dtype=np.float32)
         self.anchor = np.empty(P, dtype=np.float32)
+        # AdamW's second moments (fp32 storage), kept beside the oracle state
+        self.mom2 = np.zeros((W, P), dtype=np.float32) if adamw else None
+
+    def load_mom2(self, lo: int, hi: int) -> np.ndarray:
+        return self.mom2[:, lo:hi].astype(np.float64)
+
+    def store_mom2(self, m2: np.ndarray, lo: int, hi: int) -> None:
+        self.mom2[:, lo:hi] = _exact_f32(m2)
 
     def load(self, lo: int, hi: int) -> oracle.OracleState:
         p = self.params[:, lo:hi]
@@ -98,15 +116,20 @@ class CompactState:
 
 
 @pytest.mark.parametrize("seed", SEEDS)
-@pytest.mark.parametrize("name,gdt,mdt", CASES, ids=[f"{n}-grads_{g}-mom_{m}" for n, g, m in CASES])
-def test_every_coordinate(name, gdt, mdt, seed):
+@pytest.mark.parametrize("name,gdt,mdt,opt", CASES, ids=[_case_id(x) for x in CASES])
+def test_every_coordinate(name, gdt, mdt, opt, seed):
     w = WORKLOADS[name]
     c = Case(W=w.W, P=w.P, K=w.K, lr=w.lr, mu=w.mu, beta=w.beta, alpha=w.alpha,
              steps=w.steps if WHOLE_RUN else w.K, param_dt=w.param_dt, ld=w.ld, seed=seed,
              theta_sigma=w.theta_sigma, grad_sigma=w.grad_sigma,
-             outlier_rate=w.outlier_rate, grad_dt=gdt, mom_dt=mdt)
+             outlier_rate=w.outlier_rate, grad_dt=gdt, mom_dt=mdt, opt=opt)
     P, W = c.P, c.W
     lr, mu, beta, alpha = c.hyper32()
+    o = c.opt32() if opt is not None else None
+    # the oracle's AdamW of 1-based global step s (its step count advances on
+    # every step), with the fp32 values of the hyperparameters
+    make_opt = (lambda s: oracle.adamw(o["lr"], o["momentum"], o["beta2"], o["eps"],
+                                       o["weight_decay"], s)) if o is not None else None
     rng = np.random.default_rng(0)
     sample = np.unique(np.concatenate([np.arange(64), P - 64 + np.arange(64),
                                        rng.integers(0, P, 4096)]))
@@ -119,7 +142,7 @@ def test_every_coordinate(name, gdt, mdt, seed):
                           gen.theta0(c.seed, sample, c.theta_sigma).view(np.uint32))
 
     slices = [(lo, min(P, lo + SLICE)) for lo in range(0, P, SLICE)]
-    ref = CompactState(W, P, c.param_dt, c.mom_dt)
+    ref = CompactState(W, P, c.param_dt, c.mom_dt, adamw=opt is not None)
     oracle.lib()  # load once before the worker threads call into it
 
     def init(sl):
@@ -149,7 +172,15 @@ def test_every_coordinate(name, gdt, mdt, seed):
                 g64 = g32.astype(np.float64)
                 del g32
                 st = ref.load(lo, hi)
-                if kind == "reconcile":
+                m2 = None
+                if make_opt is not None:
+                    m2 = ref.load_mom2(lo, hi)
+                    if kind == "reconcile":
+                        oracle.sync_opt(st, "cpdp", g64, make_opt(s), beta, alpha, m2)
+                    else:
+                        oracle.local_step_opt(st, g64, make_opt(s), m2)
+                    ref.store_mom2(m2, lo, hi)
+                elif kind == "reconcile":
                     oracle.reconcile(st, g64, lr, mu, beta, alpha)
                 else:
                     oracle.local_step(st, g64, lr, mu)
@@ -159,11 +190,18 @@ def test_every_coordinate(name, gdt, mdt, seed):
                         "mom": g.st.mom[:, lo:hi].float().cpu().numpy().astype(np.float64),
                         "slow_mom": g.st.slow_mom[lo:hi].cpu().numpy().astype(np.float64),
                         "anchor": g.st.anchor[lo:hi].cpu().numpy().astype(np.float64)}
+                if m2 is not None:
+                    snap["mom2"] = g.st.mom2[:, lo:hi].cpu().numpy().astype(np.float64)
                 tag = (f"{name} grads {c.grad_dt} mom {c.mom_dt} seed {c.seed} every coordinate, "
                        f"step {s} ({kind}), coordinates [{lo}, {hi})")
                 exc = []
-                m = compare(snap, st, tolerance_regime(c), tag, lr=lr,
-                            fp32_state=state_from_grads(None, c.mom_dt), exceptions=exc)
+                if o is not None:  # as run_parity gates AdamW (v = -lr u, scaled moments)
+                    m = compare(snap, st, tolerance_regime(c), tag, mom2=m2, scaled=True,
+                                velocity_lr=o["lr"], lr=o["lr"],
+                                fp32_state=state_from_grads(c.opt, c.mom_dt), exceptions=exc)
+                else:
+                    m = compare(snap, st, tolerance_regime(c), tag, lr=lr,
+                                fp32_state=state_from_grads(None, c.mom_dt), exceptions=exc)
                 for fam, row, col, got_v, want_v, r_tight, r_loose in exc:
                     log(f"[full-coords] {name} seed {c.seed} step {s}: tight-tier exception "
                         f"{fam} replica {row} coordinate {lo + col}: got {got_v!r} want "
@@ -177,7 +215,8 @@ def test_every_coordinate(name, gdt, mdt, seed):
             for m in pool.map(work, slices):
                 for k, v in m.items():
                     worst[k] = max(worst.get(k, 0.0), v)
-            log(f"[full-coords] {name} grads {c.grad_dt} mom {c.mom_dt} seed {c.seed} step {s} "
+            log(f"[full-coords] {name} {'adamw' if opt is not None else 'sgd'} grads {c.grad_dt} "
+                f"mom {c.mom_dt} seed {c.seed} step {s} "
                 f"{kind}: {W}x{P} coordinates match; worst "
                 f"error / tolerance " + ", ".join(f"{k} {v:.3g}" for k, v in worst.items()))
     assert kind == "reconcile"
