@@ -8,7 +8,8 @@ benchmark's launch configuration (longer runs on request, below):
   stress   W=32 bf16 replicas, P=10^8, fp32 gradients, momentum, u, anchor, K=4
 and vit_s once more with AdamW, the optimizer the paper trains ViT-S with
 (Table 3: lr 5e-4, betas 0.9 / 0.999, eps 1e-8, decoupled weight decay 0.05),
-second moments included.
+second moments included, and r50_100 under the paper's two baselines (Sec.
+5.3): the LocalSGD sync and the synchronous DDP step.
 
 Inputs come from the seeded generator: on the device for the HIP path, copied
 to the host for the oracle (the generator is the one module both sides share;
@@ -50,15 +51,19 @@ WORKERS = 12
 WHOLE_RUN = os.environ.get("CPDP_FULL_PERIODS", "1") == "all"
 SEEDS = [int(x) for x in os.environ.get("CPDP_FULL_SEEDS", "42").split(",") if x]
 ADAMW = dict(kind="adamw", lr=5e-4, momentum=0.9, beta2=0.999, eps=1e-8, weight_decay=0.05)
-CASES = [("r50_100", "f32", "f32", None), ("vit_s", "f32", "f32", None),
-         ("r50_200", "f32", "f32", None), ("stress", "f32", "f32", None),
-         ("vit_s", "f32", "f32", ADAMW)]
+# (workload, gradient storage, momentum storage, general optimizer, strategy)
+CASES = [("r50_100", "f32", "f32", None, "cpdp"), ("vit_s", "f32", "f32", None, "cpdp"),
+         ("r50_200", "f32", "f32", None, "cpdp"), ("stress", "f32", "f32", None, "cpdp"),
+         ("vit_s", "f32", "f32", ADAMW, "cpdp"), ("r50_100", "f32", "f32", None, "localsgd"),
+         ("r50_100", "f32", "f32", None, "ddp")]
 if os.environ.get("CPDP_FULL_VARIANTS") == "1":
-    CASES += [("stress", "bf16", "f32", None), ("stress", "bf16", "bf16", None)]
+    CASES += [("stress", "bf16", "f32", None, "cpdp"), ("stress", "bf16", "bf16", None, "cpdp")]
 
 
 def _case_id(case) -> str:
-    name, g, m, opt = case
+    name, g, m, opt, method = case
+    if method != "cpdp":
+        return f"{name}-{method}"
     return f"{name}-adamw" if opt is not None else f"{name}-grads_{g}-mom_{m}"
 
 
@@ -116,13 +121,13 @@ class CompactState:
 
 
 @pytest.mark.parametrize("seed", SEEDS)
-@pytest.mark.parametrize("name,gdt,mdt,opt", CASES, ids=[_case_id(x) for x in CASES])
-def test_every_coordinate(name, gdt, mdt, opt, seed):
+@pytest.mark.parametrize("name,gdt,mdt,opt,method", CASES, ids=[_case_id(x) for x in CASES])
+def test_every_coordinate(name, gdt, mdt, opt, method, seed):
     w = WORKLOADS[name]
     c = Case(W=w.W, P=w.P, K=w.K, lr=w.lr, mu=w.mu, beta=w.beta, alpha=w.alpha,
              steps=w.steps if WHOLE_RUN else w.K, param_dt=w.param_dt, ld=w.ld, seed=seed,
              theta_sigma=w.theta_sigma, grad_sigma=w.grad_sigma,
-             outlier_rate=w.outlier_rate, grad_dt=gdt, mom_dt=mdt, opt=opt)
+             outlier_rate=w.outlier_rate, grad_dt=gdt, mom_dt=mdt, opt=opt, method=method)
     P, W = c.P, c.W
     lr, mu, beta, alpha = c.hyper32()
     o = c.opt32() if opt is not None else None
@@ -180,6 +185,10 @@ def test_every_coordinate(name, gdt, mdt, opt, seed):
                     else:
                         oracle.local_step_opt(st, g64, make_opt(s), m2)
                     ref.store_mom2(m2, lo, hi)
+                elif kind == "reconcile" and method == "localsgd":
+                    oracle.localsgd_sync(st, g64, lr, mu)
+                elif kind == "reconcile" and method == "ddp":
+                    oracle.ddp_step(st, g64, lr, mu)
                 elif kind == "reconcile":
                     oracle.reconcile(st, g64, lr, mu, beta, alpha)
                 else:
@@ -192,7 +201,7 @@ def test_every_coordinate(name, gdt, mdt, opt, seed):
                         "anchor": g.st.anchor[lo:hi].cpu().numpy().astype(np.float64)}
                 if m2 is not None:
                     snap["mom2"] = g.st.mom2[:, lo:hi].cpu().numpy().astype(np.float64)
-                tag = (f"{name} grads {c.grad_dt} mom {c.mom_dt} seed {c.seed} every coordinate, "
+                tag = (f"{name} {method} grads {c.grad_dt} mom {c.mom_dt} seed {c.seed} every coordinate, "
                        f"step {s} ({kind}), coordinates [{lo}, {hi})")
                 exc = []
                 if o is not None:  # as run_parity gates AdamW (v = -lr u, scaled moments)
@@ -207,7 +216,11 @@ def test_every_coordinate(name, gdt, mdt, opt, seed):
                         f"{fam} replica {row} coordinate {lo + col}: got {got_v!r} want "
                         f"{want_v!r} ({r_tight:.3f} of the tight limit, {r_loose:.3f} of the "
                         f"loose one)")
-                if kind == "reconcile":
+                if kind == "reconcile" and method == "ddp":
+                    # identical replicas stepped with the same mean gradient stay identical
+                    p = snap["params"]
+                    assert (p == p[0:1]).all(), f"{tag}: DDP replicas differ"
+                elif kind == "reconcile":
                     check_replicas_reconciled(snap, c.param_dt, tag)
                 return m
 
@@ -215,7 +228,7 @@ def test_every_coordinate(name, gdt, mdt, opt, seed):
             for m in pool.map(work, slices):
                 for k, v in m.items():
                     worst[k] = max(worst.get(k, 0.0), v)
-            log(f"[full-coords] {name} {'adamw' if opt is not None else 'sgd'} grads {c.grad_dt} "
+            log(f"[full-coords] {name} {method} {'adamw' if opt is not None else 'sgd'} grads {c.grad_dt} "
                 f"mom {c.mom_dt} seed {c.seed} step {s} "
                 f"{kind}: {W}x{P} coordinates match; worst "
                 f"error / tolerance " + ", ".join(f"{k} {v:.3g}" for k, v in worst.items()))
