@@ -8,8 +8,10 @@ benchmark's launch configuration (longer runs on request, below):
   stress   W=32 bf16 replicas, P=10^8, fp32 gradients, momentum, u, anchor, K=4
 and vit_s once more with AdamW, the optimizer the paper trains ViT-S with
 (Table 3: lr 5e-4, betas 0.9 / 0.999, eps 1e-8, decoupled weight decay 0.05),
-second moments included, and r50_100 under the paper's two baselines (Sec.
-5.3): the LocalSGD sync and the synchronous DDP step.
+second moments included, r50_100 with the paper's ResNet optimizer (momentum
+SGD with weight decay 5e-4, Table 3) through the general-optimizer path, and
+r50_100 under the paper's two baselines (Sec. 5.3): the LocalSGD sync and the
+synchronous DDP step.
 
 Inputs come from the seeded generator: on the device for the HIP path, copied
 to the host for the oracle (the generator is the one module both sides share;
@@ -51,10 +53,12 @@ WORKERS = 12
 WHOLE_RUN = os.environ.get("CPDP_FULL_PERIODS", "1") == "all"
 SEEDS = [int(x) for x in os.environ.get("CPDP_FULL_SEEDS", "42").split(",") if x]
 ADAMW = dict(kind="adamw", lr=5e-4, momentum=0.9, beta2=0.999, eps=1e-8, weight_decay=0.05)
+SGD_WD = dict(kind="sgd", lr=0.1, momentum=0.9, weight_decay=5e-4)
 # (workload, gradient storage, momentum storage, general optimizer, strategy)
 CASES = [("r50_100", "f32", "f32", None, "cpdp"), ("vit_s", "f32", "f32", None, "cpdp"),
          ("r50_200", "f32", "f32", None, "cpdp"), ("stress", "f32", "f32", None, "cpdp"),
-         ("vit_s", "f32", "f32", ADAMW, "cpdp"), ("r50_100", "f32", "f32", None, "localsgd"),
+         ("vit_s", "f32", "f32", ADAMW, "cpdp"), ("r50_100", "f32", "f32", SGD_WD, "cpdp"),
+         ("r50_100", "f32", "f32", None, "localsgd"),
          ("r50_100", "f32", "f32", None, "ddp")]
 if os.environ.get("CPDP_FULL_VARIANTS") == "1":
     CASES += [("stress", "bf16", "f32", None, "cpdp"), ("stress", "bf16", "bf16", None, "cpdp")]
@@ -64,7 +68,9 @@ def _case_id(case) -> str:
     name, g, m, opt, method = case
     if method != "cpdp":
         return f"{name}-{method}"
-    return f"{name}-adamw" if opt is not None else f"{name}-grads_{g}-mom_{m}"
+    if opt is not None:
+        return f"{name}-{'adamw' if opt['kind'] == 'adamw' else 'sgd_wd'}"
+    return f"{name}-grads_{g}-mom_{m}"
 
 
 def _exact_f32(x64: np.ndarray) -> np.ndarray:
@@ -131,10 +137,15 @@ def test_every_coordinate(name, gdt, mdt, opt, method, seed):
     P, W = c.P, c.W
     lr, mu, beta, alpha = c.hyper32()
     o = c.opt32() if opt is not None else None
-    # the oracle's AdamW of 1-based global step s (its step count advances on
-    # every step), with the fp32 values of the hyperparameters
-    make_opt = (lambda s: oracle.adamw(o["lr"], o["momentum"], o["beta2"], o["eps"],
-                                       o["weight_decay"], s)) if o is not None else None
+    # the oracle's optimizer of 1-based global step s (AdamW's step count
+    # advances on every step), with the fp32 values of the hyperparameters
+    make_opt = None
+    if o is not None and o["kind"] == "adamw":
+        make_opt = lambda s: oracle.adamw(o["lr"], o["momentum"], o["beta2"], o["eps"],  # noqa: E731
+                                          o["weight_decay"], s)
+    elif o is not None:
+        make_opt = lambda s: oracle.sgd(o["lr"], o["momentum"], o["weight_decay"])  # noqa: E731
+    adamw = o is not None and o["kind"] == "adamw"
     rng = np.random.default_rng(0)
     sample = np.unique(np.concatenate([np.arange(64), P - 64 + np.arange(64),
                                        rng.integers(0, P, 4096)]))
@@ -147,7 +158,7 @@ def test_every_coordinate(name, gdt, mdt, opt, method, seed):
                           gen.theta0(c.seed, sample, c.theta_sigma).view(np.uint32))
 
     slices = [(lo, min(P, lo + SLICE)) for lo in range(0, P, SLICE)]
-    ref = CompactState(W, P, c.param_dt, c.mom_dt, adamw=opt is not None)
+    ref = CompactState(W, P, c.param_dt, c.mom_dt, adamw=adamw)
     oracle.lib()  # load once before the worker threads call into it
 
     def init(sl):
@@ -179,12 +190,13 @@ def test_every_coordinate(name, gdt, mdt, opt, method, seed):
                 st = ref.load(lo, hi)
                 m2 = None
                 if make_opt is not None:
-                    m2 = ref.load_mom2(lo, hi)
+                    m2 = ref.load_mom2(lo, hi) if adamw else None
                     if kind == "reconcile":
                         oracle.sync_opt(st, "cpdp", g64, make_opt(s), beta, alpha, m2)
                     else:
                         oracle.local_step_opt(st, g64, make_opt(s), m2)
-                    ref.store_mom2(m2, lo, hi)
+                    if adamw:
+                        ref.store_mom2(m2, lo, hi)
                 elif kind == "reconcile" and method == "localsgd":
                     oracle.localsgd_sync(st, g64, lr, mu)
                 elif kind == "reconcile" and method == "ddp":
@@ -204,9 +216,9 @@ def test_every_coordinate(name, gdt, mdt, opt, method, seed):
                 tag = (f"{name} {method} grads {c.grad_dt} mom {c.mom_dt} seed {c.seed} every coordinate, "
                        f"step {s} ({kind}), coordinates [{lo}, {hi})")
                 exc = []
-                if o is not None:  # as run_parity gates AdamW (v = -lr u, scaled moments)
+                if o is not None:  # as run_parity gates the general optimizers
                     m = compare(snap, st, tolerance_regime(c), tag, mom2=m2, scaled=True,
-                                velocity_lr=o["lr"], lr=o["lr"],
+                                velocity_lr=o["lr"] if adamw else None, lr=o["lr"],
                                 fp32_state=state_from_grads(c.opt, c.mom_dt), exceptions=exc)
                 else:
                     m = compare(snap, st, tolerance_regime(c), tag, lr=lr,
@@ -228,7 +240,8 @@ def test_every_coordinate(name, gdt, mdt, opt, method, seed):
             for m in pool.map(work, slices):
                 for k, v in m.items():
                     worst[k] = max(worst.get(k, 0.0), v)
-            log(f"[full-coords] {name} {method} {'adamw' if opt is not None else 'sgd'} grads {c.grad_dt} "
+            log(f"[full-coords] {name} {method} {o['kind'] if o is not None else 'sgd'}"
+                f"{'+wd' if o is not None and o['kind'] == 'sgd' else ''} grads {c.grad_dt} "
                 f"mom {c.mom_dt} seed {c.seed} step {s} "
                 f"{kind}: {W}x{P} coordinates match; worst "
                 f"error / tolerance " + ", ".join(f"{k} {v:.3g}" for k, v in worst.items()))
